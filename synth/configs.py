@@ -1,0 +1,74 @@
+"""The five workload shapes of the lifelong-sequence NN-select + encode path.
+
+Each shape follows the paper's scales: a lifelong sequence of O(10^4) actions
+(Sec. 3.2.2, after Eq. 3), a selected sequence of O(10^2) tokens, and thousands
+of candidate items per ranking request (Sec. 1).  The encoder sizes are fixed
+per workload (the paper's own production encoder, d_model 64 / 1 head / FFN 32 /
+2 layers of Sec. 3.2.2, is smaller than all but the tiny workload).
+
+This module holds shapes only: no arithmetic of the method.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Optional, Tuple
+
+
+@dataclass(frozen=True)
+class Workload:
+    cid: int                      # 1..5, also the data seed
+    name: str
+    dtype: str                    # "f32" or "bf16": storage and MFMA operand type
+    R: int                        # requests (users) in one batch
+    L: Optional[int]              # lifelong length per request (fixed), or None
+    L_range: Optional[Tuple[int, int]]  # inclusive [lo, hi] when ragged
+    d: int                        # embedding width of actions and candidates
+    N: int                        # candidates per request
+    k: int                        # NN top-k over the lifelong sequence
+    d_model: int
+    n_heads: int
+    d_ffn: int
+    n_layers: int
+    has_time: bool                # time-bucket feature present
+    rt_len: int = 0               # real-time actions appended after the NN tokens
+    tie_frac: float = 0.0         # fraction of rows overwritten with another row's embedding
+
+    @property
+    def T(self) -> int:
+        """Encoder positions: k NN tokens plus the real-time tail."""
+        return self.k + self.rt_len
+
+    @property
+    def total_candidates(self) -> int:
+        return self.R * self.N
+
+    @property
+    def data_seed(self) -> int:
+        return self.cid
+
+    @property
+    def weight_seed(self) -> int:
+        return 100 + self.cid
+
+
+TINY = Workload(1, "tiny_f32", "f32", R=1, L=1024, L_range=None, d=64, N=16, k=32,
+                d_model=64, n_heads=2, d_ffn=128, n_layers=1, has_time=False)
+SINGLE = Workload(2, "single_bf16", "bf16", R=1, L=16384, L_range=None, d=256, N=1000,
+                  k=256, d_model=256, n_heads=4, d_ffn=1024, n_layers=2, has_time=True)
+RAGGED = Workload(3, "ragged_bf16", "bf16", R=64, L=None, L_range=(1024, 16384), d=256,
+                  N=500, k=128, d_model=256, n_heads=4, d_ffn=512, n_layers=2, has_time=True)
+MIXED = Workload(4, "mixed_bf16", "bf16", R=1, L=16384, L_range=None, d=256, N=1000,
+                 k=256, d_model=256, n_heads=4, d_ffn=1024, n_layers=2, has_time=True,
+                 rt_len=100)
+STRESS = Workload(5, "stress_bf16", "bf16", R=16, L=16384, L_range=None, d=256, N=4000,
+                  k=512, d_model=256, n_heads=8, d_ffn=1024, n_layers=2, has_time=True,
+                  tie_frac=0.01)
+
+WORKLOADS = {w.cid: w for w in (TINY, SINGLE, RAGGED, MIXED, STRESS)}
+BY_NAME = {w.name: w for w in WORKLOADS.values()}
+
+
+def scaled(w: Workload, **changes) -> Workload:
+    """A copy of `w` with some fields replaced (small parity cases)."""
+    from dataclasses import replace
+    return replace(w, **changes)

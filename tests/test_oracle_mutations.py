@@ -1,0 +1,109 @@
+"""The oracle's pins must fail on plausible mistakes.
+
+Each test plants one mistake in the oracle (on the CPU, by patching the oracle's
+module for the duration of the test) and checks that a pin from
+test_oracle_select.py / test_oracle_encoder.py then fails.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import oracle.encoder  # noqa: F401  (registers the submodules)
+
+enc = sys.modules["oracle.encoder"]
+sel = sys.modules["oracle.nn_select"]
+
+import test_oracle_encoder as te  # noqa: E402
+import test_oracle_select as ts  # noqa: E402
+
+
+def _fails(fn, *args, **kw):
+    with pytest.raises(AssertionError):
+        fn(*args, **kw)
+
+
+def test_reversed_tie_break_is_caught(monkeypatch):
+    def newest_first_among_ties(s):
+        # ties ordered by descending index instead of ascending
+        flipped = np.argsort(-s[:, ::-1], axis=1, kind="stable")
+        return s.shape[1] - 1 - flipped
+
+    monkeypatch.setattr(sel, "rank_order", newest_first_among_ties)
+    _fails(ts.test_hand_worked_example)
+
+
+def test_wrong_token_order_is_caught(monkeypatch):
+    monkeypatch.setattr(sel, "token_positions", lambda idx_row: idx_row[idx_row >= 0].copy())
+    _fails(ts.test_gather_places_rank_order_reversed_then_realtime_oldest_first)
+
+
+def test_wrong_layer_norm_eps_is_caught(monkeypatch):
+    monkeypatch.setattr(enc, "LN_EPS", 1e-6)
+    monkeypatch.setattr(enc.layer_norm, "__defaults__", (1e-6,))
+    _fails(te.test_layers_match_torch_transformer_encoder_layer, 2, 12)
+
+
+def test_mask_off_by_one_is_caught(monkeypatch):
+    def leaky(q, k, v):
+        T, dh = q.shape[-2], q.shape[-1]
+        s = q @ np.swapaxes(k, -1, -2) / np.sqrt(dh)
+        s = np.where(np.triu(np.ones((T, T), dtype=bool), k=2), -np.inf, s)  # sees one future key
+        s = s - s.max(axis=-1, keepdims=True)
+        p = np.exp(s)
+        return (p / p.sum(axis=-1, keepdims=True)) @ v
+
+    monkeypatch.setattr(enc, "causal_attention", leaky)
+    _fails(te.test_causal_prefix_invariance)
+    _fails(te.test_layers_match_torch_transformer_encoder_layer, 2, 12)
+
+
+def test_missing_output_bias_is_caught(monkeypatch):
+    real = enc.encoder_layer
+
+    def no_bo(X, Lw, n_heads):
+        import copy
+        L2 = copy.copy(Lw)
+        L2.b_o = np.zeros_like(Lw.b_o)
+        return real(X, L2, n_heads)
+
+    monkeypatch.setattr(enc, "encoder_layer", no_bo)
+    _fails(te.test_layers_match_torch_transformer_encoder_layer, 2, 12)
+
+
+def test_swapped_concat_is_caught(monkeypatch):
+    real = enc.feature_encode
+
+    def swapped(tok_emb, tok_act, tok_time, cand, W):
+        import copy
+        d = np.asarray(tok_emb).shape[-1]
+        W2 = copy.copy(W)
+        W2.W_in = np.concatenate([W.W_in[:, d:], W.W_in[:, :d]], axis=1)
+        return real(tok_emb, tok_act, tok_time, cand, W2)
+
+    monkeypatch.setattr(enc, "feature_encode", swapped)
+    monkeypatch.setattr(oracle, "feature_encode", swapped)
+    _fails(te.test_feature_encoding_reduces_to_eq4_with_identity_projection)
+
+
+def test_transposed_ffn_weight_is_caught(monkeypatch):
+    real = enc.encoder_layer
+
+    def transposed(X, Lw, n_heads):
+        import copy
+        L2 = copy.copy(Lw)
+        L2.W_o = Lw.W_o.T.copy()
+        return real(X, L2, n_heads)
+
+    monkeypatch.setattr(enc, "encoder_layer", transposed)
+    _fails(te.test_layers_match_torch_transformer_encoder_layer, 2, 12)
+
+
+def test_pool_on_wrong_token_is_caught(monkeypatch):
+    def first_token(X, W):
+        y = X @ np.asarray(W.W_pool, np.float64).T + W.b_pool
+        return np.concatenate([y.max(axis=1), X[:, 0, :]], axis=-1)
+
+    monkeypatch.setattr(enc, "pool", first_token)
+    _fails(te.test_pool_properties_and_valid_length_groups)
