@@ -1,0 +1,225 @@
+/*
+ * tav2.h - C ABI of the lifelong-sequence NN-select + encode library (gfx950).
+ *
+ * The library computes, for every candidate item of a ranking request, the
+ * serving hot path of TransAct V2's lifelong user-sequence module
+ * (Xia et al., "TransAct V2: Lifelong User Action Sequence Modeling on
+ * Pinterest Recommendation"):
+ *   1. candidate-anchored nearest-neighbour search over the user's lifelong
+ *      action sequence (Eq. 3, Sec. 3.2.2): dot-product scores of every action
+ *      row against the candidate embedding and the top-k rows;
+ *   2. the selected rows (plus, optionally, the kept most-recent real-time
+ *      actions of Eq. 2) gathered into a token sequence;
+ *   3. feature encoding with early fusion of the candidate embedding
+ *      (Eq. 4), a causal transformer encoder, and a linear + max-pool head
+ *      (Sec. 3.2.2, 'Transformer Encoder').
+ * The request-level sequence is stored once per request and shared by all of
+ * its candidates (the de-duplicated request-level format of Sec. 3.4.2,
+ * 'Request Level De-duplication').
+ *
+ * Conventions shared by every entry point:
+ *   - Pointers documented as "device" are HIP device pointers (or managed /
+ *     host-pinned memory the GPU can read).  Pointers documented as "host" are
+ *     read by the CPU during the call.  The caller owns every buffer, including
+ *     outputs and the workspace; the library never allocates, frees or
+ *     synchronises.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *     work is enqueued on it; the call returns before the GPU finishes.
+ *   - Argument errors are detected on the host before anything is enqueued and
+ *     return a negative status; nothing is launched in that case.  A launch
+ *     failure returns TAV2_ERR_HIP.  Faults during execution surface at the
+ *     caller's next synchronisation.
+ *   - Calls are stateless; concurrent calls are safe when they use distinct
+ *     outputs and workspaces.
+ *   - Sequences are stored most-recent-first: row 0 of a request is its newest
+ *     action.  Among equal scores, the more recent row (lower index) ranks
+ *     first, so the selection order is the total order
+ *     (score descending, row index ascending).  -0.0 and +0.0 are one score;
+ *     reported zero scores are +0.0.
+ *   - Matrices use the [out_features, in_features] row-major layout
+ *     (y = x W^T + b).
+ */
+#ifndef TAV2_H
+#define TAV2_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t tav2_status;
+#define TAV2_OK               0
+#define TAV2_ERR_NULL        -1   /* a required pointer is NULL */
+#define TAV2_ERR_SHAPE       -2   /* a size is out of range or inconsistent */
+#define TAV2_ERR_DTYPE       -3   /* unknown dtype, or dtypes that do not match */
+#define TAV2_ERR_UNSUPPORTED -4   /* a valid request this build does not implement */
+#define TAV2_ERR_WORKSPACE   -5   /* workspace NULL or smaller than the query says */
+#define TAV2_ERR_HIP         -6   /* a HIP launch failed */
+
+#define TAV2_F32  0   /* float32 storage and arithmetic */
+#define TAV2_BF16 1   /* bfloat16 storage, fp32 accumulation */
+
+#define TAV2_K_MAX     1024  /* largest k of the NN search */
+#define TAV2_T_MAX     1024  /* largest encoder sequence (k + real-time tail) */
+#define TAV2_N_ACT        8  /* action types: values in [0, 8) */
+#define TAV2_N_TIME      64  /* time buckets: values in [0, 64) */
+
+/*
+ * A de-duplicated request-level action sequence batch (Sec. 3.4.2, 'Request
+ * Level De-duplication'): the rows of all R requests are stored once; request r
+ * owns rows [offset[r], offset[r] + len[r]).  Packed (offset = prefix sum of
+ * len) and fixed-stride padded layouts are both valid.
+ */
+typedef struct tav2_seq {
+  const void*    emb;          /* device [rows, d], dtype; values finite */
+  const uint8_t* action_type;  /* device [rows], values in [0, 8) */
+  const uint8_t* time_bucket;  /* device [rows], values in [0, 64), or NULL (no time feature) */
+  const int64_t* offset;       /* device [R]: first row of each request */
+  const int32_t* len;          /* device [R]: rows of each request, 0 <= len[r] <= max_len */
+  int32_t num_requests;        /* R >= 0 */
+  int32_t d;                   /* embedding width, multiple of 8, 8..512 */
+  int32_t dtype;               /* TAV2_F32 or TAV2_BF16 */
+  int32_t max_len;             /* host-side bound: len[r] <= max_len for every r */
+} tav2_seq;
+
+/* The candidate items of the same R requests, stored contiguously by request. */
+typedef struct tav2_cands {
+  const void*    emb;          /* device [total, d], same dtype and d as the sequence */
+  const int64_t* offset;       /* device [R + 1]: candidates of request r are
+                                  [offset[r], offset[r+1]); offset[0] = 0, offset[R] = total */
+  int64_t total;               /* host: number of candidates (>= 0) */
+  int32_t max_count;           /* host-side bound: offset[r+1]-offset[r] <= max_count */
+  int32_t reserved;            /* set to 0 */
+} tav2_cands;
+
+/* Explicit gathered tokens in encoder order (what tav2_gather writes). */
+typedef struct tav2_tokens {
+  const void*    emb;          /* device [total, T, d], dtype */
+  const uint8_t* action_type;  /* device [total, T] */
+  const uint8_t* time_bucket;  /* device [total, T], or NULL when the weights have no time table */
+  const int32_t* valid_len;    /* device [total]: tokens [0, valid_len) are real, 0 <= valid_len <= T */
+  int64_t total;               /* host: number of candidates */
+  int32_t T;                   /* positions per candidate, 1..TAV2_T_MAX */
+  int32_t d;                   /* token embedding width */
+  int32_t dtype;               /* TAV2_F32 or TAV2_BF16 */
+  int32_t reserved;            /* set to 0 */
+} tav2_tokens;
+
+/* One post-LayerNorm encoder layer.  Matrices in the weights' dtype,
+ * vectors (biases, LayerNorm gain/offset) always float32.  Device pointers. */
+typedef struct tav2_layer {
+  const void*  W_qkv;  const float* b_qkv;   /* [3 dm, dm]: rows q | k | v; [3 dm] */
+  const void*  W_o;    const float* b_o;     /* [dm, dm]; [dm] */
+  const float* ln1_g;  const float* ln1_b;   /* [dm] */
+  const void*  W_1;    const float* b_1;     /* [d_ffn, dm]; [d_ffn] */
+  const void*  W_2;    const float* b_2;     /* [dm, d_ffn]; [dm] */
+  const float* ln2_g;  const float* ln2_b;   /* [dm] */
+} tav2_layer;
+
+/*
+ * Encoder weights.  Feature encoding (Eq. 4 with early fusion): the token's
+ * embedding e_p and the candidate's e_c are concatenated and projected,
+ *   x_p = [e_p ; e_c] W_in^T + b_in + E_act[a_p] + E_time[t_p] + E_pos[p],
+ * which is Eq. 4 exactly when dm = 2 d and W_in = I.  Each layer:
+ *   X <- LN1(X + MHA_causal(X) W_o^T + b_o);  X <- LN2(X + ReLU(X W_1^T + b_1) W_2^T + b_2)
+ * with per-head scale 1/sqrt(dm / n_heads) and LayerNorm eps 1e-5.
+ */
+typedef struct tav2_weights {
+  int32_t d_in;                /* token / candidate embedding width d */
+  int32_t d_model;             /* dm */
+  int32_t n_heads;             /* dm % n_heads == 0 */
+  int32_t d_ffn;
+  int32_t n_layers;            /* >= 1 */
+  int32_t max_pos;             /* rows of E_pos, >= the encoder sequence length T */
+  int32_t dtype;               /* TAV2_F32 or TAV2_BF16 */
+  int32_t reserved;            /* set to 0 */
+  const void*  W_in;  const float* b_in;     /* device [dm, 2 d] (token columns first); [dm] */
+  const void*  E_act;                        /* device [8, dm] */
+  const void*  E_time;                       /* device [64, dm], or NULL (no time feature) */
+  const void*  E_pos;                        /* device [max_pos, dm] */
+  const tav2_layer* layers;                  /* HOST array of n_layers layer records */
+  const void*  W_pool; const float* b_pool;  /* device [dm, dm]; [dm] */
+} tav2_weights;
+
+/* Human-readable text of a status code (static storage). */
+const char* tav2_status_string(tav2_status s);
+
+/* Version of the library's ABI (monotonically increasing). */
+int32_t tav2_abi_version(void);
+
+/*
+ * NN search (Eq. 3): for every candidate n of request r, the k rows i of
+ * request r with the largest score s[n, i] = <emb[offset[r] + i], cand[n]>,
+ * in the order (score desc, row asc).
+ *   out_idx   device [total, k] int32: row index within the request; -1 when
+ *             k > len[r] (positions >= len[r]).
+ *   out_score device [total, k] float32: the scores (fp32 accumulation; exact
+ *             whenever the fp32 sum is exact), -inf in padded positions.
+ *   ws        device workspace of at least tav2_nn_select_workspace() bytes,
+ *             256-byte aligned.
+ * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE (k < 1 or k > TAV2_K_MAX, d, counts),
+ * TAV2_ERR_DTYPE, TAV2_ERR_WORKSPACE, TAV2_ERR_HIP.
+ */
+size_t tav2_nn_select_workspace(const tav2_seq* seq, const tav2_cands* cands, int32_t k);
+tav2_status tav2_nn_select(const tav2_seq* seq, const tav2_cands* cands, int32_t k,
+                           int32_t* out_idx, float* out_score,
+                           void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Token assembly for the encoder (Eq. 2 restricted to NN(S_LL, c) and the kept
+ * most-recent real-time actions S_RT[:r]).  For candidate n with T_LL valid
+ * entries in idx[n] (entries >= 0, rank order as tav2_nn_select writes them),
+ * position p < T_LL holds sequence row idx[n][T_LL - 1 - p] (ascending score,
+ * best match last, as Eq. 3's ascending argsort returns them); positions
+ * T_LL .. T_LL + len_rt[r] - 1 hold the request's real-time rows oldest first;
+ * later positions are zero.
+ *   rt        NULL, or a real-time sequence batch with the same R, d and dtype.
+ *   tok_*     device outputs [total, T, d], [total, T], [total, T]
+ *             (tok_time may be NULL), with T = k + (rt ? rt->max_len : 0).
+ *   valid_len device [total] int32 output.
+ * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_DTYPE, TAV2_ERR_HIP.
+ */
+tav2_status tav2_gather(const tav2_seq* seq, const tav2_seq* rt, const tav2_cands* cands,
+                        const int32_t* idx, int32_t k,
+                        void* tok_emb, uint8_t* tok_act, uint8_t* tok_time,
+                        int32_t* valid_len, void* stream);
+
+/*
+ * Encoder + head over explicit tokens (Eq. 4, Sec. 3.2.2):
+ *   out device [total, 2 dm] float32:
+ *     out[n, 0:dm]    = max over p < valid_len[n] of (X_p W_pool^T + b_pool)
+ *     out[n, dm:2dm]  = X_{valid_len[n]-1}
+ *   where X is the last layer's output under a causal mask; rows with
+ *   valid_len = 0 are zero.
+ *   cand_emb device [total, d] (the tokens' dtype).
+ * Supported shapes: bf16 with dm == 256, dm / n_heads in {32, 64},
+ * d_ffn a multiple of 256 up to 4096, d a multiple of 32 up to 512; float32
+ * with dm <= 128, d_ffn <= 512, T <= 64 and d <= 256.
+ * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_DTYPE, TAV2_ERR_UNSUPPORTED,
+ * TAV2_ERR_WORKSPACE, TAV2_ERR_HIP.
+ */
+size_t tav2_encode_workspace(const tav2_tokens* tok, const tav2_weights* w);
+tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2_weights* w,
+                        float* out, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * The whole path for a request batch: NN search, token assembly and encoder in
+ * one call; out_idx / out_score / out as in the calls above (out_idx and
+ * out_score may not be NULL: the encoder reads the selection from them).
+ * T = k + (rt ? rt->max_len : 0) must not exceed w->max_pos.
+ */
+size_t tav2_select_encode_workspace(const tav2_seq* seq, const tav2_seq* rt,
+                                    const tav2_cands* cands, int32_t k,
+                                    const tav2_weights* w);
+tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt,
+                               const tav2_cands* cands, int32_t k, const tav2_weights* w,
+                               int32_t* out_idx, float* out_score, float* out,
+                               void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TAV2_H */

@@ -1,0 +1,272 @@
+// C ABI of the NN-select + encode library: host-side argument validation,
+// workspace carving and kernel launches.  No allocation, no synchronisation.
+#include <string.h>
+
+#include "common.h"
+#include "internal.h"
+
+using namespace tav2;
+
+namespace {
+
+constexpr int32_t ABI_VERSION = 1;
+constexpr size_t WS_ALIGN = 256;
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+tav2_status hip_status(hipError_t e) { return e == hipSuccess ? TAV2_OK : TAV2_ERR_HIP; }
+
+size_t elem_size(int32_t dtype) { return dtype == TAV2_BF16 ? 2 : 4; }
+
+tav2_status check_dtype(int32_t dt) {
+  return (dt == TAV2_F32 || dt == TAV2_BF16) ? TAV2_OK : TAV2_ERR_DTYPE;
+}
+
+// A sequence batch.  `for_select` adds the limits of the NN search kernels.
+tav2_status check_seq(const tav2_seq* s, bool for_select) {
+  if (!s) return TAV2_ERR_NULL;
+  tav2_status st = check_dtype(s->dtype);
+  if (st) return st;
+  if (s->num_requests < 0 || s->max_len < 0) return TAV2_ERR_SHAPE;
+  if (s->d < 16 || s->d > 512 || s->d % 16) return TAV2_ERR_SHAPE;
+  if (for_select && s->max_len > SEL_MAX_LEN) return TAV2_ERR_UNSUPPORTED;
+  if (s->num_requests > 0) {
+    if (!s->offset || !s->len || !s->action_type) return TAV2_ERR_NULL;
+    if (s->max_len > 0 && !s->emb) return TAV2_ERR_NULL;
+    if (s->emb && !aligned(s->emb, 16)) return TAV2_ERR_SHAPE;
+  }
+  return TAV2_OK;
+}
+
+tav2_status check_cands(const tav2_cands* c, const tav2_seq* s) {
+  if (!c) return TAV2_ERR_NULL;
+  if (c->total < 0 || c->max_count < 0 || c->max_count > c->total) return TAV2_ERR_SHAPE;
+  if (c->total > 0 && c->max_count == 0) return TAV2_ERR_SHAPE;
+  if (c->total > 0 && s->num_requests == 0) return TAV2_ERR_SHAPE;
+  if (c->total > (int64_t(1) << 31) - 1 || c->max_count > 65535) return TAV2_ERR_UNSUPPORTED;
+  if (s->num_requests > 65535) return TAV2_ERR_UNSUPPORTED;
+  if (s->num_requests > 0 && !c->offset) return TAV2_ERR_NULL;
+  if (c->total > 0) {
+    if (!c->emb) return TAV2_ERR_NULL;
+    if (!aligned(c->emb, 16)) return TAV2_ERR_SHAPE;
+  }
+  return TAV2_OK;
+}
+
+tav2_status check_k(int32_t k) { return (k >= 1 && k <= TAV2_K_MAX) ? TAV2_OK : TAV2_ERR_SHAPE; }
+
+bool vec_ok(const float* p) { return p && aligned(p, 16); }
+
+// Weights for an encoder over T positions of width-d tokens; has_time says
+// whether the tokens carry a time bucket.
+tav2_status check_weights(const tav2_weights* w, int d, int dtype, int T, bool has_time) {
+  if (!w) return TAV2_ERR_NULL;
+  if (w->dtype != dtype) return TAV2_ERR_DTYPE;
+  if (w->d_in != d) return TAV2_ERR_SHAPE;
+  if (w->d_model < 1 || w->n_heads < 1 || w->d_model % w->n_heads || w->d_ffn < 1 ||
+      w->n_layers < 1)
+    return TAV2_ERR_SHAPE;
+  if (T < 1 || T > TAV2_T_MAX || w->max_pos < T) return TAV2_ERR_SHAPE;
+  if (!w->W_in || !w->E_act || !w->E_pos || !w->W_pool || !w->layers) return TAV2_ERR_NULL;
+  if (!vec_ok(w->b_in) || !vec_ok(w->b_pool)) return w->b_in && w->b_pool ? TAV2_ERR_SHAPE : TAV2_ERR_NULL;
+  if ((w->E_time != nullptr) != has_time) return TAV2_ERR_SHAPE;
+  for (int i = 0; i < w->n_layers; ++i) {
+    const tav2_layer& L = w->layers[i];
+    if (!L.W_qkv || !L.W_o || !L.W_1 || !L.W_2) return TAV2_ERR_NULL;
+    const float* v[] = {L.b_qkv, L.b_o, L.ln1_g, L.ln1_b, L.b_1, L.b_2, L.ln2_g, L.ln2_b};
+    for (const float* p : v) {
+      if (!p) return TAV2_ERR_NULL;
+      if (!aligned(p, 16)) return TAV2_ERR_SHAPE;
+    }
+  }
+  const int dh = w->d_model / w->n_heads;
+  if (dtype == TAV2_BF16) {
+    if (w->d_model != 256 || (dh != 32 && dh != 64)) return TAV2_ERR_UNSUPPORTED;
+    if (w->d_ffn % 256 || w->d_ffn > 4096) return TAV2_ERR_UNSUPPORTED;
+    if (d % 32) return TAV2_ERR_UNSUPPORTED;
+  } else {
+    if (!encode_f32_fits(T, *w) || d > 256) return TAV2_ERR_UNSUPPORTED;
+  }
+  return TAV2_OK;
+}
+
+tav2_status check_ws(const void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return TAV2_OK;
+  if (!ws || ws_bytes < need) return TAV2_ERR_WORKSPACE;
+  if (!aligned(ws, WS_ALIGN)) return TAV2_ERR_WORKSPACE;
+  return TAV2_OK;
+}
+
+int rt_len_max(const tav2_seq* rt) { return rt ? rt->max_len : 0; }
+
+tav2_status check_rt(const tav2_seq* rt, const tav2_seq* seq) {
+  if (!rt) return TAV2_OK;
+  tav2_status st = check_seq(rt, false);
+  if (st) return st;
+  if (rt->num_requests != seq->num_requests || rt->d != seq->d) return TAV2_ERR_SHAPE;
+  if (rt->dtype != seq->dtype) return TAV2_ERR_DTYPE;
+  if ((rt->time_bucket != nullptr) != (seq->time_bucket != nullptr)) return TAV2_ERR_SHAPE;
+  return TAV2_OK;
+}
+
+size_t select_ws_bytes(const tav2_seq* s, const tav2_cands* c) {
+  return align_up(size_t(c->total) * size_t(score_ld(s->max_len)) * 4, WS_ALIGN);
+}
+
+size_t encode_ws_bytes(int64_t total, int T, const tav2_weights* w) {
+  if (w->dtype == TAV2_F32) return 0;
+  return align_up(encode_bf16_workspace(total, T, *w), WS_ALIGN);
+}
+
+tav2_status run_encode(const TokenSource& src, const void* cand_emb, int64_t total,
+                       const tav2_weights* w, float* out, void* ws, size_t ws_bytes,
+                       hipStream_t st) {
+  if (w->dtype == TAV2_BF16)
+    return hip_status(launch_encode_bf16(src, cand_emb, total, *w, out, ws, ws_bytes, st));
+  return hip_status(launch_encode_f32(src, cand_emb, total, *w, out, st));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tav2_status_string(tav2_status s) {
+  switch (s) {
+    case TAV2_OK: return "ok";
+    case TAV2_ERR_NULL: return "a required pointer is NULL";
+    case TAV2_ERR_SHAPE: return "a size is out of range or inconsistent";
+    case TAV2_ERR_DTYPE: return "unknown or mismatched dtype";
+    case TAV2_ERR_UNSUPPORTED: return "valid request not implemented by this build";
+    case TAV2_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case TAV2_ERR_HIP: return "HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+int32_t tav2_abi_version(void) { return ABI_VERSION; }
+
+size_t tav2_nn_select_workspace(const tav2_seq* seq, const tav2_cands* cands, int32_t k) {
+  if (check_seq(seq, true) || check_cands(cands, seq) || check_k(k)) return 0;
+  return select_ws_bytes(seq, cands);
+}
+
+tav2_status tav2_nn_select(const tav2_seq* seq, const tav2_cands* cands, int32_t k,
+                           int32_t* out_idx, float* out_score, void* ws, size_t ws_bytes,
+                           void* stream) {
+  tav2_status st;
+  if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
+  if (seq->dtype != TAV2_F32 && seq->dtype != TAV2_BF16) return TAV2_ERR_DTYPE;
+  if (cands->total == 0) return TAV2_OK;
+  if (!out_idx || !out_score) return TAV2_ERR_NULL;
+  if ((st = check_ws(ws, ws_bytes, select_ws_bytes(seq, cands)))) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float* scores = static_cast<float*>(ws);
+  const int64_t ld = score_ld(seq->max_len);
+  hipError_t e = launch_scores(*seq, *cands, scores, ld, s);
+  if (e == hipSuccess) e = launch_topk(*seq, *cands, scores, ld, k, out_idx, out_score, s);
+  return hip_status(e);
+}
+
+tav2_status tav2_gather(const tav2_seq* seq, const tav2_seq* rt, const tav2_cands* cands,
+                        const int32_t* idx, int32_t k, void* tok_emb, uint8_t* tok_act,
+                        uint8_t* tok_time, int32_t* valid_len, void* stream) {
+  tav2_status st;
+  if ((st = check_seq(seq, false)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
+  if ((st = check_rt(rt, seq))) return st;
+  if (cands->total == 0) return TAV2_OK;
+  if (!idx || !tok_emb || !tok_act || !valid_len) return TAV2_ERR_NULL;
+  if (!aligned(tok_emb, 16)) return TAV2_ERR_SHAPE;
+  const int T = k + rt_len_max(rt);
+  if (T > TAV2_T_MAX + TAV2_K_MAX) return TAV2_ERR_SHAPE;
+  return hip_status(launch_gather(*seq, rt, *cands, idx, k, T, tok_emb, tok_act, tok_time,
+                                  valid_len, static_cast<hipStream_t>(stream)));
+}
+
+size_t tav2_encode_workspace(const tav2_tokens* tok, const tav2_weights* w) {
+  if (!tok || !w) return 0;
+  if (check_weights(w, tok->d, tok->dtype, tok->T, tok->time_bucket != nullptr)) return 0;
+  return encode_ws_bytes(tok->total, tok->T, w);
+}
+
+tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2_weights* w,
+                        float* out, void* ws, size_t ws_bytes, void* stream) {
+  if (!tok || !w) return TAV2_ERR_NULL;
+  tav2_status st;
+  if ((st = check_dtype(tok->dtype))) return st;
+  if (tok->total < 0 || tok->d < 16 || tok->d > 512 || tok->d % 16) return TAV2_ERR_SHAPE;
+  if (tok->total > (int64_t(1) << 31) - 1) return TAV2_ERR_UNSUPPORTED;
+  if ((st = check_weights(w, tok->d, tok->dtype, tok->T, tok->time_bucket != nullptr))) return st;
+  if (tok->total == 0) return TAV2_OK;
+  if (!tok->emb || !tok->action_type || !tok->valid_len || !cand_emb || !out) return TAV2_ERR_NULL;
+  if (!aligned(tok->emb, 16) || !aligned(cand_emb, 16) || !aligned(out, 16)) return TAV2_ERR_SHAPE;
+  if ((st = check_ws(ws, ws_bytes, encode_ws_bytes(tok->total, tok->T, w)))) return st;
+  TokenSource src{};
+  src.explicit_tokens = true;
+  src.tok_emb = tok->emb;
+  src.tok_act = tok->action_type;
+  src.tok_time = tok->time_bucket;
+  src.valid_len = tok->valid_len;
+  src.T = tok->T;
+  src.d = tok->d;
+  return run_encode(src, cand_emb, tok->total, w, out, ws, ws_bytes,
+                    static_cast<hipStream_t>(stream));
+}
+
+size_t tav2_select_encode_workspace(const tav2_seq* seq, const tav2_seq* rt,
+                                    const tav2_cands* cands, int32_t k, const tav2_weights* w) {
+  if (check_seq(seq, true) || check_cands(cands, seq) || check_k(k) || check_rt(rt, seq)) return 0;
+  const int T = k + rt_len_max(rt);
+  if (check_weights(w, seq->d, seq->dtype, T, seq->time_bucket != nullptr)) return 0;
+  return select_ws_bytes(seq, cands) + align_up(size_t(cands->total) * 4, WS_ALIGN) +
+         encode_ws_bytes(cands->total, T, w);
+}
+
+tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt, const tav2_cands* cands,
+                               int32_t k, const tav2_weights* w, int32_t* out_idx,
+                               float* out_score, float* out, void* ws, size_t ws_bytes,
+                               void* stream) {
+  tav2_status st;
+  if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
+  if ((st = check_rt(rt, seq))) return st;
+  const int T = k + rt_len_max(rt);
+  if ((st = check_weights(w, seq->d, seq->dtype, T, seq->time_bucket != nullptr))) return st;
+  if (cands->total == 0) return TAV2_OK;
+  if (!out_idx || !out_score || !out) return TAV2_ERR_NULL;
+  if (!aligned(out, 16)) return TAV2_ERR_SHAPE;
+  const size_t sel_b = select_ws_bytes(seq, cands);
+  const size_t req_b = align_up(size_t(cands->total) * 4, WS_ALIGN);
+  const size_t enc_b = encode_ws_bytes(cands->total, T, w);
+  if ((st = check_ws(ws, ws_bytes, sel_b + req_b + enc_b))) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  float* scores = reinterpret_cast<float*>(base);
+  int32_t* cand_req = reinterpret_cast<int32_t*>(base + sel_b);
+  void* enc_ws = base + sel_b + req_b;
+  const int64_t ld = score_ld(seq->max_len);
+  hipError_t e = launch_scores(*seq, *cands, scores, ld, s);
+  if (e == hipSuccess) e = launch_topk(*seq, *cands, scores, ld, k, out_idx, out_score, s);
+  if (e == hipSuccess) e = launch_cand_request(*cands, seq->num_requests, cand_req, s);
+  if (e != hipSuccess) return TAV2_ERR_HIP;
+  TokenSource src{};
+  src.explicit_tokens = false;
+  src.seq_emb = seq->emb;
+  src.seq_act = seq->action_type;
+  src.seq_time = seq->time_bucket;
+  src.seq_off = seq->offset;
+  src.seq_len = seq->len;
+  if (rt) {
+    src.rt_emb = rt->emb;
+    src.rt_act = rt->action_type;
+    src.rt_time = rt->time_bucket;
+    src.rt_off = rt->offset;
+    src.rt_len = rt->len;
+  }
+  src.idx = out_idx;
+  src.cand_req = cand_req;
+  src.k = k;
+  src.T = T;
+  src.d = seq->d;
+  return run_encode(src, cands->emb, cands->total, w, out, enc_ws, enc_b, s);
+}
+
+}  // extern "C"

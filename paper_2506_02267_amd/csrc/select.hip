@@ -1,0 +1,266 @@
+// NN search of Eq. 3 (Sec. 3.2.2): candidate x action dot-product scores over the
+// de-duplicated request-level sequence, then the per-candidate top-k under the
+// total order (score desc, row asc).
+//
+// Scores: bf16 operands on the 32x32x16 MFMA with fp32 accumulation (float32
+// inputs use fp32 FMA).  Each request's rows are read by every candidate tile of
+// that request straight from the one stored copy (no per-candidate broadcast).
+//
+// Top-k: one workgroup per candidate holds the candidate's score row in
+// registers as order-preserving 32-bit keys, finds the k-th largest key with a
+// 32-step bitwise search (each step one block-wide count), keeps every key
+// above it plus the lowest-indexed rows equal to it (an ordered compaction by
+// block-wide prefix sum), and places the k survivors by counting, for each,
+// how many survivors precede it in the total order.
+#include "common.h"
+#include "internal.h"
+
+namespace tav2 {
+
+// ---------------------------------------------------------------- scores, bf16
+// Block: 4 waves, 64 candidates x 256 rows; wave w covers rows [64w, 64w + 64).
+// Candidates are the MFMA rows (A), sequence rows the MFMA columns (B), so each
+// D register holds one candidate and 32 consecutive lanes 32 consecutive rows.
+constexpr int SC_CANDS = 64;
+constexpr int SC_ROWS = 256;
+
+__global__ __launch_bounds__(256) void score_bf16_kernel(
+    const bf16_t* __restrict__ emb, const int64_t* __restrict__ seq_off,
+    const int32_t* __restrict__ seq_len, const bf16_t* __restrict__ cand,
+    const int64_t* __restrict__ cand_off, int d, int max_len, float* __restrict__ scores,
+    int64_t ld) {
+  const int r = blockIdx.z;
+  const int64_t c_begin = cand_off[r], c_end = cand_off[r + 1];
+  const int64_t n0 = c_begin + int64_t(blockIdx.y) * SC_CANDS;
+  if (n0 >= c_end) return;
+  const int L = min(seq_len[r], max_len);
+  const int row0 = blockIdx.x * SC_ROWS + (threadIdx.x / WAVE) * 64;
+  if (row0 >= L) return;
+  const int lane = threadIdx.x % WAVE;
+  const int h = lane / 32, l32 = lane % 32;
+  const bf16_t* seq = emb + seq_off[r] * int64_t(d);
+
+  // clamp out-of-range candidates / rows to a valid one; their results are not stored
+  const bf16_t* arow[2];
+  const bf16_t* brow[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    int64_t n = n0 + t * 32 + l32;
+    n = n < c_end ? n : c_end - 1;
+    arow[t] = cand + n * d + 8 * h;
+    int i = row0 + t * 32 + l32;
+    i = i < L ? i : L - 1;
+    brow[t] = seq + int64_t(i) * d + 8 * h;
+  }
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+
+  for (int k0 = 0; k0 < d; k0 += 16) {
+    bf16x8 av[2], bv[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      av[t] = as_bf16x8(*reinterpret_cast<const uint4*>(arow[t] + k0));
+      bv[t] = as_bf16x8(*reinterpret_cast<const uint4*>(brow[t] + k0));
+    }
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < 2; ++b) acc[a][b] = mfma32(av[a], bv[b], acc[a][b]);
+  }
+
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int i = row0 + b * 32 + l32;
+    if (i >= L) continue;
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) {
+        const int64_t n = n0 + a * 32 + 8 * (reg / 4) + 4 * h + (reg % 4);
+        if (n < c_end) scores[n * ld + i] = acc[a][b][reg];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- scores, fp32
+__global__ __launch_bounds__(256) void score_f32_kernel(
+    const float* __restrict__ emb, const int64_t* __restrict__ seq_off,
+    const int32_t* __restrict__ seq_len, const float* __restrict__ cand,
+    const int64_t* __restrict__ cand_off, int d, int max_len, float* __restrict__ scores,
+    int64_t ld) {
+  __shared__ float cv[512];
+  const int r = blockIdx.z;
+  const int64_t n = cand_off[r] + blockIdx.y;
+  if (n >= cand_off[r + 1]) return;
+  const int L = min(seq_len[r], max_len);
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (blockIdx.x * 256 >= L) return;
+  for (int j = threadIdx.x; j < d; j += 256) cv[j] = cand[n * d + j];
+  __syncthreads();
+  if (i >= L) return;
+  const float4* row = reinterpret_cast<const float4*>(emb + (seq_off[r] + i) * int64_t(d));
+  float s = 0.f;
+  for (int j = 0; j < d / 4; ++j) {
+    float4 v = row[j];
+    s = fmaf(v.x, cv[4 * j], s);
+    s = fmaf(v.y, cv[4 * j + 1], s);
+    s = fmaf(v.z, cv[4 * j + 2], s);
+    s = fmaf(v.w, cv[4 * j + 3], s);
+  }
+  scores[n * ld + i] = s;
+}
+
+// ---------------------------------------------------------------- top-k
+constexpr int TK_THREADS = 512;
+
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane) {
+#pragma unroll
+  for (int o = 1; o < WAVE; o <<= 1) {
+    uint32_t t = __shfl_up(v, o, WAVE);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
+
+template <int PT>
+__global__ __launch_bounds__(TK_THREADS) void topk_kernel(
+    const float* __restrict__ scores, int64_t ld, const int64_t* __restrict__ cand_off,
+    const int32_t* __restrict__ seq_len, int max_len, int k, int32_t* __restrict__ out_idx,
+    float* __restrict__ out_score) {
+  __shared__ int red[2][TK_THREADS / WAVE];
+  __shared__ uint32_t wtot[TK_THREADS / WAVE];
+  __shared__ uint64_t sel[TAV2_K_MAX];
+
+  const int r = blockIdx.y;
+  const int64_t n = cand_off[r] + blockIdx.x;
+  if (n >= cand_off[r + 1]) return;
+  const int L = min(seq_len[r], max_len);
+  const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
+  const int kk = k < L ? k : L;
+  int32_t* oi = out_idx + n * k;
+  float* os = out_score + n * k;
+  for (int p = kk + tid; p < k; p += TK_THREADS) {
+    oi[p] = -1;
+    os[p] = -__builtin_inff();
+  }
+  if (kk == 0) return;
+
+  // this thread's rows: [base, base + PT), key 0 (below every score) past L
+  const float* srow = scores + n * ld;
+  const int base = tid * PT;
+  uint32_t key[PT];
+#pragma unroll
+  for (int j = 0; j < PT; j += 4) {
+    if (base + j + 4 <= L) {
+      float4 v = *reinterpret_cast<const float4*>(srow + base + j);
+      key[j] = score_key(v.x);
+      key[j + 1] = score_key(v.y);
+      key[j + 2] = score_key(v.z);
+      key[j + 3] = score_key(v.w);
+    } else {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) key[j + u] = (base + j + u < L) ? score_key(srow[base + j + u]) : 0u;
+    }
+  }
+
+  // largest threshold t with count(key >= t) >= kk, one bit at a time
+  uint32_t thr = 0;
+  for (int b = 31; b >= 0; --b) {
+    const uint32_t probe = thr | (1u << b);
+    int cnt = 0;
+#pragma unroll
+    for (int j = 0; j < PT; ++j) cnt += key[j] >= probe ? 1 : 0;
+    cnt = wave_sum_i(cnt);
+    if (lane == 0) red[b & 1][wid] = cnt;
+    __syncthreads();
+    int tot = 0;
+#pragma unroll
+    for (int w = 0; w < TK_THREADS / WAVE; ++w) tot += red[b & 1][w];
+    if (tot >= kk) thr = probe;
+  }
+
+  // ordered compaction: keys above thr anywhere, then the lowest rows equal to thr
+  uint32_t gt = 0, eq = 0;
+#pragma unroll
+  for (int j = 0; j < PT; ++j) {
+    gt += key[j] > thr ? 1u : 0u;
+    eq += key[j] == thr ? 1u : 0u;
+  }
+  const uint32_t mine = (gt << 16) | eq;
+  const uint32_t incl = wave_incl_scan(mine, lane);
+  if (lane == WAVE - 1) wtot[wid] = incl;
+  __syncthreads();
+  uint32_t pre = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < TK_THREADS / WAVE; ++w) {
+    pre += w < wid ? wtot[w] : 0u;
+    all += wtot[w];
+  }
+  const uint32_t excl = pre + incl - mine;
+  const int count_gt = int(all >> 16);
+  const int need_eq = kk - count_gt;
+  int gpos = int(excl >> 16), epos = int(excl & 0xFFFFu);
+#pragma unroll
+  for (int j = 0; j < PT; ++j) {
+    const uint64_t packed = (uint64_t(key[j]) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(base + j));
+    if (key[j] > thr) {
+      sel[gpos++] = packed;
+    } else if (key[j] == thr) {
+      if (epos < need_eq) sel[count_gt + epos] = packed;
+      ++epos;
+    }
+  }
+  __syncthreads();
+
+  // survivors are distinct under (key, -row): rank = number of survivors before it
+  for (int s = tid; s < kk; s += TK_THREADS) {
+    const uint64_t me = sel[s];
+    int rank = 0;
+    for (int t = 0; t < kk; ++t) rank += sel[t] > me ? 1 : 0;
+    oi[rank] = int32_t(0xFFFFFFFFu - uint32_t(me));
+    os[rank] = key_score(uint32_t(me >> 32));
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores, int64_t ld,
+                         hipStream_t st) {
+  if (seq.num_requests == 0 || c.total == 0 || seq.max_len == 0) return hipSuccess;
+  if (seq.dtype == TAV2_BF16) {
+    dim3 grid(unsigned(cdiv(seq.max_len, SC_ROWS)), unsigned(cdiv(c.max_count, SC_CANDS)),
+              unsigned(seq.num_requests));
+    score_bf16_kernel<<<grid, 256, 0, st>>>(
+        static_cast<const bf16_t*>(seq.emb), seq.offset, seq.len,
+        static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
+  } else {
+    dim3 grid(unsigned(cdiv(seq.max_len, 256)), unsigned(c.max_count), unsigned(seq.num_requests));
+    score_f32_kernel<<<grid, 256, 0, st>>>(
+        static_cast<const float*>(seq.emb), seq.offset, seq.len,
+        static_cast<const float*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* scores, int64_t ld,
+                       int k, int32_t* out_idx, float* out_score, hipStream_t st) {
+  if (seq.num_requests == 0 || c.total == 0) return hipSuccess;
+  dim3 grid(unsigned(c.max_count), unsigned(seq.num_requests));
+  const int per = int(cdiv(seq.max_len > 0 ? seq.max_len : 1, TK_THREADS));
+#define TAV2_TOPK(PT) \
+  topk_kernel<PT><<<grid, TK_THREADS, 0, st>>>(scores, ld, c.offset, seq.len, seq.max_len, k, out_idx, out_score)
+  if (per <= 4) TAV2_TOPK(4);
+  else if (per <= 8) TAV2_TOPK(8);
+  else if (per <= 16) TAV2_TOPK(16);
+  else if (per <= 32) TAV2_TOPK(32);
+  else TAV2_TOPK(64);
+#undef TAV2_TOPK
+  return hipGetLastError();
+}
+
+int64_t score_ld(int32_t max_len) { return int64_t(align_up(size_t(max_len > 0 ? max_len : 1), 64)); }
+
+}  // namespace tav2

@@ -1,0 +1,55 @@
+"""Shared plumbing for the GPU parity tests (device upload, oracle sampling)."""
+import numpy as np
+import torch
+
+import oracle
+import synth
+from paper_2506_02267_amd import tav2 as T
+
+BF16_TOL = 2e-2   # max-abs error bound for bf16 encoder outputs
+F32_TOL = 1e-4    # max-abs error bound for fp32 encoder outputs
+
+
+def dtype_code(w):
+    return T.BF16 if w.dtype == "bf16" else T.F32
+
+
+def upload(inp, device="cuda"):
+    dt = dtype_code(inp.w)
+    seq = T.DeviceSeq.from_host(inp.seq, dt, device)
+    rt = T.DeviceSeq.from_host(inp.rt, dt, device) if inp.rt is not None else None
+    cands = T.DeviceCands.from_host(inp.cand, inp.cand_offset, dt, device)
+    return seq, rt, cands
+
+
+def sample_ids(inp, per_request):
+    ids = []
+    for r in range(inp.seq.R):
+        a, b = int(inp.cand_offset[r]), int(inp.cand_offset[r + 1])
+        n = b - a
+        if n == 0:
+            continue
+        step = max(1, n // per_request)
+        ids.extend(range(a, b, step)[:per_request])
+        if b - 1 not in ids:
+            ids.append(b - 1)
+    return np.array(sorted(set(ids)), dtype=np.int64)
+
+
+def assert_select_equal(idx_gpu, score_gpu, idx_ref, score_ref, ids=None):
+    ig = idx_gpu.cpu().numpy()
+    sg = score_gpu.cpu().numpy()
+    if ids is not None:
+        ig, sg, idx_ref, score_ref = ig[ids], sg[ids], idx_ref[ids], score_ref[ids]
+    bad = np.argwhere(ig != idx_ref)
+    assert bad.size == 0, f"{len(bad)} idx mismatches, first at {bad[:5].tolist()}"
+    # scores compared bit for bit (+0.0 canonical, -inf padding)
+    assert np.array_equal(sg.view(np.uint32), score_ref.astype(np.float32).view(np.uint32))
+
+
+def max_abs(out_gpu, out_ref, ids=None):
+    og = out_gpu.cpu().numpy().astype(np.float64)
+    if ids is not None:
+        og, out_ref = og[ids], out_ref[ids]
+    assert np.all(np.isfinite(og))
+    return float(np.abs(og - out_ref).max()) if og.size else 0.0

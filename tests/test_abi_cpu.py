@@ -1,0 +1,210 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/tav2.h declares, its structs match the binding's
+layout, workspace queries are pure host arithmetic, and every argument error
+is reported before anything is launched."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2506_02267_amd import tav2 as T
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tav2.h")
+
+FAKE = 0x10000   # an aligned non-null "device" address; never dereferenced on error paths
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b(tav2_\w+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def test_library_exports_every_declared_function():
+    lib = T.load_library()
+    names = declared_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(T.FUNCTIONS), "binding and header disagree"
+    out = subprocess.run(["nm", "-D", "--defined-only", T.LIB_PATH], capture_output=True,
+                         text=True).stdout
+    for n in names:
+        assert re.search(rf"\bT {n}$", out, flags=re.M), n
+
+
+def test_struct_layouts_match_header(tmp_path):
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "tav2.h"\n'
+                   'int main(void){printf("%zu %zu %zu %zu %zu %zu %zu %zu\\n",'
+                   'sizeof(tav2_seq), sizeof(tav2_cands), sizeof(tav2_tokens),'
+                   'sizeof(tav2_layer), sizeof(tav2_weights), offsetof(tav2_seq, max_len),'
+                   'offsetof(tav2_weights, layers), offsetof(tav2_tokens, total));return 0;}\n')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = [ctypes.sizeof(T.Seq), ctypes.sizeof(T.Cands), ctypes.sizeof(T.Tokens),
+            ctypes.sizeof(T.Layer), ctypes.sizeof(T.Weights), T.Seq.max_len.offset,
+            T.Weights.layers.offset, T.Tokens.total.offset]
+    assert got == want
+
+
+def fake_seq(R=2, d=64, dtype=T.BF16, max_len=100, time=True):
+    return T.Seq(emb=FAKE, action_type=FAKE, time_bucket=FAKE if time else None, offset=FAKE,
+                 len=FAKE, num_requests=R, d=d, dtype=dtype, max_len=max_len)
+
+
+def fake_cands(total=10, max_count=5):
+    return T.Cands(emb=FAKE, offset=FAKE, total=total, max_count=max_count, reserved=0)
+
+
+def fake_weights(d=64, dm=256, heads=4, ffn=512, layers=2, max_pos=64, dtype=T.BF16, time=True):
+    L = (T.Layer * layers)(*[T.Layer(*([FAKE] * 12)) for _ in range(layers)])
+    w = T.Weights(d_in=d, d_model=dm, n_heads=heads, d_ffn=ffn, n_layers=layers,
+                  max_pos=max_pos, dtype=dtype, reserved=0, W_in=FAKE, b_in=FAKE, E_act=FAKE,
+                  E_time=FAKE if time else None, E_pos=FAKE, layers=L, W_pool=FAKE, b_pool=FAKE)
+    w._keep = L
+    return w
+
+
+def call_select(seq, cands, k, idx=FAKE, score=FAKE, ws=FAKE, wsb=1 << 40):
+    lib = T.load_library()
+    return lib.tav2_nn_select(ctypes.byref(seq) if seq is not None else None,
+                              ctypes.byref(cands) if cands is not None else None, k, idx, score,
+                              ws, wsb, None)
+
+
+def test_workspace_queries():
+    lib = T.load_library()
+    s, c = fake_seq(max_len=1000), fake_cands(total=10)
+    # scores: total x round_up(max_len, 64) fp32
+    assert lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 16) == 10 * 1024 * 4
+    assert lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 0) == 0
+    w = fake_weights()
+    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
+                   d=64, dtype=T.BF16, reserved=0)
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) > 10 * 64 * 256 * 4
+    wf = fake_weights(dm=64, heads=2, ffn=128, layers=1, max_pos=32, dtype=T.F32, time=False)
+    tokf = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=None, valid_len=FAKE, total=16, T=32,
+                    d=64, dtype=T.F32, reserved=0)
+    assert lib.tav2_encode_workspace(ctypes.byref(tokf), ctypes.byref(wf)) == 0
+    se = lib.tav2_select_encode_workspace(ctypes.byref(s), None, ctypes.byref(c), 64,
+                                          ctypes.byref(w))
+    assert se > lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 64)
+
+
+@pytest.mark.parametrize("case,status", [
+    ("null_seq", -1), ("null_cands", -1), ("k0", -2), ("k_big", -2), ("bad_dtype", -3),
+    ("bad_d", -2), ("neg_R", -2), ("long_seq", -4), ("null_out", -1), ("small_ws", -5),
+    ("null_ws", -5), ("misaligned_ws", -5), ("misaligned_emb", -2), ("count_gt_total", -2),
+])
+def test_nn_select_argument_errors(case, status):
+    s, c = fake_seq(), fake_cands()
+    kw = {}
+    k = 8
+    if case == "null_seq":
+        s = None
+    elif case == "null_cands":
+        c = None
+    elif case == "k0":
+        k = 0
+    elif case == "k_big":
+        k = 1025
+    elif case == "bad_dtype":
+        s.dtype = 7
+    elif case == "bad_d":
+        s.d = 60
+    elif case == "neg_R":
+        s.num_requests = -1
+    elif case == "long_seq":
+        s.max_len = 40000
+    elif case == "null_out":
+        kw["idx"] = None
+    elif case == "small_ws":
+        kw["wsb"] = 16
+    elif case == "null_ws":
+        kw["ws"] = None
+    elif case == "misaligned_ws":
+        kw["ws"] = FAKE + 8
+    elif case == "misaligned_emb":
+        s.emb = FAKE + 2
+    elif case == "count_gt_total":
+        c.max_count = 11
+    assert call_select(s, c, k, **kw) == status
+
+
+def test_empty_candidate_set_is_a_no_op():
+    assert call_select(fake_seq(), fake_cands(total=0, max_count=0), 8, idx=None, score=None,
+                       ws=None, wsb=0) == 0
+
+
+@pytest.mark.parametrize("case,status", [
+    ("dtype_mismatch", -3), ("heads", -2), ("dm_unsupported", -4), ("ffn", -4),
+    ("max_pos", -2), ("time_mismatch", -2), ("null_layer_ptr", -1), ("T_too_big", -2),
+    ("f32_too_big", -4), ("null_out", -1), ("ws", -5), ("d_in", -2),
+])
+def test_encode_argument_errors(case, status):
+    lib = T.load_library()
+    w = fake_weights()
+    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
+                   d=64, dtype=T.BF16, reserved=0)
+    out, ws, wsb = FAKE, FAKE, 1 << 40
+    if case == "dtype_mismatch":
+        w.dtype = T.F32
+    elif case == "heads":
+        w.n_heads = 3
+    elif case == "dm_unsupported":
+        w.d_model, w.n_heads = 128, 2
+    elif case == "ffn":
+        w.d_ffn = 300
+    elif case == "max_pos":
+        w.max_pos = 63
+    elif case == "time_mismatch":
+        tok.time_bucket = None
+    elif case == "null_layer_ptr":
+        w.layers[1].W_2 = None
+    elif case == "T_too_big":
+        tok.T = 2000
+        w.max_pos = 2000
+    elif case == "f32_too_big":
+        tok.dtype = T.F32
+        w.dtype = T.F32
+    elif case == "null_out":
+        out = None
+    elif case == "ws":
+        wsb = 10
+    elif case == "d_in":
+        w.d_in = 32
+    st = lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), out, ws, wsb, None)
+    assert st == status
+
+
+def test_select_encode_checks_realtime_and_positions():
+    lib = T.load_library()
+    s, c = fake_seq(d=64), fake_cands()
+    rt = fake_seq(d=64, max_len=100)
+    w = fake_weights(max_pos=64 + 99)
+    st = lib.tav2_select_encode(ctypes.byref(s), ctypes.byref(rt), ctypes.byref(c), 64,
+                                ctypes.byref(w), FAKE, FAKE, FAKE, FAKE, 1 << 40, None)
+    assert st == -2          # k + rt->max_len exceeds max_pos
+    rt2 = fake_seq(R=3, d=64, max_len=10)
+    st = lib.tav2_select_encode(ctypes.byref(s), ctypes.byref(rt2), ctypes.byref(c), 64,
+                                ctypes.byref(fake_weights(max_pos=100)), FAKE, FAKE, FAKE, FAKE,
+                                1 << 40, None)
+    assert st == -2          # real-time batch with a different request count
+    st = lib.tav2_select_encode(ctypes.byref(s), None, ctypes.byref(c), 64,
+                                ctypes.byref(fake_weights(time=False)), FAKE, FAKE, FAKE, FAKE,
+                                1 << 40, None)
+    assert st == -2          # sequence has time buckets, weights have no time table
+
+
+def test_status_strings():
+    lib = T.load_library()
+    for code in range(-6, 1):
+        assert lib.tav2_status_string(code).decode()
+    assert lib.tav2_abi_version() >= 1

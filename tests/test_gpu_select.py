@@ -1,0 +1,135 @@
+"""GPU parity of tav2_nn_select (Eq. 3) against the oracle: indices and scores
+bit for bit, on the five workloads (full runs, all or sampled candidates) and
+on edge cases (ragged, empty and short requests, k = 1 and k = K_MAX, heavy
+ties, padded layout, every register-tile size of the top-k kernel)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from helpers import assert_select_equal, sample_ids, upload
+from paper_2506_02267_amd import tav2 as T
+
+pytestmark = pytest.mark.gpu
+
+
+def run_select(inp, k):
+    seq, _, cands = upload(inp)
+    idx, score = T.nn_select(seq, cands, k)
+    torch.cuda.synchronize()
+    return idx, score
+
+
+@pytest.mark.parametrize("cid", [1, 2, 4])
+def test_full_workload_all_candidates(cid):
+    w = synth.WORKLOADS[cid]
+    inp = synth.make_inputs(w)
+    print(f"select workload {w.name}", flush=True)
+    idx, score = run_select(inp, w.k)
+    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, w.k)
+    assert_select_equal(idx, score, ref_i, ref_s)
+
+
+@pytest.mark.parametrize("cid,per", [(3, 6), (5, 12)])
+def test_full_workload_sampled_candidates(cid, per):
+    w = synth.WORKLOADS[cid]
+    inp = synth.make_inputs(w)
+    print(f"select workload {w.name}", flush=True)
+    idx, score = run_select(inp, w.k)
+    ids = sample_ids(inp, per)
+    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, w.k, only=ids)
+    assert_select_equal(idx, score, ref_i, ref_s, ids=ids)
+
+
+def custom_inputs(lengths, counts, d=64, dtype="bf16", levels=8, seed=0):
+    """Requests with the given lengths and candidate counts (grid values)."""
+    rng = np.random.default_rng(seed)
+    w = synth.scaled(synth.SINGLE, R=len(lengths), d=d, dtype=dtype, N=max(counts) if counts else 0)
+    off = np.zeros(len(lengths), dtype=np.int64)
+    off[1:] = np.cumsum(lengths)[:-1]
+    rows = int(np.sum(lengths))
+    seq = synth.SeqBatch(emb=rng.integers(-levels, levels + 1, (rows, d)).astype(np.float32) / 8,
+                         act=rng.integers(0, 8, rows).astype(np.uint8),
+                         time=np.sort(rng.integers(0, 64, rows)).astype(np.uint8),
+                         offset=off, length=np.asarray(lengths, dtype=np.int32))
+    coff = np.zeros(len(counts) + 1, dtype=np.int64)
+    coff[1:] = np.cumsum(counts)
+    cand = rng.integers(-levels, levels + 1, (int(coff[-1]), d)).astype(np.float32) / 8
+    return synth.Inputs(w=w, seq=seq, cand=cand, cand_offset=coff)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_ragged_short_and_empty_requests(dtype):
+    inp = custom_inputs([0, 5, 300, 2000, 64], [3, 4, 7, 5, 2], dtype=dtype)
+    for k in (1, 64, 301):
+        idx, score = run_select(inp, k)
+        ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
+        assert_select_equal(idx, score, ref_i, ref_s)
+
+
+def test_request_without_candidates():
+    inp = custom_inputs([100, 200, 300], [4, 0, 3])
+    idx, score = run_select(inp, 16)
+    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, 16)
+    assert_select_equal(idx, score, ref_i, ref_s)
+
+
+@pytest.mark.parametrize("L", [100, 3000, 6000, 16384, 20000, 32768])
+def test_each_register_tile_size(L):
+    inp = custom_inputs([L], [9], d=32, levels=2, seed=L)
+    k = min(1024, L)
+    idx, score = run_select(inp, k)
+    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
+    assert_select_equal(idx, score, ref_i, ref_s)
+
+
+def test_heavy_ties_and_k_max():
+    inp = custom_inputs([4096, 3000], [6, 6], d=16, levels=1, seed=3)   # values in {-1/8, 0, 1/8}
+    for k in (1, 2, 1024):
+        idx, score = run_select(inp, k)
+        ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
+        assert_select_equal(idx, score, ref_i, ref_s)
+
+
+def test_zero_scores_are_positive_zero():
+    inp = custom_inputs([50], [3], d=16)
+    inp.seq.emb[:] = 0.0
+    inp.cand[0] = -1.0
+    idx, score = run_select(inp, 10)
+    s = score.cpu().numpy()
+    assert np.all(s == 0) and not np.any(np.signbit(s))
+    np.testing.assert_array_equal(idx.cpu().numpy(), np.tile(np.arange(10), (3, 1)))
+
+
+def test_padded_layout_equals_packed_and_batch_equals_single():
+    w = synth.scaled(synth.RAGGED, R=5, L_range=(700, 3000), N=11, k=128)
+    inp = synth.make_inputs(w)
+    idx, score = run_select(inp, 128)
+    padded = synth.Inputs(w=w, seq=synth.to_padded(inp.seq, pad_to=3072), cand=inp.cand,
+                          cand_offset=inp.cand_offset)
+    i2, s2 = run_select(padded, 128)
+    assert torch.equal(idx, i2) and torch.equal(score.view(torch.int32), s2.view(torch.int32))
+    for r in range(w.R):
+        a, b = int(inp.cand_offset[r]), int(inp.cand_offset[r + 1])
+        one = synth.Inputs(w=w, seq=synth.SeqBatch(
+            emb=inp.seq.emb[inp.seq.rows(r)], act=inp.seq.act[inp.seq.rows(r)],
+            time=inp.seq.time[inp.seq.rows(r)], offset=np.zeros(1, np.int64),
+            length=inp.seq.length[r:r + 1].copy()), cand=inp.cand[a:b],
+            cand_offset=np.array([0, b - a], dtype=np.int64))
+        i1, s1 = run_select(one, 128)
+        assert torch.equal(i1, idx[a:b]) and torch.equal(s1, score[a:b])
+
+
+def test_repeated_runs_and_streams_are_bitwise_identical():
+    w = synth.scaled(synth.STRESS, R=2, N=300, k=512)
+    inp = synth.make_inputs(w)
+    seq, _, cands = upload(inp)
+    outs = []
+    for i in range(3):
+        st = torch.cuda.Stream()
+        with torch.cuda.stream(st):
+            outs.append(T.nn_select(seq, cands, 512, stream=st))
+        st.synchronize()
+    for i, s in outs[1:]:
+        assert torch.equal(i, outs[0][0]) and torch.equal(s, outs[0][1])
