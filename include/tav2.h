@@ -79,7 +79,7 @@ typedef struct tav2_seq {
   const int64_t* offset;       /* device [R]: first row of each request */
   const int32_t* len;          /* device [R]: rows of each request, 0 <= len[r] <= max_len */
   int32_t num_requests;        /* R >= 0 */
-  int32_t d;                   /* embedding width, multiple of 8, 8..512 */
+  int32_t d;                   /* embedding width, multiple of 16, 16..512 */
   int32_t dtype;               /* TAV2_F32 or TAV2_BF16 */
   int32_t max_len;             /* host-side bound: len[r] <= max_len for every r */
 } tav2_seq;
@@ -217,6 +217,21 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt,
                                const tav2_cands* cands, int32_t k, const tav2_weights* w,
                                int32_t* out_idx, float* out_score, float* out,
                                void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Measurement hook for benchmarks and profilers (not needed for serving).
+ * tav2_profile_enable(1, site) makes every later kernel launch of the library
+ * whose site name equals `site` (NULL: every site) record a HIP event before
+ * and after itself on its stream; tav2_profile_enable(0, NULL) stops it.
+ * After the caller has synchronised, tav2_profile_report() writes one line
+ * "<site> <launches> <total_ms>" per site into buf (NUL-terminated, truncated
+ * to buf_bytes), forgets the recorded launches and returns the untruncated
+ * text length.  Site names: score_bf16, score_f32, topk, cand_request, gather,
+ * gemm_cand, gemm_embed, gemm_qkv, attention, gemm_oproj_ln1, gemm_ffn1,
+ * gemm_ffn2_ln2, fill, gemm_pool, pool_finalize, encode_f32.
+ */
+int32_t tav2_profile_enable(int32_t on, const char* only_site);
+int64_t tav2_profile_report(char* buf, size_t buf_bytes);
 
 #ifdef __cplusplus
 }

@@ -199,6 +199,9 @@ struct EpiQKV {
 };
 
 // X[m, :] = LN(C + bias + X[m, :]) over the GN (= dm) columns; one wave per row.
+// SITE distinguishes the attention sublayer (1) from the FFN sublayer (2) so the
+// two instantiations are separate kernels in traces.
+template <int SITE>
 struct EpiResLN {
   float* X;
   bf16_t* Xb;
@@ -465,10 +468,11 @@ Layout make_layout(int64_t total, int T, const tav2_weights& w) {
 }
 
 template <class ALoad, class Epi>
-hipError_t gemm(ALoad al, int64_t M, const void* B, int64_t ldb, int N, int K, Epi epi,
-                hipStream_t st) {
+hipError_t gemm(const char* site, ALoad al, int64_t M, const void* B, int64_t ldb, int N, int K,
+                Epi epi, hipStream_t st) {
   if (M == 0) return hipSuccess;
   dim3 grid(unsigned(cdiv(M, GM)), unsigned(N / GN));
+  ProfScope prof(site, st);
   gemm_kernel<ALoad, Epi><<<grid, 256, 0, st>>>(al, static_cast<const bf16_t*>(B), ldb, K, epi);
   return hipGetLastError();
 }
@@ -509,35 +513,44 @@ hipError_t launch_encode_bf16(const TokenSource& src, const void* cand_emb, int6
     const int64_t nc = (total - c0 < Lo.chunk) ? total - c0 : Lo.chunk;
     const int64_t M = nc * T;
     // candidate half of the fused input projection, once per candidate
-    TAV2_TRY(gemm(AMat{static_cast<const bf16_t*>(cand_emb) + c0 * d, d, nc}, nc, W_in + d,
+    TAV2_TRY(gemm("gemm_cand", AMat{static_cast<const bf16_t*>(cand_emb) + c0 * d, d, nc}, nc, W_in + d,
                   2 * d, dm, d, EpiBiasF32{cvec, dm, w.b_in, nc}, st));
     // token half + side tables, with the gather fused into the A loads
-    TAV2_TRY(gemm(ATokens{src, c0, M}, M, W_in, 2 * d, dm, d,
+    TAV2_TRY(gemm("gemm_embed", ATokens{src, c0, M}, M, W_in, 2 * d, dm, d,
                   EpiEmbed{X, Xb, cvec, static_cast<const bf16_t*>(w.E_act),
                            static_cast<const bf16_t*>(w.E_time),
                            static_cast<const bf16_t*>(w.E_pos), src, c0, M},
                   st));
     for (int li = 0; li < w.n_layers; ++li) {
       const tav2_layer& Lw = w.layers[li];
-      TAV2_TRY(gemm(AMat{Xb, dm, M}, M, Lw.W_qkv, dm, 3 * dm, dm,
+      TAV2_TRY(gemm("gemm_qkv", AMat{Xb, dm, M}, M, Lw.W_qkv, dm, 3 * dm, dm,
                     EpiQKV{Q, Kb, Vt, Lw.b_qkv, T, Tp, H, dh, M}, st));
       dim3 ag(unsigned(cdiv(T, 128)), unsigned(H), unsigned(nc));
-      if (dh == 64)
-        attention_kernel<64><<<ag, 256, 0, st>>>(Q, Kb, Vt, O, T, Tp, H);
-      else
-        attention_kernel<32><<<ag, 256, 0, st>>>(Q, Kb, Vt, O, T, Tp, H);
+      {
+        ProfScope prof("attention", st);
+        if (dh == 64)
+          attention_kernel<64><<<ag, 256, 0, st>>>(Q, Kb, Vt, O, T, Tp, H);
+        else
+          attention_kernel<32><<<ag, 256, 0, st>>>(Q, Kb, Vt, O, T, Tp, H);
+      }
       TAV2_TRY(hipGetLastError());
-      TAV2_TRY(gemm(AMat{O, dm, M}, M, Lw.W_o, dm, dm, dm,
-                    EpiResLN{X, Xb, Lw.b_o, Lw.ln1_g, Lw.ln1_b, M}, st));
-      TAV2_TRY(gemm(AMat{Xb, dm, M}, M, Lw.W_1, dm, ff, dm, EpiReluBf16{Hb, ff, Lw.b_1, M}, st));
-      TAV2_TRY(gemm(AMat{Hb, ff, M}, M, Lw.W_2, ff, dm, ff,
-                    EpiResLN{X, Xb, Lw.b_2, Lw.ln2_g, Lw.ln2_b, M}, st));
+      TAV2_TRY(gemm("gemm_oproj_ln1", AMat{O, dm, M}, M, Lw.W_o, dm, dm, dm,
+                    EpiResLN<1>{X, Xb, Lw.b_o, Lw.ln1_g, Lw.ln1_b, M}, st));
+      TAV2_TRY(gemm("gemm_ffn1", AMat{Xb, dm, M}, M, Lw.W_1, dm, ff, dm, EpiReluBf16{Hb, ff, Lw.b_1, M}, st));
+      TAV2_TRY(gemm("gemm_ffn2_ln2", AMat{Hb, ff, M}, M, Lw.W_2, ff, dm, ff,
+                    EpiResLN<2>{X, Xb, Lw.b_2, Lw.ln2_g, Lw.ln2_b, M}, st));
     }
-    fill_u32_kernel<<<unsigned(cdiv(nc * dm, 256)), 256, 0, st>>>(keys, nc * dm, 0u);
+    {
+      ProfScope prof("fill", st);
+      fill_u32_kernel<<<unsigned(cdiv(nc * dm, 256)), 256, 0, st>>>(keys, nc * dm, 0u);
+    }
     TAV2_TRY(hipGetLastError());
-    TAV2_TRY(gemm(AMat{Xb, dm, M}, M, w.W_pool, dm, dm, dm,
+    TAV2_TRY(gemm("gemm_pool", AMat{Xb, dm, M}, M, w.W_pool, dm, dm, dm,
                   EpiPool{keys, w.b_pool, src, c0, M}, st));
-    pool_finalize_kernel<<<unsigned(nc), 256, 0, st>>>(keys, X, src, c0, dm, out);
+    {
+      ProfScope prof("pool_finalize", st);
+      pool_finalize_kernel<<<unsigned(nc), 256, 0, st>>>(keys, X, src, c0, dm, out);
+    }
     TAV2_TRY(hipGetLastError());
   }
 #undef TAV2_TRY

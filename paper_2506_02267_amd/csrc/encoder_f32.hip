@@ -174,6 +174,7 @@ hipError_t launch_encode_f32(const TokenSource& src, const void* cand_emb, int64
   a.b_pool = w.b_pool;
   for (int i = 0; i < w.n_layers; ++i) a.layers[i] = w.layers[i];
   a.out = out;
+  ProfScope prof("encode_f32", st);
   encode_f32_kernel<<<unsigned(total), 256, 0, st>>>(a);
   return hipGetLastError();
 }

@@ -63,6 +63,7 @@ __global__ __launch_bounds__(256) void gather_kernel(
 hipError_t launch_cand_request(const tav2_cands& c, int R, int32_t* cand_req, hipStream_t st) {
   if (R == 0 || c.total == 0) return hipSuccess;
   dim3 grid(unsigned(cdiv(c.max_count, 256)), unsigned(R));
+  ProfScope prof("cand_request", st);
   cand_request_kernel<<<grid, 256, 0, st>>>(c.offset, cand_req);
   return hipGetLastError();
 }
@@ -73,6 +74,7 @@ hipError_t launch_gather(const tav2_seq& seq, const tav2_seq* rt, const tav2_can
   if (seq.num_requests == 0 || c.total == 0) return hipSuccess;
   const int es = seq.dtype == TAV2_BF16 ? 2 : 4;
   dim3 grid(unsigned(c.max_count), unsigned(seq.num_requests));
+  ProfScope prof("gather", st);
   gather_kernel<<<grid, 256, 0, st>>>(
       static_cast<const uint8_t*>(seq.emb), seq.action_type, seq.time_bucket, seq.offset, seq.len,
       rt ? static_cast<const uint8_t*>(rt->emb) : nullptr, rt ? rt->action_type : nullptr,

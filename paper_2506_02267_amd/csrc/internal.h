@@ -9,7 +9,22 @@
 
 namespace tav2 {
 
-constexpr int SEL_MAX_LEN = 32768;   // longest request sequence the top-k kernel holds in registers
+constexpr int SEL_MAX_LEN = 32768;
+
+// Brackets one kernel launch with HIP events when profiling is enabled
+// (tav2_profile_enable); a no-op otherwise.
+class ProfScope {
+ public:
+  ProfScope(const char* name, hipStream_t st);
+  ~ProfScope();
+  ProfScope(const ProfScope&) = delete;
+  ProfScope& operator=(const ProfScope&) = delete;
+
+ private:
+  const char* name_;
+  hipStream_t st_;
+  void* start_;
+};   // longest request sequence the top-k kernel holds in registers
 
 // ---- select.hip
 int64_t score_ld(int32_t max_len);

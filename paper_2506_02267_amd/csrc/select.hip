@@ -233,11 +233,13 @@ hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores
   if (seq.dtype == TAV2_BF16) {
     dim3 grid(unsigned(cdiv(seq.max_len, SC_ROWS)), unsigned(cdiv(c.max_count, SC_CANDS)),
               unsigned(seq.num_requests));
+    ProfScope prof("score_bf16", st);
     score_bf16_kernel<<<grid, 256, 0, st>>>(
         static_cast<const bf16_t*>(seq.emb), seq.offset, seq.len,
         static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
   } else {
     dim3 grid(unsigned(cdiv(seq.max_len, 256)), unsigned(c.max_count), unsigned(seq.num_requests));
+    ProfScope prof("score_f32", st);
     score_f32_kernel<<<grid, 256, 0, st>>>(
         static_cast<const float*>(seq.emb), seq.offset, seq.len,
         static_cast<const float*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
@@ -250,6 +252,7 @@ hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* sc
   if (seq.num_requests == 0 || c.total == 0) return hipSuccess;
   dim3 grid(unsigned(c.max_count), unsigned(seq.num_requests));
   const int per = int(cdiv(seq.max_len > 0 ? seq.max_len : 1, TK_THREADS));
+  ProfScope prof("topk", st);
 #define TAV2_TOPK(PT) \
   topk_kernel<PT><<<grid, TK_THREADS, 0, st>>>(scores, ld, c.offset, seq.len, seq.max_len, k, out_idx, out_score)
   if (per <= 4) TAV2_TOPK(4);

@@ -70,6 +70,8 @@ FUNCTIONS = {
     "tav2_select_encode": (c_int32, [POINTER(Seq), POINTER(Seq), POINTER(Cands), c_int32,
                                      POINTER(Weights), c_void_p, c_void_p, c_void_p, c_void_p,
                                      c_size_t, c_void_p]),
+    "tav2_profile_enable": (c_int32, [c_int32, ctypes.c_char_p]),
+    "tav2_profile_report": (ctypes.c_int64, [ctypes.c_char_p, c_size_t]),
 }
 
 _lib = None
@@ -334,6 +336,24 @@ class SelectEncode:
             ctypes.byref(self.c), self.k, ctypes.byref(self.w.s), _ptr(self.idx),
             _ptr(self.score), _ptr(self.out), self.wp, self.wb, _stream_handle(stream)))
         return self.idx, self.score, self.out
+
+
+def profile_enable(on: bool, site: Optional[str] = None):
+    """Bracket the library's launches (all, or one site) with HIP events."""
+    load_library().tav2_profile_enable(1 if on else 0, site.encode() if site else None)
+
+
+def profile_report() -> dict:
+    """{site: (launches, total_ms)} since the last report; call after synchronising."""
+    lib = load_library()
+    n = lib.tav2_profile_report(None, 0)
+    buf = ctypes.create_string_buffer(int(n) + 1)
+    lib.tav2_profile_report(buf, len(buf))
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, cnt, ms = line.split()
+        out[name] = (int(cnt), float(ms))
+    return out
 
 
 def select_encode(seq, rt, cands, k, w, stream=None):
