@@ -70,19 +70,6 @@ __global__ __launch_bounds__(256) void gemm_kernel(ALoad al, const bf16_t* __res
 #pragma unroll
   for (int q = 0; q < 4; ++q) brow[q] = B + int64_t(n0 + lr + 64 * q) * ldb;
 
-  uint4 ra, rb[4];
-  auto gload = [&](int k0) {
-    ra = arow ? *reinterpret_cast<const uint4*>(arow + k0 + lc) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) rb[q] = *reinterpret_cast<const uint4*>(brow[q] + k0 + lc);
-  };
-  auto sstore = [&](int buf) {
-    *reinterpret_cast<uint4*>(As + (buf * GM + lr) * GLD + lc) = ra;
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<uint4*>(Bs + (buf * GN + lr + 64 * q) * GLD + lc) = rb[q];
-  };
-
   f32x16 acc[2][2];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
@@ -90,12 +77,31 @@ __global__ __launch_bounds__(256) void gemm_kernel(ALoad al, const bf16_t* __res
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
 
   const int nk = K / GK;
-  gload(0);
-  sstore(0);
+  uint4 ra = arow ? *reinterpret_cast<const uint4*>(arow + lc) : make_uint4(0, 0, 0, 0);
+  uint4 rb0 = *reinterpret_cast<const uint4*>(brow[0] + lc);
+  uint4 rb1 = *reinterpret_cast<const uint4*>(brow[1] + lc);
+  uint4 rb2 = *reinterpret_cast<const uint4*>(brow[2] + lc);
+  uint4 rb3 = *reinterpret_cast<const uint4*>(brow[3] + lc);
+#define TAV2_SSTORE(buf)                                                        \
+  do {                                                                          \
+    *reinterpret_cast<uint4*>(As + ((buf) * GM + lr) * GLD + lc) = ra;          \
+    *reinterpret_cast<uint4*>(Bs + ((buf) * GN + lr) * GLD + lc) = rb0;         \
+    *reinterpret_cast<uint4*>(Bs + ((buf) * GN + lr + 64) * GLD + lc) = rb1;    \
+    *reinterpret_cast<uint4*>(Bs + ((buf) * GN + lr + 128) * GLD + lc) = rb2;   \
+    *reinterpret_cast<uint4*>(Bs + ((buf) * GN + lr + 192) * GLD + lc) = rb3;   \
+  } while (0)
+  TAV2_SSTORE(0);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * GK);
+    if (kt + 1 < nk) {
+      const int k1 = (kt + 1) * GK + lc;
+      ra = arow ? *reinterpret_cast<const uint4*>(arow + k1) : make_uint4(0, 0, 0, 0);
+      rb0 = *reinterpret_cast<const uint4*>(brow[0] + k1);
+      rb1 = *reinterpret_cast<const uint4*>(brow[1] + k1);
+      rb2 = *reinterpret_cast<const uint4*>(brow[2] + k1);
+      rb3 = *reinterpret_cast<const uint4*>(brow[3] + k1);
+    }
 #pragma unroll
     for (int kb = 0; kb < GK / 16; ++kb) {
       bf16x8 av[2], bv[2];
@@ -111,9 +117,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(ALoad al, const bf16_t* __res
 #pragma unroll
         for (int b = 0; b < 2; ++b) acc[a][b] = mfma32(av[a], bv[b], acc[a][b]);
     }
-    if (kt + 1 < nk) sstore(buf ^ 1);
+    if (kt + 1 < nk) TAV2_SSTORE(buf ^ 1);
     __syncthreads();
   }
+#undef TAV2_SSTORE
 
   // stage the fp32 tile: D register 4j + i of tile (a, b) is row a*32 + 8j + 4h + i,
   // column 64w + b*32 + l32

@@ -43,17 +43,26 @@ ProfScope::ProfScope(const char* name, hipStream_t st) : name_(name), st_(st), s
   if (!g_on.load(std::memory_order_relaxed)) return;
   std::lock_guard<std::mutex> lk(g_mu);
   if (!g_filter.empty() && g_filter != name) return;
-  start_ = take_event();
-  if (start_) hipEventRecord(static_cast<hipEvent_t>(start_), st_);
+  hipEvent_t e = take_event();
+  if (!e) return;
+  if (hipEventRecord(e, st_) != hipSuccess) {
+    g_free.push_back(e);
+    return;
+  }
+  start_ = e;
 }
 
 ProfScope::~ProfScope() {
   if (!start_) return;
   std::lock_guard<std::mutex> lk(g_mu);
+  hipEvent_t start = static_cast<hipEvent_t>(start_);
   hipEvent_t stop = take_event();
-  if (!stop) return;
-  hipEventRecord(stop, st_);
-  g_sites[name_].pairs.emplace_back(static_cast<hipEvent_t>(start_), stop);
+  if (!stop || hipEventRecord(stop, st_) != hipSuccess) {
+    g_free.push_back(start);
+    if (stop) g_free.push_back(stop);
+    return;
+  }
+  g_sites[name_].pairs.emplace_back(start, stop);
 }
 
 }  // namespace tav2

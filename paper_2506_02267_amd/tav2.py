@@ -346,9 +346,10 @@ def profile_enable(on: bool, site: Optional[str] = None):
 def profile_report() -> dict:
     """{site: (launches, total_ms)} since the last report; call after synchronising."""
     lib = load_library()
-    n = lib.tav2_profile_report(None, 0)
-    buf = ctypes.create_string_buffer(int(n) + 1)
-    lib.tav2_profile_report(buf, len(buf))
+    buf = ctypes.create_string_buffer(1 << 16)
+    n = lib.tav2_profile_report(buf, len(buf))
+    if n >= len(buf):
+        raise RuntimeError("profile report truncated")
     out = {}
     for line in buf.value.decode().splitlines():
         name, cnt, ms = line.split()
