@@ -51,6 +51,13 @@ def site_work(w, total, valid_tokens, max_len, launches_per_step):
     per["gemm_cand"] = ("flop", 2.0 * total * d * dm)
     T = w.T
     per["attention"] = ("flop", 4.0 * H * dh * total * T * (T + 1) / 2.0)
+    # the fused encoder: input projection (token half per token, candidate half per
+    # candidate), all layers (causal attention over valid positions) and the head
+    Tv = valid_tokens / max(total, 1)
+    per["encoder_fused"] = ("flop", 2.0 * valid_tokens * d * dm + 2.0 * total * d * dm
+                            + w.n_layers * (2.0 * M * (3 * dm * dm + dm * dm + 2 * ff * dm)
+                                            + 4.0 * H * dh * total * Tv * (Tv + 1) / 2.0)
+                            + 2.0 * M * dm * dm)
     per["score_bf16"] = ("flop", 2.0 * total * max_len * d)
     per["score_f32"] = ("flop", 2.0 * total * max_len * d)
     per["topk"] = ("byte", 4.0 * total * max_len)

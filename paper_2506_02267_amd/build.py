@@ -16,7 +16,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtav2.so")
-SOURCES = ["api.cpp", "profile.cpp", "select.hip", "gather.hip", "encoder_bf16.hip", "encoder_f32.hip"]
+SOURCES = ["api.cpp", "profile.cpp", "select.hip", "gather.hip", "encoder_bf16.hip", "encoder_fused.hip",
+           "encoder_f32.hip"]
 ARCH = "gfx950"
 
 

@@ -115,14 +115,18 @@ size_t select_ws_bytes(const tav2_seq* s, const tav2_cands* c) {
 
 size_t encode_ws_bytes(int64_t total, int T, const tav2_weights* w) {
   if (w->dtype == TAV2_F32) return 0;
+  if (encode_fused_supported(w->d_in, *w)) return align_up(encode_fused_workspace(total, T, *w), WS_ALIGN);
   return align_up(encode_bf16_workspace(total, T, *w), WS_ALIGN);
 }
 
 tav2_status run_encode(const TokenSource& src, const void* cand_emb, int64_t total,
                        const tav2_weights* w, float* out, void* ws, size_t ws_bytes,
                        hipStream_t st) {
-  if (w->dtype == TAV2_BF16)
+  if (w->dtype == TAV2_BF16) {
+    if (encode_fused_supported(w->d_in, *w))
+      return hip_status(launch_encode_fused(src, cand_emb, total, *w, out, ws, st));
     return hip_status(launch_encode_bf16(src, cand_emb, total, *w, out, ws, ws_bytes, st));
+  }
   return hip_status(launch_encode_f32(src, cand_emb, total, *w, out, st));
 }
 

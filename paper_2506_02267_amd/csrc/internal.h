@@ -72,6 +72,12 @@ hipError_t launch_encode_bf16(const TokenSource& src, const void* cand_emb, int6
                               const tav2_weights& w, float* out, void* ws, size_t ws_bytes,
                               hipStream_t st);
 
+// ---- encoder_fused.hip
+bool encode_fused_supported(int d, const tav2_weights& w);
+size_t encode_fused_workspace(int64_t total, int T, const tav2_weights& w);
+hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int64_t total,
+                               const tav2_weights& w, float* out, void* ws, hipStream_t st);
+
 // ---- encoder_f32.hip
 constexpr int F32_MAX_T = 64;
 constexpr int F32_MAX_DM = 128;

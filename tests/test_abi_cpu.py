@@ -88,7 +88,13 @@ def test_workspace_queries():
     w = fake_weights()
     tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
                    d=64, dtype=T.BF16, reserved=0)
-    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) > 10 * 64 * 256 * 4
+    # T <= 128: the fused bf16 encoder keeps everything on chip
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == 0
+    # T = 256: a K / V cache of layers x 2 x T x d_model bf16 per candidate
+    w256 = fake_weights(max_pos=256)
+    tok.T = 256
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w256)) == 10 * 2 * 2 * 256 * 256 * 2
+    tok.T = 64
     wf = fake_weights(dm=64, heads=2, ffn=128, layers=1, max_pos=32, dtype=T.F32, time=False)
     tokf = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=None, valid_len=FAKE, total=16, T=32,
                     d=64, dtype=T.F32, reserved=0)
@@ -176,7 +182,9 @@ def test_encode_argument_errors(case, status):
         w.dtype = T.F32
     elif case == "null_out":
         out = None
-    elif case == "ws":
+    elif case == "ws":       # T > 128 needs the K / V cache workspace
+        tok.T = 256
+        w.max_pos = 256
         wsb = 10
     elif case == "d_in":
         w.d_in = 32
