@@ -7,21 +7,26 @@
 //    causal mask a block depends on earlier blocks only through their keys and
 //    values, so each block runs through all layers in turn and leaves its K/V in a
 //    per-candidate cache (workspace) for the blocks after it.
-//  * 8 waves.  The fp32 residual stream of the block lives in registers as the
-//    transposed product X^T [feature x token] (MFMA accumulator layout: one token
-//    per lane, 4 consecutive features per register group), so LayerNorm over
-//    features is an in-lane sum, one cross-half exchange and a 4-way exchange
-//    between waves through LDS.
-//  * The bf16 copy of the block's activations (MFMA operand), the per-head-group
-//    Q / K / V^T, the attention output and the FFN hidden chunk live in LDS; weight
-//    tiles [rows x 32] stream from L2 through a double-buffered LDS stage with a
-//    register prefetch two steps ahead.
-//  * Every LDS write of an activation is 4 consecutive bf16 of one row (8 bytes):
-//    products whose consumer needs [token][feature] are computed transposed
-//    (weights as MFMA A operand); V is computed untransposed to give V^T [dim][token].
-//  * Attention: 16x16x32 MFMAs, wave w owns queries 16w .. 16w+15 of the block;
-//    S^T = K Q^T puts one query per lane column, and P^T goes back into
-//    O^T = V^T P^T from its accumulator registers with the matching key order.
+//  * 4 waves, one per SIMD, each with the full 512-register budget.  The fp32
+//    residual stream of the block lives in registers as the transposed product
+//    X^T [feature x token] (MFMA accumulator layout: one token per lane, 4
+//    consecutive features per register group); wave w owns features
+//    128 (w & 1) .. +127 of tokens 64 (w >> 1) .. +63.  LayerNorm over features is
+//    an in-lane sum, one cross-half exchange and a 2-way exchange through LDS.
+//  * Weights stream from L2 straight into registers: each call first packs every
+//    matrix into MFMA-fragment order (one 32 x 16 fragment = 1 KB contiguous,
+//    lane-major), so every fragment load is one coalesced 16-byte-per-lane load
+//    and no weight tile passes through LDS or a barrier.
+//  * LDS holds only activations: the bf16 copy of the block (MFMA operand), the
+//    head group's Q / K / V^T, the attention output, the FFN hidden chunk, and
+//    cached keys/values of earlier blocks during attention.  Every activation
+//    write is 4 consecutive bf16 of one row: products whose consumer needs
+//    [token][feature] are computed transposed (weights as MFMA A operand); V is
+//    computed untransposed to give V^T [dim][token].
+//  * Attention: 32x32x16 MFMAs, wave w owns queries 32w .. 32w+31 of the block;
+//    S^T = K Q^T puts one query per lane, so the softmax reductions are in-lane
+//    plus one exchange between lane halves, and P^T feeds O^T = V^T P^T straight
+//    from its accumulator registers with the matching key order.
 #include "common.h"
 #include "internal.h"
 #include "token_source.h"
@@ -31,70 +36,102 @@ namespace fz {
 
 constexpr int DM = 256;          // d_model
 constexpr int BT = 128;          // tokens per block
-constexpr int NT = 512;          // threads (8 waves)
-constexpr int KS = 32;           // k extent of one weight stage
+constexpr int NT = 256;          // threads (4 waves)
 constexpr int XLD = DM + 8;      // Xs row stride (bf16 elements)
-constexpr int WLD = KS + 8;      // weight stage row stride
-constexpr int WROWS = 256;       // rows per weight stage
 constexpr int QLD = 64 + 8;      // Qs / Ks / Os row stride (one 64-dim head group)
 constexpr int VLD = BT + 8;      // Vts row stride
 constexpr int FC = 128;          // FFN hidden units per chunk
 constexpr int HLD = FC + 8;      // Hs row stride
 constexpr int MAX_LAYERS = 8;
+constexpr int KIN = 256;         // packed width of the token half of W_in (d zero-padded)
 
 constexpr int XS_BYTES = BT * XLD * 2;                 // 67584
-constexpr int WS_BYTES = 2 * WROWS * WLD * 2;          // 40960
 constexpr int QS_BYTES = BT * QLD * 2;                 // 18432
 constexpr int VS_BYTES = 64 * VLD * 2;                 // 17408
 constexpr int SC_BYTES = 2 * QS_BYTES + VS_BYTES;      // 54272
+constexpr int CS_BYTES = QS_BYTES + VS_BYTES;          // 35840: cached K / V^T chunk
 constexpr int PM_BYTES = DM * 4;                       // running pooled max
-constexpr int LDS_BYTES = XS_BYTES + WS_BYTES + SC_BYTES + PM_BYTES;
+constexpr int LDS_BYTES = XS_BYTES + SC_BYTES + CS_BYTES + PM_BYTES;
 static_assert(LDS_BYTES <= 163840, "fused encoder exceeds the 160 KiB of LDS");
 static_assert(BT * HLD * 2 <= SC_BYTES, "FFN chunk does not fit the scratch region");
-static_assert(2 * BT * 4 * 4 + 2 * DM * 4 <= SC_BYTES, "reduction buffers do not fit");
+static_assert(BT * 8 + BT * 8 <= SC_BYTES, "encoding buffers do not fit");
 
-typedef float f32x4v __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ f32x4v mfma16(const bf16x8& a, const bf16x8& b, const f32x4v& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-// The thread index through an empty asm: index and address arithmetic derived from
-// it is recomputed inside each phase instead of being hoisted out of the block and
-// layer loops (which would keep it live, and spilled, across the whole kernel).
+// The thread index through an empty asm: index and address arithmetic derived
+// from it is recomputed inside each phase instead of being hoisted out of the
+// block and layer loops (which would keep it live across the whole kernel).
 __device__ __forceinline__ int otid() {
   int t = threadIdx.x;
   asm volatile("" : "+v"(t));
   return t;
 }
 
-// Per-phase lane coordinates: lane, wave (uniform), half, column-in-half, and the
-// residual tile coordinates fq (feature quarter) and th (token half).
 #define FZ_LANE_VARS                                                      \
   const int tid_ = otid();                                                \
   const int lane = tid_ % WAVE;                                           \
   const int w = __builtin_amdgcn_readfirstlane(tid_ / WAVE);              \
   const int hf = lane / 32, l32 = lane % 32;                              \
-  const int fq = w & 3, th = w >> 2;                                      \
-  (void)hf; (void)l32; (void)fq; (void)th;
+  const int fh = w & 1, th = w >> 1;                                      \
+  (void)hf; (void)l32; (void)fh; (void)th;
 
-__device__ __forceinline__ bf16x8 frag(const bf16_t* p) {
+__device__ __forceinline__ bf16x8 lfrag(const bf16_t* p) {   // 16 bytes from LDS
   return as_bf16x8(*reinterpret_cast<const uint4*>(p));
+}
+// Fragment (rt, kb) of a packed matrix with nkb k-blocks: 64 lanes x 16 bytes.
+__device__ __forceinline__ bf16x8 gfrag(const bf16_t* P, int nkb, int rt, int kb, int lane) {
+  return __builtin_bit_cast(
+      bf16x8, *reinterpret_cast<const u32x4*>(P + ((int64_t(rt) * nkb + kb) * 64 + lane) * 8));
 }
 __device__ __forceinline__ void st4(bf16_t* p, float a, float b, float c, float d) {
   *reinterpret_cast<uint2*>(p) = make_uint2(pack2(a, b), pack2(c, d));
 }
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Partner values across lane halves without LDS: the gfx950 permlane swaps of a
+// register with itself leave {v[l], v[l ^ 32]} (or {v[l], v[l ^ 16]}) in the pair.
+__device__ __forceinline__ float xmax32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xmax16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xsum32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xsum16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+struct LayerPk {
+  const bf16_t* qkv;    // [768 rows][16 kb]
+  const bf16_t* o;      // [256][16]
+  const bf16_t* w1;     // [ffn][16]
+  const bf16_t* w2;     // [256][ffn / 16]
+};
 
 struct Args {
   TokenSource s;
   const bf16_t* cand;       // [total, d]
-  const bf16_t* W_in;       // [DM, 2d]
+  const bf16_t* W_in;       // [DM, 2d] (candidate half read directly)
   const float* b_in;
   const bf16_t* E_act;
   const bf16_t* E_time;     // may be null
   const bf16_t* E_pos;
-  const bf16_t* W_pool;
   const float* b_pool;
-  tav2_layer layers[MAX_LAYERS];
+  const float* cvec;        // [chunk, DM]: c W_in[:, d:]^T + b_in per candidate
+  const bf16_t* pk_in;      // packed token half of W_in, [256][KIN / 16]
+  const bf16_t* pk_pool;    // packed W_pool
+  tav2_layer layers[MAX_LAYERS];   // biases and LayerNorm vectors
+  LayerPk pk[MAX_LAYERS];
   int n_layers;
   int d;
   int dh;                   // head width, 32 or 64
@@ -106,90 +143,108 @@ struct Args {
   float* out;               // [total, 2 DM]
 };
 
-// ---------------------------------------------------------------- weight staging
-// A [R x 32] bf16 tile moves as 16-byte items, 4 per row; thread t owns items t
-// and t + NT.  Items travel in native vector registers (no arrays, no references)
-// so they stay in VGPRs while the loads are in flight.
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+// ---------------------------------------------------------------- weight stream
+// Every GEMM phase reads its weight fragments from L2 PD k-blocks ahead, and its
+// last PD iterations already load the first PD k-blocks of the NEXT phase into
+// `pre`, so the stream keeps running across phase boundaries (attention,
+// LayerNorm and block boundaries included) instead of refilling at each phase.
+constexpr int PD = 4;                    // prefetch depth in k-blocks
+typedef bf16x8 Pre[PD][4];
 
-#define FZ_WLOAD(RA, RB, ROWS, R, K0)                                                   \
-  do {                                                                                  \
-    if (wt_ < (R) * 4)                                                                  \
-      RA = *reinterpret_cast<const u32x4*>(ROWS(wt_ >> 2) + (K0) + (wt_ & 3) * 8);      \
-    if (wt_ + NT < (R) * 4)                                                             \
-      RB = *reinterpret_cast<const u32x4*>(ROWS((wt_ + NT) >> 2) + (K0) + (wt_ & 3) * 8); \
-  } while (0)
+struct WSeg {                            // a phase's weight fragments: up to 4 row tiles
+  const bf16_t* P;                       // packed matrix
+  int nkb;                               // k-blocks per row of P
+  int kb0;                               // first k-block of the phase
+  int nr;                                // row tiles used (1..4)
+  int r0, r1, r2, r3;                    // packed row tiles
+};
 
-#define FZ_WSTORE(RA, RB, BUF, R)                                                       \
-  do {                                                                                  \
-    if (wt_ < (R) * 4)                                                                  \
-      *reinterpret_cast<u32x4*>(Ws + ((BUF) * WROWS + (wt_ >> 2)) * WLD + (wt_ & 3) * 8) = RA; \
-    if (wt_ + NT < (R) * 4)                                                             \
-      *reinterpret_cast<u32x4*>(Ws + ((BUF) * WROWS + ((wt_ + NT) >> 2)) * WLD + (wt_ & 3) * 8) = RB; \
-  } while (0)
-
-// Streams R weight rows x K columns through the two LDS stages.  BODY runs once
-// per 32-wide k step with `stage` (the resident [R x 32] tile) and `k0` defined.
-// The register prefetch runs two steps ahead; the loop is unrolled by two so the
-// two register sets alternate without copies.  Ends with a barrier.
-#define FZ_STREAM(ROWS, R, K, BODY)                                             \
-  do {                                                                          \
-    const int nks_ = (K) / KS;                                                  \
-    const int wt_ = otid();                                                     \
-    u32x4 r0a_ = {}, r0b_ = {}, r1a_ = {}, r1b_ = {};                           \
-    FZ_WLOAD(r1a_, r1b_, ROWS, R, 0);                                           \
-    if (nks_ > 1) FZ_WLOAD(r0a_, r0b_, ROWS, R, KS);                            \
-    FZ_WSTORE(r1a_, r1b_, 0, R);                                                \
-    __syncthreads();                                                            \
-    for (int ks_ = 0; ks_ < nks_; ks_ += 2) {                                   \
-      if (ks_ + 2 < nks_) FZ_WLOAD(r1a_, r1b_, ROWS, R, (ks_ + 2) * KS);        \
-      {                                                                         \
-        const bf16_t* stage = Ws + (ks_ & 1) * WROWS * WLD;                     \
-        const int k0 = ks_ * KS;                                                \
-        BODY                                                                    \
-      }                                                                         \
-      if (ks_ + 1 < nks_) FZ_WSTORE(r0a_, r0b_, (ks_ + 1) & 1, R);              \
-      __syncthreads();                                                          \
-      if (ks_ + 1 >= nks_) break;                                               \
-      if (ks_ + 3 < nks_) FZ_WLOAD(r0a_, r0b_, ROWS, R, (ks_ + 3) * KS);        \
-      {                                                                         \
-        const bf16_t* stage = Ws + ((ks_ + 1) & 1) * WROWS * WLD;               \
-        const int k0 = (ks_ + 1) * KS;                                          \
-        BODY                                                                    \
-      }                                                                         \
-      if (ks_ + 2 < nks_) FZ_WSTORE(r1a_, r1b_, (ks_ + 2) & 1, R);              \
-      __syncthreads();                                                          \
-    }                                                                           \
-  } while (0)
-
-// C^T[256 feature x 128 token] += W[256 x K] . ACT[128 x K]^T; wave tile
-// 64 features (fq) x 64 tokens (th) as acc[feature tile][token tile].
-#define FZ_RESID_BODY(ACT, ALD)                                                          \
-  _Pragma("unroll") for (int kb = 0; kb < KS / 16; ++kb) {                                \
-    bf16x8 wa_[2], xb_[2];                                                                \
-    _Pragma("unroll") for (int t = 0; t < 2; ++t) {                                       \
-      wa_[t] = frag(stage + (fq * 64 + t * 32 + l32) * WLD + kb * 16 + 8 * hf);           \
-      xb_[t] = frag((ACT) + (th * 64 + t * 32 + l32) * (ALD) + k0 + kb * 16 + 8 * hf);    \
-    }                                                                                     \
-    _Pragma("unroll") for (int a = 0; a < 2; ++a)                                         \
-      _Pragma("unroll") for (int b = 0; b < 2; ++b) acc[a][b] = mfma32(wa_[a], xb_[b], acc[a][b]); \
+__device__ __forceinline__ int seg_rt(const WSeg& s, int f) {
+  return f == 0 ? s.r0 : f == 1 ? s.r1 : f == 2 ? s.r2 : s.r3;
+}
+// k-block `slot` of segment s into pre[slot]
+__device__ __forceinline__ void seg_load(Pre& pre, int slot, const WSeg& s, int lane) {
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+    if (f < s.nr) pre[slot][f] = gfrag(s.P, s.nkb, seg_rt(s, f), s.kb0 + slot, lane);
+}
+__device__ __forceinline__ void seg_prime(Pre& pre, const WSeg& s, int lane) {
+#pragma unroll
+  for (int j = 0; j < PD; ++j) seg_load(pre, j, s, lane);
+}
+// residual-shaped phase of wave w: row tiles 4 (w & 1) + 0..3
+__device__ __forceinline__ WSeg seg_resid(const bf16_t* P, int nkb, int kb0, int w) {
+  const int r = 4 * (w & 1);
+  return WSeg{P, nkb, kb0, 4, r, r + 1, r + 2, r + 3};
+}
+// FFN first layer, chunk c: hidden row tiles 4c + 2(w & 1) + 0..1
+__device__ __forceinline__ WSeg seg_ffn1(const bf16_t* P, int c, int w) {
+  const int r = c * (128 / 32) + 2 * (w & 1);
+  return WSeg{P, 256 / 16, 0, 2, r, r + 1, 0, 0};
+}
+// Q / K / V of head group g: column tiles 3(w >> 1) + 0..2 of [q0 q1 k0 k1 v0 v1]
+// are packed row tiles 8 part + 2g + dt
+__device__ __forceinline__ WSeg seg_qkv(const bf16_t* P, int g, int w) {
+  int r[3];
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const int ct = 3 * (w >> 1) + t;
+    r[t] = 8 * (ct >> 1) + 2 * g + (ct & 1);
   }
+  return WSeg{P, 256 / 16, 0, 3, r[0], r[1], r[2], 0};
+}
+
+// acc[ft][tt] += C^T: features 128 fh + 32 ft (packed rows of cur), tokens
+// 64 th + 32 tt (rows of ACT in LDS, columns 16 j), over NKB k-blocks.
+template <int NKB>
+__device__ __forceinline__ void resid_phase(f32x16 (&acc)[4][2], Pre& pre, const WSeg& cur,
+                                            const WSeg& nxt, const bf16_t* ACT, int ald) {
+  static_assert(NKB >= PD, "phase shorter than the prefetch depth");
+  FZ_LANE_VARS
+  bf16x8 wq[NKB][4];
+  bf16x8 xq[NKB][2];
+  const bf16_t* arow = ACT + (th * 64 + l32) * ald + 8 * hf;
+  xq[0][0] = lfrag(arow);
+  xq[0][1] = lfrag(arow + 32 * ald);
+#pragma unroll
+  for (int j = 0; j < NKB; ++j) {
+    bf16x8 a[4];
+#pragma unroll
+    for (int f = 0; f < 4; ++f) a[f] = j < PD ? pre[j][f] : wq[j][f];
+    if (j + PD < NKB) {
+#pragma unroll
+      for (int f = 0; f < 4; ++f) wq[j + PD][f] = gfrag(cur.P, cur.nkb, seg_rt(cur, f), cur.kb0 + j + PD, lane);
+    } else {
+      seg_load(pre, j + PD - NKB, nxt, lane);
+    }
+    if (j + 1 < NKB) {
+      xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
+      xq[j + 1][1] = lfrag(arow + 32 * ald + (j + 1) * 16);
+    }
+#pragma unroll
+    for (int ft = 0; ft < 4; ++ft) {
+      acc[ft][0] = mfma32(a[ft], xq[j][0], acc[ft][0]);
+      acc[ft][1] = mfma32(a[ft], xq[j][1], acc[ft][1]);
+    }
+    sched_fence();
+  }
+}
 
 // ---------------------------------------------------------------- LayerNorm
-// acc holds C^T (features x tokens) of the block without the sublayer bias.
-// x <- LN(acc + bias) with gain g and offset b; Xs <- bf16(x).  Ends with a barrier.
-__device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][2], const float* bias,
+// x <- LN(acc + bias) with gain g and offset b over the 256 features of every
+// token; Xs <- bf16(x).  Ends with a barrier.
+__device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* bias,
                                            const float* g, const float* b, float* red,
                                            bf16_t* Xs) {
   FZ_LANE_VARS
   float s[2] = {0.f, 0.f}, ss[2] = {0.f, 0.f};
 #pragma unroll
-  for (int tt = 0; tt < 2; ++tt)
+  for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
-    for (int ft = 0; ft < 2; ++ft)
+    for (int j = 0; j < 4; ++j) {
+      const float4 bi = *reinterpret_cast<const float4*>(bias + fh * 128 + ft * 32 + 8 * j + 4 * hf);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float4 bi = *reinterpret_cast<const float4*>(bias + fq * 64 + ft * 32 + 8 * j + 4 * hf);
+      for (int tt = 0; tt < 2; ++tt) {
         const float v0 = acc[ft][tt][4 * j] + bi.x;
         const float v1 = acc[ft][tt][4 * j + 1] + bi.y;
         const float v2 = acc[ft][tt][4 * j + 2] + bi.z;
@@ -201,18 +256,17 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][2], const float* bia
         s[tt] += (v0 + v1) + (v2 + v3);
         ss[tt] += (v0 * v0 + v1 * v1) + (v2 * v2 + v3 * v3);
       }
+    }
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
-    s[tt] += __shfl_xor(s[tt], 32, WAVE);
-    ss[tt] += __shfl_xor(ss[tt], 32, WAVE);
+    s[tt] = xsum32(s[tt]);
+    ss[tt] = xsum32(ss[tt]);
   }
-  // red[tok][fq] = (sum, sumsq) over this wave's 64 features
-  if (hf == 0) {
+  if (hf == 0) {   // red[tok][fh] = (sum, sumsq) over this wave's 128 features
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
       const int tok = th * 64 + tt * 32 + l32;
-      red[(tok * 4 + fq) * 2] = s[tt];
-      red[(tok * 4 + fq) * 2 + 1] = ss[tt];
+      *reinterpret_cast<float2*>(red + (tok * 2 + fh) * 2) = make_float2(s[tt], ss[tt]);
     }
   }
   __syncthreads();
@@ -220,23 +274,20 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][2], const float* bia
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
     const int tok = th * 64 + tt * 32 + l32;
-    const float4 a = *reinterpret_cast<const float4*>(red + tok * 8);
-    const float4 c = *reinterpret_cast<const float4*>(red + tok * 8 + 4);
-    const float sum = (a.x + a.z) + (c.x + c.z);
-    const float sq = (a.y + a.w) + (c.y + c.w);
-    mean[tt] = sum * (1.f / DM);
-    const float var = fmaxf(sq * (1.f / DM) - mean[tt] * mean[tt], 0.f);
+    const float4 a = *reinterpret_cast<const float4*>(red + tok * 4);
+    mean[tt] = (a.x + a.z) * (1.f / DM);
+    const float var = fmaxf((a.y + a.w) * (1.f / DM) - mean[tt] * mean[tt], 0.f);
     rstd[tt] = rsqrtf(var + 1e-5f);
   }
 #pragma unroll
-  for (int tt = 0; tt < 2; ++tt)
+  for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
-    for (int ft = 0; ft < 2; ++ft)
+    for (int j = 0; j < 4; ++j) {
+      const int f = fh * 128 + ft * 32 + 8 * j + 4 * hf;
+      const float4 gg = *reinterpret_cast<const float4*>(g + f);
+      const float4 bb = *reinterpret_cast<const float4*>(b + f);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int f = fq * 64 + ft * 32 + 8 * j + 4 * hf;
-        const float4 gg = *reinterpret_cast<const float4*>(g + f);
-        const float4 bb = *reinterpret_cast<const float4*>(b + f);
+      for (int tt = 0; tt < 2; ++tt) {
         const float v0 = (acc[ft][tt][4 * j] - mean[tt]) * rstd[tt] * gg.x + bb.x;
         const float v1 = (acc[ft][tt][4 * j + 1] - mean[tt]) * rstd[tt] * gg.y + bb.y;
         const float v2 = (acc[ft][tt][4 * j + 2] - mean[tt]) * rstd[tt] * gg.z + bb.z;
@@ -245,17 +296,17 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][2], const float* bia
         acc[ft][tt][4 * j + 1] = v1;
         acc[ft][tt][4 * j + 2] = v2;
         acc[ft][tt][4 * j + 3] = v3;
-        st4(Xs + (th * 64 + tt * 32 + l32) * XLD + fq * 64 + ft * 32 + 8 * j + 4 * hf, v0, v1, v2,
-            v3);
+        st4(Xs + (th * 64 + tt * 32 + l32) * XLD + f, v0, v1, v2, v3);
       }
+    }
   __syncthreads();
 }
 
 // ---------------------------------------------------------------- pooling
 // Max over the block's valid tokens (token < nvalid) of Y^T = acc + b_pool, folded
-// into pmax.  The 32 per-lane features are max-reduced across the 32 lanes of a
-// half with a transposing butterfly, so lane l32 ends with feature index
-// bitrev5(l32) of its half.  Ends with a barrier.
+// into pmax.  The 64 per-lane features are max-reduced across the 32 lanes of a
+// half with a transposing butterfly (each step halves the values a lane keeps).
+// Ends with a barrier.
 #define FZ_TMAX(HALF, MASK)                                                   \
   _Pragma("unroll") for (int k = 0; k < (HALF); ++k) {                        \
     const bool up = (l32 & (MASK)) != 0;                                      \
@@ -264,12 +315,12 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][2], const float* bia
     v[k] = fmaxf(keep, __shfl_xor(send, (MASK), WAVE));                       \
   }
 
-__device__ __forceinline__ void pool_block(f32x16 (&acc)[2][2], const float* b_pool, float* pmax,
+__device__ __forceinline__ void pool_block(f32x16 (&acc)[4][2], const float* b_pool, float* pmax,
                                            float* red, int nvalid) {
   FZ_LANE_VARS
-  float v[32];
+  float v[64];
 #pragma unroll
-  for (int ft = 0; ft < 2; ++ft)
+  for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       float m = -__builtin_inff();
@@ -278,16 +329,22 @@ __device__ __forceinline__ void pool_block(f32x16 (&acc)[2][2], const float* b_p
         if (th * 64 + tt * 32 + l32 < nvalid) m = fmaxf(m, acc[ft][tt][r]);
       v[ft * 16 + r] = m;
     }
-  FZ_TMAX(16, 1)
-  FZ_TMAX(8, 2)
-  FZ_TMAX(4, 4)
-  FZ_TMAX(2, 8)
-  FZ_TMAX(1, 16)
-  const int k = ((l32 & 1) << 4) | ((l32 & 2) << 2) | (l32 & 4) | ((l32 & 8) >> 2) | ((l32 & 16) >> 4);
-  const int f = fq * 64 + (k >> 4) * 32 + 8 * ((k & 15) >> 2) + 4 * hf + (k & 3);
-  red[th * DM + f] = v[0] + b_pool[f];
+  FZ_TMAX(32, 1)
+  FZ_TMAX(16, 2)
+  FZ_TMAX(8, 4)
+  FZ_TMAX(4, 8)
+  FZ_TMAX(2, 16)
+  // this lane now holds value indices base and base + 1 of its 64
+  const int base = ((l32 & 1) << 5) | ((l32 & 2) << 3) | ((l32 & 4) << 1) | ((l32 & 8) >> 1) |
+                   ((l32 & 16) >> 3);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int k = base + u;
+    const int f = fh * 128 + (k >> 4) * 32 + 8 * ((k & 15) >> 2) + 4 * hf + (k & 3);
+    red[th * DM + f] = v[u] + b_pool[f];
+  }
   __syncthreads();
-  if (tid_ < DM) {
+  {
     const int c = tid_;
     pmax[c] = fmaxf(pmax[c], fmaxf(red[c], red[DM + c]));
   }
@@ -295,174 +352,212 @@ __device__ __forceinline__ void pool_block(f32x16 (&acc)[2][2], const float* b_p
 }
 
 // ---------------------------------------------------------------- attention
-// Causal attention of one head (columns col0 .. col0 + DH of the 64-dim group)
-// for the block's 128 queries; wave w owns queries 16w .. 16w+15.  Keys before
-// the block come from the cache, keys of the block from Ks / Vts.  The output
-// overwrites the wave's own rows of Qs (already read into registers).
-template <int DH>
-__device__ __forceinline__ void attend_head(int g, int col0, int p0, bf16_t* Qs, const bf16_t* Ks,
-                                            const bf16_t* Vts, const bf16_t* kc,
-                                            const bf16_t* vc, int tpad) {
-  FZ_LANE_VARS
-  const int gq = lane / 16, c16 = lane % 16;
-  const int qrow = 16 * w + c16;
-  bf16x8 qf[DH / 32];
-#pragma unroll
-  for (int kb = 0; kb < DH / 32; ++kb) qf[kb] = frag(Qs + qrow * QLD + col0 + 32 * kb + 8 * gq);
-  f32x4v o[DH / 16];
-#pragma unroll
-  for (int t = 0; t < DH / 16; ++t) o[t] = f32x4v{0.f, 0.f, 0.f, 0.f};
-  float mrun = -__builtin_inff(), lrun = 0.f;
-  const float sc = rsqrtf(float(DH)) * 1.4426950408889634f;
+// Causal attention of the block's 128 queries in 8 tiles of 16; wave w owns tiles
+// w and 7 - w, which together need the same number of causal key steps for every
+// wave.  16x16x32 MFMAs: S^T tile = 16 keys x 16 queries, one query per lane
+// column, keys 4 (lane / 16) + i in the tile's 4 registers.
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f32x4v mfma16(const bf16x8& a, const bf16x8& b, const f32x4v& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
 
-  // keys cached from earlier blocks: all visible
-  for (int k0 = 0; k0 < p0; k0 += 32) {
-    f32x4v s[2];
+template <int DH>
+struct AttnState {
+  bf16x8 qf[DH / 32];   // Q^T fragments (32 dims x 16 queries each)
+  f32x4v o[DH / 16];    // O^T accumulators (16 dims x 16 queries each)
+  float m, l;           // running max (log2 units) and this lane's partial sum
+};
+
+template <int DH>
+__device__ __forceinline__ void attn_init(AttnState<DH>& st, const bf16_t* Qs, int col0, int qt) {
+  const int lane = otid() % WAVE;
+  const int gq = lane / 16, c16 = lane % 16;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      s[t] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  for (int kb = 0; kb < DH / 32; ++kb)
+    st.qf[kb] = lfrag(Qs + (16 * qt + c16) * QLD + col0 + 32 * kb + 8 * gq);
 #pragma unroll
-      for (int kb = 0; kb < DH / 32; ++kb) {
-        const bf16x8 kf = frag(kc + int64_t(k0 + 16 * t + c16) * DM + g * 64 + col0 + 32 * kb + 8 * gq);
-        s[t] = mfma16(kf, qf[kb], s[t]);
-      }
-    }
-    float mx = -__builtin_inff();
+  for (int t = 0; t < DH / 16; ++t) st.o[t] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  st.m = -__builtin_inff();
+  st.l = 0.f;
+}
+
+// One 32-key step at key k0 of K (LDS [key][kld], head dims at col0) and V^T (LDS
+// [dim][vld]) for query tile qt.  S^T tile t holds keys k0 + 16t + 4gq + i; the P^T
+// fragment takes them in that order (keys 4gq.., then 16 + 4gq..) and V^T is read
+// to match.  CAUSAL masks keys above the lane's query row (only a step that
+// reaches past the tile's first query has any).  Scores stay unscaled until the
+// exponent: max(s) scaled equals the max of the scaled scores, and the scale and
+// the max are applied by one fma.  exp2 is the hardware instruction (results
+// below 2^-126 flush to zero, far under the bf16 resolution of P).
+template <int DH, bool CAUSAL>
+__device__ __forceinline__ void attn_step(AttnState<DH>& st, const bf16_t* Kl, int kld,
+                                          const bf16_t* Vl, int vld, int col0, int k0, int qt,
+                                          int lane) {
+  const int gq = lane / 16, c16 = lane % 16;
+  constexpr float sc = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
+  f32x4v s[2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+  for (int t = 0; t < 2; ++t) {
+    s[t] = f32x4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        s[t][i] *= sc;
-        mx = fmaxf(mx, s[t][i]);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
-    const float mnew = fmaxf(mrun, mx);
-    const float alpha = exp2f(mrun - mnew);
-    bf16x8 pb;
-    float psum = 0.f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = exp2f(s[t][i] - mnew);
-        psum += p;
-        pb[4 * t + i] = static_cast<__bf16>(p);
-      }
-    lrun = lrun * alpha + psum;
-    mrun = mnew;
-#pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) {
-      o[dt] *= alpha;
-      const bf16_t* vr = vc + int64_t(g * 64 + col0 + 16 * dt + c16) * tpad + k0 + 4 * gq;
-      const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-      const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-      o[dt] = mfma16(as_bf16x8(lo, hi), pb, o[dt]);
-    }
+    for (int kb = 0; kb < DH / 32; ++kb)
+      s[t] = mfma16(lfrag(Kl + (k0 + 16 * t + c16) * kld + col0 + 32 * kb + 8 * gq), st.qf[kb], s[t]);
   }
-  // keys of this block up to the wave's last query, causal mask inside
-  const int kend = 16 * w + 16;
-  for (int k0 = 0; k0 < kend; k0 += 32) {
-    f32x4v s[2];
+  bf16x8 vf[DH / 16];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      s[t] = f32x4v{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < DH / 32; ++kb) {
-        const bf16x8 kf = frag(Ks + (k0 + 16 * t + c16) * QLD + col0 + 32 * kb + 8 * gq);
-        s[t] = mfma16(kf, qf[kb], s[t]);
-      }
-    }
-    float mx = -__builtin_inff();
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = k0 + 16 * t + 4 * gq + i;
-        s[t][i] = key > qrow ? -__builtin_inff() : s[t][i] * sc;
-        mx = fmaxf(mx, s[t][i]);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
-    const float mnew = fmaxf(mrun, mx);
-    const float alpha = exp2f(mrun - mnew);
-    bf16x8 pb;
-    float psum = 0.f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float p = exp2f(s[t][i] - mnew);
-        psum += p;
-        pb[4 * t + i] = static_cast<__bf16>(p);
-      }
-    lrun = lrun * alpha + psum;
-    mrun = mnew;
-#pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) {
-      o[dt] *= alpha;
-      const bf16_t* vr = Vts + (col0 + 16 * dt + c16) * VLD + k0 + 4 * gq;
-      const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-      const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-      o[dt] = mfma16(as_bf16x8(lo, hi), pb, o[dt]);
-    }
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    const bf16_t* vr = Vl + (col0 + 16 * dt + c16) * vld + k0 + 4 * gq;
+    vf[dt] = as_bf16x8(*reinterpret_cast<const uint2*>(vr), *reinterpret_cast<const uint2*>(vr + 16));
   }
-  float l = lrun + __shfl_xor(lrun, 16, WAVE);
-  l += __shfl_xor(l, 32, WAVE);
+  if (CAUSAL && k0 + 32 > 16 * qt) {   // wave-uniform
+    const int qrow = 16 * qt + c16;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (k0 + 16 * t + 4 * gq + i > qrow) s[t][i] = -__builtin_inff();
+  }
+  float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                   fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+  mx = xmax32(xmax16(mx));
+  const float mnew = fmaxf(st.m, mx * sc);
+  const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
+  bf16x8 pb;
+  float psum = 0.f;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float p = __builtin_amdgcn_exp2f(fmaf(s[t][i], sc, -mnew));
+      psum += p;
+      pb[4 * t + i] = static_cast<__bf16>(p);
+    }
+  st.l = st.l * alpha + psum;
+  st.m = mnew;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = mfma16(vf[dt], pb, st.o[dt] * alpha);
+}
+
+// O = O^T / l into the tile's rows of Qs (the tile's Q is already in registers).
+template <int DH>
+__device__ __forceinline__ void attn_finish(AttnState<DH>& st, bf16_t* Qs, int col0, int qt) {
+  const int lane = otid() % WAVE;
+  const int gq = lane / 16, c16 = lane % 16;
+  const float l = xsum32(xsum16(st.l));
   const float inv = 1.f / l;
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt)
-    st4(Qs + qrow * QLD + col0 + 16 * dt + 4 * gq, o[dt][0] * inv, o[dt][1] * inv, o[dt][2] * inv,
-        o[dt][3] * inv);
+    st4(Qs + (16 * qt + c16) * QLD + col0 + 16 * dt + 4 * gq, st.o[dt][0] * inv, st.o[dt][1] * inv,
+        st.o[dt][2] * inv, st.o[dt][3] * inv);
 }
 
-// ---------------------------------------------------------------- the kernel
-// Feature encoding of block rows [p0, p0 + BT): token rows into Xs, then
-// acc = X0^T = W_in[:, :d] Xs^T + c W_in[:, d:]^T + b_in + E_act + E_time + E_pos
-// (zero for positions past the valid length), and Xs <- bf16(X0).
+// Cached keys [c0, c0 + 128) of head group g (K rows and V^T columns) into LDS.
+// Ends with a barrier.
+__device__ __forceinline__ void stage_cached(const bf16_t* kc, const bf16_t* vc, int tpad, int g,
+                                             int c0, bf16_t* Kc, bf16_t* Vc) {
+  const int tid = otid();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = tid + q * NT;                      // K: 128 keys x 8 pieces
+    const int r = e >> 3, c = (e & 7) * 8;
+    *reinterpret_cast<u32x4*>(Kc + r * QLD + c) =
+        *reinterpret_cast<const u32x4*>(kc + int64_t(c0 + r) * DM + g * 64 + c);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = tid + q * NT;                      // V^T: 64 dims x 16 pieces
+    const int r = e >> 4, c = (e & 15) * 8;
+    *reinterpret_cast<u32x4*>(Vc + r * VLD + c) =
+        *reinterpret_cast<const u32x4*>(vc + int64_t(g * 64 + r) * tpad + c0 + c);
+  }
+  __syncthreads();
+}
+
+template <int DH>
+__device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf16_t* Ks,
+                                             const bf16_t* Vts, const bf16_t* kc,
+                                             const bf16_t* vc, int tpad, bf16_t* Kc, bf16_t* Vc) {
+  constexpr int NH = 64 / DH;
+  const int lane = otid() % WAVE;
+  const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
+  const int qa = w, qb = 7 - w;      // qa < qb
+#pragma unroll
+  for (int hd = 0; hd < NH; ++hd) {
+    AttnState<DH> sa, sb;
+    attn_init<DH>(sa, Qs, hd * DH, qa);
+    attn_init<DH>(sb, Qs, hd * DH, qb);
+    for (int c0 = 0; c0 < p0; c0 += BT) {     // earlier blocks: every key visible
+      stage_cached(kc, vc, tpad, g, c0, Kc, Vc);
+      for (int k0 = 0; k0 < BT; k0 += 32) {
+        attn_step<DH, false>(sa, Kc, QLD, Vc, VLD, hd * DH, k0, qa, lane);
+        attn_step<DH, false>(sb, Kc, QLD, Vc, VLD, hd * DH, k0, qb, lane);
+      }
+      __syncthreads();
+    }
+    const int na = 16 * qa + 16, nb = 16 * qb + 16;
+    for (int k0 = 0; k0 < nb; k0 += 32) {
+      if (k0 < na) attn_step<DH, true>(sa, Ks, QLD, Vts, VLD, hd * DH, k0, qa, lane);
+      attn_step<DH, true>(sb, Ks, QLD, Vts, VLD, hd * DH, k0, qb, lane);
+    }
+    attn_finish<DH>(sa, Qs, hd * DH, qa);
+    attn_finish<DH>(sb, Qs, hd * DH, qb);
+  }
+}
+
+__device__ __forceinline__ int64_t nl_of(const Args& A, int64_t n) { return n - A.c0; }
+
+// ---------------------------------------------------------------- block input
+// Feature encoding of block rows [p0, p0 + BT): token rows into Xs (zeros past the
+// valid length and past d), then acc = X0^T = W_in[:, :d] Xs^T + cvec + E_act +
+// E_time + E_pos (zero for padding positions), Xs <- bf16(X0).  cvec (the
+// candidate half of the projection plus b_in) is computed once per candidate by
+// cand_proj_kernel.
 __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int p0, int Tv,
-                                                   f32x16 (&acc)[2][2], bf16_t* Xs, bf16_t* Ws,
-                                                   float* cvec, int* tinfo) {
+                                                   f32x16 (&acc)[4][2], bf16_t* Xs,
+                                                   int* tinfo, const uint8_t** rowptr, Pre& pre,
+                                                   const WSeg& nxt) {
   const int d = A.d;
   {
     const int tid = otid();
-    for (int e = tid; e < BT * (d / 8); e += NT) {
-      const int r = e / (d / 8), c = e % (d / 8);
-      const int p = p0 + r;
-      uint4 v = make_uint4(0, 0, 0, 0);
+    if (tid < BT) {   // resolve each row once: its embedding row and act / time
+      const int p = p0 + tid;
+      const uint8_t* rp = nullptr;
+      int info = 0;
       if (p < Tv) {
         const TokenRef t = resolve_token(A.s, n, p, d * 2);
-        if (t.emb) v = reinterpret_cast<const uint4*>(t.emb)[c];
-        if (c == 0) tinfo[r] = t.act | (t.time << 8) | (1 << 16);
-      } else if (c == 0) {
-        tinfo[r] = 0;
+        rp = t.emb;
+        info = t.act | (t.time << 8) | (1 << 16);
       }
-      *reinterpret_cast<uint4*>(Xs + r * XLD + c * 8) = v;
+      rowptr[tid] = rp;
+      tinfo[tid] = info;
     }
-    if (tid < DM) {   // candidate half of the input projection: c W_in[:, d:]^T + b_in
-      const bf16_t* wr = A.W_in + int64_t(tid) * 2 * d + d;
-      const bf16_t* cr = A.cand + n * d;
-      float s = A.b_in[tid];
-      for (int j = 0; j < d; j += 8) {
-        const uint4 wv = *reinterpret_cast<const uint4*>(wr + j);
-        const uint4 cv = *reinterpret_cast<const uint4*>(cr + j);
-        const bf16_t* wp = reinterpret_cast<const bf16_t*>(&wv);
-        const bf16_t* cp = reinterpret_cast<const bf16_t*>(&cv);
+    __syncthreads();
+    // all of the thread's row pieces in flight at once, then into LDS
+    constexpr int PER = BT * (KIN / 8) / NT;
+    u32x4 v[PER];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) s = fmaf(bf2f(wp[u]), bf2f(cp[u]), s);
-      }
-      cvec[tid] = s;
+    for (int q = 0; q < PER; ++q) {
+      const int e = tid + q * NT;
+      const int r = e / (KIN / 8), c = e % (KIN / 8);
+      const uint8_t* rp = rowptr[r];
+      v[q] = u32x4{0u, 0u, 0u, 0u};
+      if (rp && c < d / 8) v[q] = reinterpret_cast<const u32x4*>(rp)[c];
     }
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int e = tid + q * NT;
+      const int r = e / (KIN / 8), c = e % (KIN / 8);
+      *reinterpret_cast<u32x4*>(Xs + r * XLD + c * 8) = v[q];
+    }
+    __syncthreads();
   }
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
   {
-    FZ_LANE_VARS
-    const bf16_t* W_in = A.W_in;
-    auto rows = [W_in, d](int i) { return W_in + int64_t(i) * 2 * d; };
-    FZ_STREAM(rows, DM, d, FZ_RESID_BODY(Xs, XLD));
+    const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
+    resid_phase<KIN / 16>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), nxt, Xs, XLD);
   }
   {
     FZ_LANE_VARS
@@ -474,192 +569,254 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
       const int act = info & 0xFF, tim = (info >> 8) & 0xFF;
       const int p = valid ? p0 + r : 0;
 #pragma unroll
-      for (int ft = 0; ft < 2; ++ft)
+      for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int f = fq * 64 + ft * 32 + 8 * j + 4 * hf;
+          const int f = fh * 128 + ft * 32 + 8 * j + 4 * hf;
           const uint2 ea = *reinterpret_cast<const uint2*>(A.E_act + act * DM + f);
           const uint2 ep = *reinterpret_cast<const uint2*>(A.E_pos + int64_t(p) * DM + f);
           uint2 et = make_uint2(0, 0);
           if (A.E_time) et = *reinterpret_cast<const uint2*>(A.E_time + tim * DM + f);
+          const float4 cv = *reinterpret_cast<const float4*>(A.cvec + nl_of(A, n) * DM + f);
           const bf16_t* eap = reinterpret_cast<const bf16_t*>(&ea);
           const bf16_t* epp = reinterpret_cast<const bf16_t*>(&ep);
           const bf16_t* etp = reinterpret_cast<const bf16_t*>(&et);
+          const float cva[4] = {cv.x, cv.y, cv.z, cv.w};
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float v = acc[ft][tt][4 * j + i];
             acc[ft][tt][4 * j + i] =
-                valid ? v + cvec[f + i] + bf2f(eap[i]) + bf2f(epp[i]) + bf2f(etp[i]) : 0.f;
+                valid ? v + cva[i] + bf2f(eap[i]) + bf2f(epp[i]) + bf2f(etp[i]) : 0.f;
           }
         }
     }
-    __syncthreads();   // every wave is past Xs (tokens), cvec and tinfo
+    __syncthreads();   // every wave is past Xs (tokens) and tinfo
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int ft = 0; ft < 2; ++ft)
+      for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          st4(Xs + (th * 64 + tt * 32 + l32) * XLD + fq * 64 + ft * 32 + 8 * j + 4 * hf,
+          st4(Xs + (th * 64 + tt * 32 + l32) * XLD + fh * 128 + ft * 32 + 8 * j + 4 * hf,
               acc[ft][tt][4 * j], acc[ft][tt][4 * j + 1], acc[ft][tt][4 * j + 2],
               acc[ft][tt][4 * j + 3]);
     __syncthreads();
   }
 }
 
-// Attention sublayer of one layer for the block: per 64-dim head group, the
-// group's Q / K / V^T into LDS (and K / V^T into the cache for later blocks),
-// causal attention per head, and acc += O_g W_o[:, group]^T.
-__device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_layer& L,
-                                                   f32x16 (&acc)[2][2], bf16_t* Xs, bf16_t* Ws,
-                                                   bf16_t* Qs, bf16_t* Ks, bf16_t* Vts,
-                                                   bf16_t* kc, bf16_t* vc, int p0, bool keep) {
-  const bf16_t* Wqkv = static_cast<const bf16_t*>(L.W_qkv);
-  const bf16_t* Wo = static_cast<const bf16_t*>(L.W_o);
-  for (int g = 0; g < DM / 64; ++g) {
-    {
-      // wave w: token tile w & 3; column tiles 3(w >> 2) .. +2 of q0 q1 k0 k1 v0 v1
-      FZ_LANE_VARS
-      const int tt = w & 3;
-      f32x16 qa[3];
+// ---------------------------------------------------------------- sublayers
+// Q / K / V of head group g: wave w computes token tiles 2(w & 1), 2(w & 1) + 1 of
+// column tiles 3 CS .. +2 of [q0 q1 k0 k1 v0 v1] (CS = w >> 1); Q and K
+// transposed ([dim][token]), V untransposed.  Prefetches `nxt` at its end.  The
+// column split is a template parameter so that each wave runs a branch-free
+// loop with fixed accumulator registers.
+template <int CS>
+__device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
+                                          const float* b_qkv, int g, const bf16_t* Xs, bf16_t* Qs,
+                                          bf16_t* Ks, bf16_t* Vts) {
+  FZ_LANE_VARS
+  constexpr int NKB = DM / 16;
+  constexpr int cs = CS;
+  const int tp = w & 1;
+  f32x16 qa[3][2];
 #pragma unroll
-      for (int t = 0; t < 3; ++t) qa[t] = f32x16{};
-      auto rows = [Wqkv, g](int i) { return Wqkv + int64_t((i >> 6) * DM + g * 64 + (i & 63)) * DM; };
-      if (w < 4) {   // q0 q1 k0: transposed
-        FZ_STREAM(rows, 192, DM, {
-          _Pragma("unroll") for (int kb = 0; kb < KS / 16; ++kb) {
-            const bf16x8 xf = frag(Xs + (tt * 32 + l32) * XLD + k0 + kb * 16 + 8 * hf);
-            _Pragma("unroll") for (int t = 0; t < 3; ++t) {
-              const bf16x8 wf = frag(stage + (t * 32 + l32) * WLD + kb * 16 + 8 * hf);
-              qa[t] = mfma32(wf, xf, qa[t]);
-            }
-          }
-        });
-      } else {       // k1 transposed; v0 v1 untransposed
-        FZ_STREAM(rows, 192, DM, {
-          _Pragma("unroll") for (int kb = 0; kb < KS / 16; ++kb) {
-            const bf16x8 xf = frag(Xs + (tt * 32 + l32) * XLD + k0 + kb * 16 + 8 * hf);
-            const bf16x8 w3 = frag(stage + (3 * 32 + l32) * WLD + kb * 16 + 8 * hf);
-            const bf16x8 w4 = frag(stage + (4 * 32 + l32) * WLD + kb * 16 + 8 * hf);
-            const bf16x8 w5 = frag(stage + (5 * 32 + l32) * WLD + kb * 16 + 8 * hf);
-            qa[0] = mfma32(w3, xf, qa[0]);
-            qa[1] = mfma32(xf, w4, qa[1]);
-            qa[2] = mfma32(xf, w5, qa[2]);
-          }
-        });
-      }
+  for (int t = 0; t < 3; ++t) qa[t][0] = qa[t][1] = f32x16{};
+  bf16x8 wq[NKB][3];
+  bf16x8 xq[NKB][2];
+  const bf16_t* arow = Xs + (tp * 64 + l32) * XLD + 8 * hf;
+  xq[0][0] = lfrag(arow);
+  xq[0][1] = lfrag(arow + 32 * XLD);
+#pragma unroll
+  for (int j = 0; j < NKB; ++j) {
+    bf16x8 a[3];
+#pragma unroll
+    for (int f = 0; f < 3; ++f) a[f] = j < PD ? pre[j][f] : wq[j][f];
+    if (j + PD < NKB) {
+#pragma unroll
+      for (int f = 0; f < 3; ++f) wq[j + PD][f] = gfrag(cur.P, cur.nkb, seg_rt(cur, f), j + PD, lane);
+    } else {
+      seg_load(pre, j + PD - NKB, nxt, lane);
+    }
+    if (j + 1 < NKB) {
+      xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
+      xq[j + 1][1] = lfrag(arow + 32 * XLD + (j + 1) * 16);
+    }
+    if constexpr (CS == 0) {   // q0 q1 k0: transposed
 #pragma unroll
       for (int t = 0; t < 3; ++t) {
-        const int ct = (w >> 2) * 3 + t;
-        const int part = ct >> 1;                 // 0 q, 1 k, 2 v
-        const int dt = ct & 1;
-        const float* bias = L.b_qkv + part * DM + g * 64 + dt * 32;
-        if (part < 2) {
-          bf16_t* dst = part == 0 ? Qs : Ks;
+        qa[t][0] = mfma32(a[t], xq[j][0], qa[t][0]);
+        qa[t][1] = mfma32(a[t], xq[j][1], qa[t][1]);
+      }
+    } else {         // k1 transposed; v0 v1 untransposed
+      qa[0][0] = mfma32(a[0], xq[j][0], qa[0][0]);
+      qa[0][1] = mfma32(a[0], xq[j][1], qa[0][1]);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int dim = 8 * j + 4 * hf;
-            const float4 bv = *reinterpret_cast<const float4*>(bias + dim);
-            st4(dst + (tt * 32 + l32) * QLD + dt * 32 + dim, qa[t][4 * j] + bv.x,
-                qa[t][4 * j + 1] + bv.y, qa[t][4 * j + 2] + bv.z, qa[t][4 * j + 3] + bv.w);
-          }
-        } else {
-          const float bv = bias[l32];
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + 8 * j + 4 * hf, qa[t][4 * j] + bv,
-                qa[t][4 * j + 1] + bv, qa[t][4 * j + 2] + bv, qa[t][4 * j + 3] + bv);
-        }
+      for (int t = 1; t < 3; ++t) {
+        qa[t][0] = mfma32(xq[j][0], a[t], qa[t][0]);
+        qa[t][1] = mfma32(xq[j][1], a[t], qa[t][1]);
       }
     }
+    sched_fence();
+  }
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const int ct = 3 * cs + t;
+    const int part = ct >> 1, dt = ct & 1;
+    const float* bias = b_qkv + part * DM + g * 64 + dt * 32;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int tt = 2 * tp + u;
+      if (part < 2) {
+        bf16_t* dst = part == 0 ? Qs : Ks;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int dim = 8 * j + 4 * hf;
+          const float4 bv = *reinterpret_cast<const float4*>(bias + dim);
+          st4(dst + (tt * 32 + l32) * QLD + dt * 32 + dim, qa[t][u][4 * j] + bv.x,
+              qa[t][u][4 * j + 1] + bv.y, qa[t][u][4 * j + 2] + bv.z, qa[t][u][4 * j + 3] + bv.w);
+        }
+      } else {
+        const float bv = bias[l32];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j] + bv,
+              qa[t][u][4 * j + 1] + bv, qa[t][u][4 * j + 2] + bv, qa[t][u][4 * j + 3] + bv);
+      }
+    }
+  }
+}
+
+// FFN first layer, chunk c: H^T = ReLU(W_1[chunk] Xs^T + b_1) into Hs (wave w:
+// hidden tiles 2(w & 1) + {0,1}, token tiles 2(w >> 1) + {0,1}).
+__device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
+                                           const float* b_1, int c, const bf16_t* Xs, bf16_t* Hs) {
+  FZ_LANE_VARS
+  constexpr int NKB = DM / 16;
+  const int hp = w & 1, tp = w >> 1;
+  f32x16 ha[2][2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) ha[t][0] = ha[t][1] = f32x16{};
+  bf16x8 wq[NKB][2];
+  bf16x8 xq[NKB][2];
+  const bf16_t* arow = Xs + (tp * 64 + l32) * XLD + 8 * hf;
+  xq[0][0] = lfrag(arow);
+  xq[0][1] = lfrag(arow + 32 * XLD);
+#pragma unroll
+  for (int j = 0; j < NKB; ++j) {
+    bf16x8 a[2];
+#pragma unroll
+    for (int f = 0; f < 2; ++f) a[f] = j < PD ? pre[j][f] : wq[j][f];
+    if (j + PD < NKB) {
+#pragma unroll
+      for (int f = 0; f < 2; ++f) wq[j + PD][f] = gfrag(cur.P, cur.nkb, seg_rt(cur, f), j + PD, lane);
+    } else {
+      seg_load(pre, j + PD - NKB, nxt, lane);
+    }
+    if (j + 1 < NKB) {
+      xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
+      xq[j + 1][1] = lfrag(arow + 32 * XLD + (j + 1) * 16);
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      ha[t][0] = mfma32(a[t], xq[j][0], ha[t][0]);
+      ha[t][1] = mfma32(a[t], xq[j][1], ha[t][1]);
+    }
+    sched_fence();
+  }
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int hid = (2 * hp + t) * 32 + 8 * j + 4 * hf;
+        const float4 bv = *reinterpret_cast<const float4*>(b_1 + c * FC + hid);
+        st4(Hs + ((2 * tp + u) * 32 + l32) * HLD + hid, fmaxf(ha[t][u][4 * j] + bv.x, 0.f),
+            fmaxf(ha[t][u][4 * j + 1] + bv.y, 0.f), fmaxf(ha[t][u][4 * j + 2] + bv.z, 0.f),
+            fmaxf(ha[t][u][4 * j + 3] + bv.w, 0.f));
+      }
+}
+
+// Attention sublayer of one layer for the block: per 64-dim head group, Q / K /
+// V^T into LDS (and K / V^T into the cache for later blocks), causal attention
+// per head, and acc += O_g W_o[:, group]^T.  `after` is the phase that follows
+// the sublayer (the first FFN chunk).
+__device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_layer& L,
+                                                   const LayerPk& pk, f32x16 (&acc)[4][2],
+                                                   Pre& pre, const WSeg& after, bf16_t* Xs,
+                                                   bf16_t* Qs, bf16_t* Ks, bf16_t* Vts, bf16_t* Kc,
+                                                   bf16_t* Vc, bf16_t* kc, bf16_t* vc, int p0,
+                                                   bool keep) {
+  const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
+  for (int g = 0; g < DM / 64; ++g) {
+    const WSeg so = seg_resid(pk.o, DM / 16, 4 * g, w);
+    if (w < 2)
+      qkv_phase<0>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
+    else
+      qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
     __syncthreads();
     if (keep) {   // this block's K and V^T for the later blocks of the candidate
       const int tid = otid();
-      for (int e = tid; e < BT * 8; e += NT) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = tid + q * NT;
         const int r = e >> 3, c = (e & 7) * 8;
-        *reinterpret_cast<uint4*>(kc + int64_t(p0 + r) * DM + g * 64 + c) =
-            *reinterpret_cast<const uint4*>(Ks + r * QLD + c);
+        *reinterpret_cast<u32x4*>(kc + int64_t(p0 + r) * DM + g * 64 + c) =
+            *reinterpret_cast<const u32x4*>(Ks + r * QLD + c);
       }
-      for (int e = tid; e < 64 * (BT / 8); e += NT) {
-        const int r = e / (BT / 8), c = (e % (BT / 8)) * 8;
-        *reinterpret_cast<uint4*>(vc + int64_t(g * 64 + r) * A.tpad + p0 + c) =
-            *reinterpret_cast<const uint4*>(Vts + r * VLD + c);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = tid + q * NT;
+        const int r = e >> 4, c = (e & 15) * 8;
+        *reinterpret_cast<u32x4*>(vc + int64_t(g * 64 + r) * A.tpad + p0 + c) =
+            *reinterpret_cast<const u32x4*>(Vts + r * VLD + c);
       }
     }
-    if (A.dh == 64) {
-      attend_head<64>(g, 0, p0, Qs, Ks, Vts, kc, vc, A.tpad);
-    } else {
-      attend_head<32>(g, 0, p0, Qs, Ks, Vts, kc, vc, A.tpad);
-      attend_head<32>(g, 32, p0, Qs, Ks, Vts, kc, vc, A.tpad);
-    }
+    if (A.dh == 64)
+      attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
+    else
+      attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
     __syncthreads();
-    {   // acc += O_g W_o[:, 64g : 64g + 64]^T
-      FZ_LANE_VARS
-      auto rows = [Wo, g](int i) { return Wo + int64_t(i) * DM + g * 64; };
-      FZ_STREAM(rows, DM, 64, FZ_RESID_BODY(Qs, QLD));
-    }
+    const WSeg nq = g + 1 < DM / 64 ? seg_qkv(pk.qkv, g + 1, w) : after;
+    resid_phase<4>(acc, pre, so, nq, Qs, QLD);
+    __syncthreads();   // Qs (O) and Ks / Vts are rewritten by the next group
   }
 }
 
-// FFN sublayer: per chunk of 128 hidden units, H^T = ReLU(W_1[chunk] Xs^T + b_1)
-// into LDS, then acc += W_2[:, chunk] H^T.
+// FFN sublayer: per chunk of 128 hidden units, H^T into LDS, then
+// acc += W_2[:, chunk] H^T.  The stream enters primed with chunk 0 and leaves
+// primed with `after`.
 __device__ __forceinline__ void ffn_sublayer(const Args& A, const tav2_layer& L,
-                                             f32x16 (&acc)[2][2], bf16_t* Xs, bf16_t* Ws,
-                                             bf16_t* Hs) {
-  const bf16_t* W1 = static_cast<const bf16_t*>(L.W_1);
-  const bf16_t* W2 = static_cast<const bf16_t*>(L.W_2);
+                                             const LayerPk& pk, f32x16 (&acc)[4][2], Pre& pre,
+                                             const WSeg& after, bf16_t* Xs, bf16_t* Hs) {
+  const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
   const int ffn = A.ffn;
-  for (int c = 0; c < ffn / FC; ++c) {
-    {
-      // wave w: hidden tile w & 3, token tiles 2(w >> 2) and 2(w >> 2) + 1
-      FZ_LANE_VARS
-      const int ht = w & 3, tp = w >> 2;
-      f32x16 ha[2];
-      ha[0] = f32x16{};
-      ha[1] = f32x16{};
-      auto rows = [W1, c](int i) { return W1 + int64_t(c * FC + i) * DM; };
-      FZ_STREAM(rows, FC, DM, {
-        _Pragma("unroll") for (int kb = 0; kb < KS / 16; ++kb) {
-          const bf16x8 wf = frag(stage + (ht * 32 + l32) * WLD + kb * 16 + 8 * hf);
-          _Pragma("unroll") for (int t = 0; t < 2; ++t) {
-            const bf16x8 xf = frag(Xs + ((2 * tp + t) * 32 + l32) * XLD + k0 + kb * 16 + 8 * hf);
-            ha[t] = mfma32(wf, xf, ha[t]);
-          }
-        }
-      });
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int hid = ht * 32 + 8 * j + 4 * hf;
-          const float4 bv = *reinterpret_cast<const float4*>(L.b_1 + c * FC + hid);
-          st4(Hs + ((2 * tp + t) * 32 + l32) * HLD + hid, fmaxf(ha[t][4 * j] + bv.x, 0.f),
-              fmaxf(ha[t][4 * j + 1] + bv.y, 0.f), fmaxf(ha[t][4 * j + 2] + bv.z, 0.f),
-              fmaxf(ha[t][4 * j + 3] + bv.w, 0.f));
-        }
-    }
+  const int nch = ffn / FC;
+  for (int c = 0; c < nch; ++c) {
+    const WSeg s2 = seg_resid(pk.w2, ffn / 16, c * (FC / 16), w);
+    ffn1_phase(pre, seg_ffn1(pk.w1, c, w), s2, L.b_1, c, Xs, Hs);
     __syncthreads();
-    {
-      FZ_LANE_VARS
-      auto rows = [W2, c, ffn](int i) { return W2 + int64_t(i) * ffn + c * FC; };
-      FZ_STREAM(rows, DM, FC, FZ_RESID_BODY(Hs, HLD));
-    }
+    const WSeg nx = c + 1 < nch ? seg_ffn1(pk.w1, c + 1, w) : after;
+    resid_phase<FC / 16>(acc, pre, s2, nx, Hs, HLD);
+    __syncthreads();   // Hs is rewritten by the next chunk
   }
 }
 
+// ---------------------------------------------------------------- the kernel
 __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
   bf16_t* Xs = reinterpret_cast<bf16_t*>(smem);
-  bf16_t* Ws = reinterpret_cast<bf16_t*>(smem + XS_BYTES);
-  uint8_t* Sc = smem + XS_BYTES + WS_BYTES;
-  float* pmax = reinterpret_cast<float*>(smem + XS_BYTES + WS_BYTES + SC_BYTES);
+  uint8_t* Sc = smem + XS_BYTES;
+  bf16_t* Kc = reinterpret_cast<bf16_t*>(smem + XS_BYTES + SC_BYTES);
+  bf16_t* Vc = reinterpret_cast<bf16_t*>(smem + XS_BYTES + SC_BYTES + QS_BYTES);
+  float* pmax = reinterpret_cast<float*>(smem + XS_BYTES + SC_BYTES + CS_BYTES);
   bf16_t* Qs = reinterpret_cast<bf16_t*>(Sc);                    // [BT][QLD], then O
   bf16_t* Ks = reinterpret_cast<bf16_t*>(Sc + QS_BYTES);         // [BT][QLD]
   bf16_t* Vts = reinterpret_cast<bf16_t*>(Sc + 2 * QS_BYTES);    // [64][VLD]
   bf16_t* Hs = reinterpret_cast<bf16_t*>(Sc);                    // [BT][HLD]
   float* red = reinterpret_cast<float*>(Sc);                     // reductions
-  float* cvec = reinterpret_cast<float*>(Sc);                    // [DM] during encoding
-  int* tinfo = reinterpret_cast<int*>(Sc + DM * 4);              // [BT] during encoding
+  int* tinfo = reinterpret_cast<int*>(Sc);                       // [BT] during encoding
+  const uint8_t** rowptr = reinterpret_cast<const uint8_t**>(Sc + BT * 8);   // [BT]
 
   const int64_t nl = blockIdx.x;
   const int64_t n = A.c0 + nl;
@@ -674,19 +831,27 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
   // layer records are read through the kernel-argument segment so the runtime
   // layer index stays a scalar load instead of a private copy of the array
   const Args* AK = (const Args*)(__builtin_amdgcn_kernarg_segment_ptr());
-
-  f32x16 acc[2][2];
+  const int wv = __builtin_amdgcn_readfirstlane(otid() / WAVE);
+  const WSeg s_embed = seg_resid(A.pk_in, KIN / 16, 0, wv);
+  const WSeg s_pool = seg_resid(A.pk_pool, DM / 16, 0, wv);
+  Pre pre;
+  seg_prime(pre, s_embed, otid() % WAVE);
+  f32x16 acc[4][2];
   for (int blk = 0; blk < nblk; ++blk) {
     const int p0 = blk * BT;
     __syncthreads();
-    encode_block_input(A, n, p0, Tv, acc, Xs, Ws, cvec, tinfo);
+    encode_block_input(A, n, p0, Tv, acc, Xs, tinfo, rowptr, pre,
+                       seg_qkv(AK->pk[0].qkv, 0, wv));
     for (int li = 0; li < A.n_layers; ++li) {
       const tav2_layer L = AK->layers[li];
+      const LayerPk pk = AK->pk[li];
       bf16_t* kc = A.kcache ? A.kcache + (nl * A.n_layers + li) * int64_t(A.tpad) * DM : nullptr;
       bf16_t* vc = A.vcache ? A.vcache + (nl * A.n_layers + li) * int64_t(DM) * A.tpad : nullptr;
-      attention_sublayer(A, L, acc, Xs, Ws, Qs, Ks, Vts, kc, vc, p0, blk + 1 < nblk);
+      attention_sublayer(A, L, pk, acc, pre, seg_ffn1(pk.w1, 0, wv), Xs, Qs, Ks, Vts, Kc, Vc, kc,
+                         vc, p0, blk + 1 < nblk);
       layer_norm(acc, L.b_o, L.ln1_g, L.ln1_b, red, Xs);
-      ffn_sublayer(A, L, acc, Xs, Ws, Hs);
+      const WSeg after = li + 1 < A.n_layers ? seg_qkv(AK->pk[li + 1].qkv, 0, wv) : s_pool;
+      ffn_sublayer(A, L, pk, acc, pre, after, Xs, Hs);
       layer_norm(acc, L.b_2, L.ln2_g, L.ln2_b, red, Xs);
     }
     // ---- head: out[DM:] = X of the last valid token; running max of the pool
@@ -698,10 +863,10 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
         for (int tt = 0; tt < 2; ++tt)
           if (th * 64 + tt * 32 + l32 == last) {
 #pragma unroll
-            for (int ft = 0; ft < 2; ++ft)
+            for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
               for (int j = 0; j < 4; ++j) {
-                const int f = fq * 64 + ft * 32 + 8 * j + 4 * hf;
+                const int f = fh * 128 + ft * 32 + 8 * j + 4 * hf;
                 *reinterpret_cast<float4*>(out + DM + f) =
                     make_float4(acc[ft][tt][4 * j], acc[ft][tt][4 * j + 1],
                                 acc[ft][tt][4 * j + 2], acc[ft][tt][4 * j + 3]);
@@ -710,18 +875,86 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
       }
     }
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < 4; ++a)
 #pragma unroll
       for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
-    {
-      FZ_LANE_VARS
-      const bf16_t* Wp = A.W_pool;
-      auto rows = [Wp](int i) { return Wp + int64_t(i) * DM; };
-      FZ_STREAM(rows, DM, DM, FZ_RESID_BODY(Xs, XLD));
-    }
+    // the pool phase prefetches the next block's input projection (also after the
+    // last block, where the loads are simply unused)
+    resid_phase<DM / 16>(acc, pre, s_pool, s_embed, Xs, XLD);
     pool_block(acc, A.b_pool, pmax, red, Tv - p0);
   }
   for (int c = threadIdx.x; c < DM; c += NT) out[c] = pmax[c];
+}
+
+// ---------------------------------------------------------------- candidate half
+// cvec[i] = c W_in[:, d:]^T + b_in for candidates c0 + i (the candidate's part of
+// the Eq. 4 input projection, the same for every position of the candidate);
+// CB candidates per workgroup, thread f computes output feature f.
+constexpr int CB = 16;
+__global__ __launch_bounds__(DM) void cand_proj_kernel(const bf16_t* __restrict__ cand,
+                                                       const bf16_t* __restrict__ W_in,
+                                                       const float* __restrict__ b_in, int d,
+                                                       int64_t c0, int64_t nc,
+                                                       float* __restrict__ cvec) {
+  __shared__ float cs[CB][KIN];
+  const int64_t base = int64_t(blockIdx.x) * CB;
+  const int nb = nc - base < CB ? int(nc - base) : CB;
+  for (int e = threadIdx.x; e < CB * d; e += DM) {
+    const int r = e / d, c = e % d;
+    cs[r][c] = r < nb ? bf2f(cand[(c0 + base + r) * d + c]) : 0.f;
+  }
+  __syncthreads();
+  const int f = threadIdx.x;
+  float acc[CB];
+#pragma unroll
+  for (int r = 0; r < CB; ++r) acc[r] = b_in[f];
+  const bf16_t* wr = W_in + int64_t(f) * 2 * d + d;
+  for (int j = 0; j < d; j += 8) {
+    const uint4 wv = *reinterpret_cast<const uint4*>(wr + j);
+    const bf16_t* wp = reinterpret_cast<const bf16_t*>(&wv);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float wf = bf2f(wp[u]);
+#pragma unroll
+      for (int r = 0; r < CB; ++r) acc[r] = fmaf(wf, cs[r][j + u], acc[r]);
+    }
+  }
+  for (int r = 0; r < nb; ++r) cvec[(base + r) * DM + f] = acc[r];
+}
+
+// ---------------------------------------------------------------- weight packing
+// Rewrites a row-major [rows x K] bf16 matrix (row stride ld, columns >= kvalid
+// read as zero) into MFMA-fragment order: fragment (rt, kb) is 1 KB at
+// ((rt * K/16) + kb) * 512 elements, lane l holding row 32 rt + l % 32, columns
+// 16 kb + 8 (l / 32) .. +7.
+struct PackJob {
+  const bf16_t* src;
+  bf16_t* dst;
+  int rows, K, ld, kvalid;
+  int64_t first;   // first item (16-byte piece) of this job
+};
+constexpr int MAX_JOBS = 2 + 4 * MAX_LAYERS;
+struct PackArgs {
+  PackJob job[MAX_JOBS];
+  int njobs;
+  int64_t items;
+};
+
+__global__ __launch_bounds__(256) void pack_weights_kernel(PackArgs P) {
+  const int64_t it = int64_t(blockIdx.x) * 256 + threadIdx.x;
+  if (it >= P.items) return;
+  int j = 0;
+  while (j + 1 < P.njobs && it >= P.job[j + 1].first) ++j;
+  const PackJob& J = P.job[j];
+  const int64_t e = it - J.first;               // piece within the job
+  const int lane = int(e % 64);
+  const int64_t frag = e / 64;
+  const int nkb = J.K / 16;
+  const int rt = int(frag / nkb), kb = int(frag % nkb);
+  const int row = rt * 32 + lane % 32, col = kb * 16 + 8 * (lane / 32);
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (col < J.kvalid) v = *reinterpret_cast<const uint4*>(J.src + int64_t(row) * J.ld + col);
+  *reinterpret_cast<uint4*>(J.dst + e * 8) = v;
 }
 
 }  // namespace fz
@@ -744,23 +977,70 @@ int64_t fused_chunk(int64_t total, int T, const tav2_weights& w) {
   if (c < 1) c = 1;
   return c < total ? c : (total > 0 ? total : 1);
 }
+
+size_t packed_bytes(const tav2_weights& w) {
+  const size_t dm = fz::DM, ff = size_t(w.d_ffn);
+  const size_t per_layer = 3 * dm * dm + dm * dm + ff * dm + dm * ff;
+  return align_up((dm * fz::KIN + dm * dm + size_t(w.n_layers) * per_layer) * 2, 256);
+}
 }  // namespace
 
 bool encode_fused_supported(int d, const tav2_weights& w) {
   const int dh = w.d_model / w.n_heads;
   return w.d_model == fz::DM && (dh == 32 || dh == 64) && w.d_ffn % fz::FC == 0 &&
-         d % 32 == 0 && d <= fz::DM && w.n_layers <= fz::MAX_LAYERS;
+         d % 32 == 0 && d <= fz::KIN && w.n_layers <= fz::MAX_LAYERS;
 }
 
 size_t encode_fused_workspace(int64_t total, int T, const tav2_weights& w) {
   const size_t per = per_candidate_cache(T, w);
-  return per * size_t(fused_chunk(total, T, w));
+  const size_t chunk = size_t(fused_chunk(total, T, w));
+  return packed_bytes(w) + align_up(chunk * fz::DM * 4, 256) + per * chunk;
 }
 
 hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int64_t total,
                                const tav2_weights& w, float* out, void* ws, hipStream_t st) {
   if (total == 0) return hipSuccess;
+  const int d = src.d, dm = fz::DM, ff = w.d_ffn;
+  // ---- pack every matrix into fragment order (head of the workspace)
+  bf16_t* pk = static_cast<bf16_t*>(ws);
+  fz::PackArgs P{};
+  int64_t items = 0;
+  size_t off = 0;
+  auto add = [&](const void* srcm, int rows, int K, int ld, int kvalid) {
+    fz::PackJob& J = P.job[P.njobs++];
+    J.src = static_cast<const bf16_t*>(srcm);
+    J.dst = pk + off;
+    J.rows = rows;
+    J.K = K;
+    J.ld = ld;
+    J.kvalid = kvalid;
+    J.first = items;
+    items += int64_t(rows) * K / 8;
+    off += size_t(rows) * K;
+    return static_cast<const bf16_t*>(J.dst);
+  };
   fz::Args a{};
+  a.pk_in = add(w.W_in, dm, fz::KIN, 2 * d, d);
+  a.pk_pool = add(w.W_pool, dm, dm, dm, dm);
+  for (int i = 0; i < w.n_layers; ++i) {
+    const tav2_layer& L = w.layers[i];
+    a.pk[i].qkv = add(L.W_qkv, 3 * dm, dm, dm, dm);
+    a.pk[i].o = add(L.W_o, dm, dm, dm, dm);
+    a.pk[i].w1 = add(L.W_1, ff, dm, dm, dm);
+    a.pk[i].w2 = add(L.W_2, dm, ff, ff, ff);
+  }
+  P.items = items;
+  {
+    ProfScope prof("pack_weights", st);
+    fz::pack_weights_kernel<<<unsigned(cdiv(items, 256)), 256, 0, st>>>(P);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const size_t per = per_candidate_cache(src.T, w);
+  const int64_t chunk = fused_chunk(total, src.T, w);
+  float* cvec = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + packed_bytes(w));
+  uint8_t* cache = reinterpret_cast<uint8_t*>(cvec) + align_up(size_t(chunk) * fz::DM * 4, 256);
+
   a.s = src;
   a.cand = static_cast<const bf16_t*>(cand_emb);
   a.W_in = static_cast<const bf16_t*>(w.W_in);
@@ -768,23 +1048,28 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
   a.E_act = static_cast<const bf16_t*>(w.E_act);
   a.E_time = static_cast<const bf16_t*>(w.E_time);
   a.E_pos = static_cast<const bf16_t*>(w.E_pos);
-  a.W_pool = static_cast<const bf16_t*>(w.W_pool);
   a.b_pool = w.b_pool;
   for (int i = 0; i < w.n_layers; ++i) a.layers[i] = w.layers[i];
   a.n_layers = w.n_layers;
-  a.d = src.d;
+  a.d = d;
   a.dh = w.d_model / w.n_heads;
-  a.ffn = w.d_ffn;
+  a.ffn = ff;
   a.tpad = int(fused_tpad(src.T));
   a.out = out;
-  const size_t per = per_candidate_cache(src.T, w);
-  const int64_t chunk = fused_chunk(total, src.T, w);
+  a.cvec = cvec;
   for (int64_t c0 = 0; c0 < total; c0 += chunk) {
     const int64_t nc = total - c0 < chunk ? total - c0 : chunk;
     a.c0 = c0;
+    {
+      ProfScope prof("cand_proj", st);
+      fz::cand_proj_kernel<<<unsigned(cdiv(nc, fz::CB)), fz::DM, 0, st>>>(
+          a.cand, a.W_in, a.b_in, d, c0, nc, cvec);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
     if (per) {
-      a.kcache = static_cast<bf16_t*>(ws);
-      a.vcache = reinterpret_cast<bf16_t*>(static_cast<uint8_t*>(ws) + per / 2 * size_t(chunk));
+      a.kcache = reinterpret_cast<bf16_t*>(cache);
+      a.vcache = reinterpret_cast<bf16_t*>(cache + per / 2 * size_t(chunk));
     }
     ProfScope prof("encoder_fused", st);
     fz::encoder_fused_kernel<<<unsigned(nc), fz::NT, 0, st>>>(a);

@@ -88,12 +88,17 @@ def test_workspace_queries():
     w = fake_weights()
     tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
                    d=64, dtype=T.BF16, reserved=0)
-    # T <= 128: the fused bf16 encoder keeps everything on chip
-    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == 0
-    # T = 256: a K / V cache of layers x 2 x T x d_model bf16 per candidate
+    # fused bf16 encoder: every matrix in fragment order (W_in's token half padded to
+    # 256 columns), the candidate half of the input projection (fp32 per candidate)
+    # and, past one 128-position block, a K / V cache of layers x 2 x T x d_model bf16
+    dm, ff, layers = 256, 512, 2
+    packed = (dm * 256 + dm * dm + layers * (4 * dm * dm + 2 * ff * dm)) * 2
+    cvec = 10 * dm * 4
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == packed + cvec
     w256 = fake_weights(max_pos=256)
     tok.T = 256
-    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w256)) == 10 * 2 * 2 * 256 * 256 * 2
+    assert (lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w256))
+            == packed + cvec + 10 * layers * 2 * 256 * dm * 2)
     tok.T = 64
     wf = fake_weights(dm=64, heads=2, ffn=128, layers=1, max_pos=32, dtype=T.F32, time=False)
     tokf = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=None, valid_len=FAKE, total=16, T=32,
