@@ -31,6 +31,12 @@
 #include "internal.h"
 #include "token_source.h"
 
+#ifndef FZ_D2
+#define FZ_D2 8
+#define FZ_D3 5
+#define FZ_D4 4
+#endif
+
 namespace tav2 {
 namespace fz {
 
@@ -54,6 +60,8 @@ constexpr int PM_BYTES = DM * 4;                       // running pooled max
 constexpr int LDS_BYTES = XS_BYTES + SC_BYTES + CS_BYTES + PM_BYTES;
 static_assert(LDS_BYTES <= 163840, "fused encoder exceeds the 160 KiB of LDS");
 static_assert(BT * HLD * 2 <= SC_BYTES, "FFN chunk does not fit the scratch region");
+static_assert(BT * HLD * 2 + 3 * DM * 4 <= SC_BYTES, "LayerNorm 2 parameters do not fit");
+static_assert(BT * 4 * 4 <= QS_BYTES && 3 * DM * 4 <= QS_BYTES, "LayerNorm 1 buffers do not fit");
 static_assert(BT * 8 + BT * 8 <= SC_BYTES, "encoding buffers do not fit");
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -78,11 +86,10 @@ __device__ __forceinline__ int otid() {
 __device__ __forceinline__ bf16x8 lfrag(const bf16_t* p) {   // 16 bytes from LDS
   return as_bf16x8(*reinterpret_cast<const uint4*>(p));
 }
-// Fragment (rt, kb) of a packed matrix with nkb k-blocks: 64 lanes x 16 bytes.
-__device__ __forceinline__ bf16x8 gfrag(const bf16_t* P, int nkb, int rt, int kb, int lane) {
-  return __builtin_bit_cast(
-      bf16x8, *reinterpret_cast<const u32x4*>(P + ((int64_t(rt) * nkb + kb) * 64 + lane) * 8));
-}
+// Fragment `frag` (1 KB, 64 lanes x 16 bytes) of the packed weights: a buffer load
+// with the fragment offset in a scalar register and the lane offset as the only
+// per-lane address (loads past the packed region would return zeros).
+__device__ __forceinline__ bf16x8 wfrag(int frag, int lane);
 __device__ __forceinline__ void st4(bf16_t* p, float a, float b, float c, float d) {
   *reinterpret_cast<uint2*>(p) = make_uint2(pack2(a, b), pack2(c, d));
 }
@@ -111,11 +118,11 @@ __device__ __forceinline__ float xsum16(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-struct LayerPk {
-  const bf16_t* qkv;    // [768 rows][16 kb]
-  const bf16_t* o;      // [256][16]
-  const bf16_t* w1;     // [ffn][16]
-  const bf16_t* w2;     // [256][ffn / 16]
+struct LayerPk {        // first fragment of each packed matrix
+  int qkv;              // [768 rows][16 kb]
+  int o;                // [256][16]
+  int w1;               // [ffn][16]
+  int w2;               // [256][ffn / 16]
 };
 
 struct Args {
@@ -128,8 +135,10 @@ struct Args {
   const bf16_t* E_pos;
   const float* b_pool;
   const float* cvec;        // [chunk, DM]: c W_in[:, d:]^T + b_in per candidate
-  const bf16_t* pk_in;      // packed token half of W_in, [256][KIN / 16]
-  const bf16_t* pk_pool;    // packed W_pool
+  const bf16_t* pkw;        // packed weights (fragment order)
+  unsigned pk_bytes;
+  int pk_in;                // packed token half of W_in, [256][KIN / 16]
+  int pk_pool;              // packed W_pool
   tav2_layer layers[MAX_LAYERS];   // biases and LayerNorm vectors
   LayerPk pk[MAX_LAYERS];
   int n_layers;
@@ -143,63 +152,115 @@ struct Args {
   float* out;               // [total, 2 DM]
 };
 
-// ---------------------------------------------------------------- weight stream
-// Every GEMM phase reads its weight fragments from L2 PD k-blocks ahead, and its
-// last PD iterations already load the first PD k-blocks of the NEXT phase into
-// `pre`, so the stream keeps running across phase boundaries (attention,
-// LayerNorm and block boundaries included) instead of refilling at each phase.
-constexpr int PD = 4;                    // prefetch depth in k-blocks
-typedef bf16x8 Pre[PD][4];
+__device__ __forceinline__ bf16x8 wfrag(int frag, int lane) {
+  const Args* AK = (const Args*)(__builtin_amdgcn_kernarg_segment_ptr());
+  const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(AK->pkw), (short)0, int(AK->pk_bytes), 0x00020000);
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, lane * 16, frag * 1024, 0));
+}
 
-struct WSeg {                            // a phase's weight fragments: up to 4 row tiles
-  const bf16_t* P;                       // packed matrix
+// ---------------------------------------------------------------- weight stream
+// Every GEMM phase streams its weight fragments from L2 into registers ahead of
+// use, and its last iterations already load the head of the NEXT phase's stream
+// into `pre`, so the stream keeps running across phase boundaries (attention,
+// LayerNorm and block boundaries included).  The look-ahead is a fixed number of
+// fragments (NSLOT), i.e. NSLOT / nr k-blocks for a phase with nr row tiles,
+// which gives every phase about the same look-ahead in MFMA time.
+constexpr int NSLOT = 16;
+typedef bf16x8 Pre[NSLOT];
+// k-blocks of look-ahead for a phase with nr row tiles, and the slots it fills
+constexpr int depth(int nr) { return nr == 2 ? FZ_D2 : nr == 3 ? FZ_D3 : FZ_D4; }
+constexpr int used_slots(int nr) { return depth(nr) * nr; }
+static_assert(used_slots(2) <= NSLOT && used_slots(3) <= NSLOT && used_slots(4) <= NSLOT, "look-ahead");
+
+struct WSeg {                            // a phase's weight fragments (all wave-uniform)
+  int P;                                 // first fragment of the packed matrix
   int nkb;                               // k-blocks per row of P
   int kb0;                               // first k-block of the phase
-  int nr;                                // row tiles used (1..4)
-  int r0, r1, r2, r3;                    // packed row tiles
+  int r0, r1, r2, r3;                    // packed row tiles (the phase uses nr of them)
 };
 
 __device__ __forceinline__ int seg_rt(const WSeg& s, int f) {
   return f == 0 ? s.r0 : f == 1 ? s.r1 : f == 2 ? s.r2 : s.r3;
 }
-// k-block `slot` of segment s into pre[slot]
-__device__ __forceinline__ void seg_load(Pre& pre, int slot, const WSeg& s, int lane) {
-#pragma unroll
-  for (int f = 0; f < 4; ++f)
-    if (f < s.nr) pre[slot][f] = gfrag(s.P, s.nkb, seg_rt(s, f), s.kb0 + slot, lane);
+// slot i of the look-ahead of a segment with NR row tiles holds k-block i / NR,
+// row tile i % NR (slots past the last whole k-block stay unused)
+template <int NR>
+__device__ __forceinline__ void seg_slot(Pre& pre, int i, const WSeg& s, int lane) {
+  if (i < used_slots(NR)) pre[i] = wfrag(s.P + seg_rt(s, i % NR) * s.nkb + s.kb0 + i / NR, lane);
 }
+template <int NR>
 __device__ __forceinline__ void seg_prime(Pre& pre, const WSeg& s, int lane) {
 #pragma unroll
-  for (int j = 0; j < PD; ++j) seg_load(pre, j, s, lane);
+  for (int i = 0; i < NSLOT; ++i) seg_slot<NR>(pre, i, s, lane);
 }
 // residual-shaped phase of wave w: row tiles 4 (w & 1) + 0..3
-__device__ __forceinline__ WSeg seg_resid(const bf16_t* P, int nkb, int kb0, int w) {
+__device__ __forceinline__ WSeg seg_resid(int P, int nkb, int kb0, int w) {
   const int r = 4 * (w & 1);
-  return WSeg{P, nkb, kb0, 4, r, r + 1, r + 2, r + 3};
+  return WSeg{P, nkb, kb0, r, r + 1, r + 2, r + 3};
 }
 // FFN first layer, chunk c: hidden row tiles 4c + 2(w & 1) + 0..1
-__device__ __forceinline__ WSeg seg_ffn1(const bf16_t* P, int c, int w) {
+__device__ __forceinline__ WSeg seg_ffn1(int P, int c, int w) {
   const int r = c * (128 / 32) + 2 * (w & 1);
-  return WSeg{P, 256 / 16, 0, 2, r, r + 1, 0, 0};
+  return WSeg{P, 256 / 16, 0, r, r + 1, 0, 0};
 }
 // Q / K / V of head group g: column tiles 3(w >> 1) + 0..2 of [q0 q1 k0 k1 v0 v1]
 // are packed row tiles 8 part + 2g + dt
-__device__ __forceinline__ WSeg seg_qkv(const bf16_t* P, int g, int w) {
+__device__ __forceinline__ WSeg seg_qkv(int P, int g, int w) {
   int r[3];
 #pragma unroll
   for (int t = 0; t < 3; ++t) {
     const int ct = 3 * (w >> 1) + t;
     r[t] = 8 * (ct >> 1) + 2 * g + (ct & 1);
   }
-  return WSeg{P, 256 / 16, 0, 3, r[0], r[1], r[2], 0};
+  return WSeg{P, 256 / 16, 0, r[0], r[1], r[2], 0};
+}
+
+// Whether refilling the look-ahead (slots of a next phase with NRN row tiles)
+// during the last iterations of an NKB-block phase with NR row tiles never
+// overwrites a slot before this phase has read it.
+constexpr bool stream_ok(int NKB, int NR, int NRN) {
+  const int D = depth(NR), NU = used_slots(NRN);
+  if (NKB < D) return false;
+  for (int q = 0; q < D; ++q)
+    for (int i = NU * q / D; i < NU * (q + 1) / D; ++i)
+      if (i < used_slots(NR) && q + NKB - D < i / NR) return false;
+  return true;
+}
+// Weight fragment (k-block j, row tile f) of the running phase, by value (an
+// array copy out of the look-ahead would merge into one wide copy that keeps the
+// look-ahead in scratch memory).
+template <int NKB, int NR>
+__device__ __forceinline__ bf16x8 stream_frag(const bf16x8 (&wq)[NKB][NR], const Pre& pre, int j,
+                                              int f) {
+  constexpr int D = depth(NR);
+  return j < D ? pre[(j < D ? j : 0) * NR + f] : wq[j][f];
+}
+// Loads issued at k-block j: k-block j + D of this phase, or (in the last D
+// iterations) this iteration's share of the look-ahead of the next phase, which
+// has NRN row tiles.
+template <int NKB, int NR, int NRN>
+__device__ __forceinline__ void stream_fetch(bf16x8 (&wq)[NKB][NR], Pre& pre, const WSeg& cur,
+                                             const WSeg& nxt, int j, int lane) {
+  constexpr int D = depth(NR), NU = used_slots(NRN);
+  static_assert(stream_ok(NKB, NR, NRN), "phase too short for the weight look-ahead");
+  if (j + D < NKB) {
+#pragma unroll
+    for (int f = 0; f < NR; ++f)
+      wq[j + D][f] = wfrag(cur.P + seg_rt(cur, f) * cur.nkb + cur.kb0 + j + D, lane);
+  } else {
+    const int q = j - (NKB - D);
+#pragma unroll
+    for (int i = 0; i < NSLOT; ++i)   // constant bounds: unrolled before j is known
+      if (i >= NU * q / D && i < NU * (q + 1) / D) seg_slot<NRN>(pre, i, nxt, lane);
+  }
 }
 
 // acc[ft][tt] += C^T: features 128 fh + 32 ft (packed rows of cur), tokens
 // 64 th + 32 tt (rows of ACT in LDS, columns 16 j), over NKB k-blocks.
-template <int NKB>
+template <int NKB, int NRN>
 __device__ __forceinline__ void resid_phase(f32x16 (&acc)[4][2], Pre& pre, const WSeg& cur,
                                             const WSeg& nxt, const bf16_t* ACT, int ald) {
-  static_assert(NKB >= PD, "phase shorter than the prefetch depth");
   FZ_LANE_VARS
   bf16x8 wq[NKB][4];
   bf16x8 xq[NKB][2];
@@ -208,33 +269,46 @@ __device__ __forceinline__ void resid_phase(f32x16 (&acc)[4][2], Pre& pre, const
   xq[0][1] = lfrag(arow + 32 * ald);
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
-    bf16x8 a[4];
-#pragma unroll
-    for (int f = 0; f < 4; ++f) a[f] = j < PD ? pre[j][f] : wq[j][f];
-    if (j + PD < NKB) {
-#pragma unroll
-      for (int f = 0; f < 4; ++f) wq[j + PD][f] = gfrag(cur.P, cur.nkb, seg_rt(cur, f), cur.kb0 + j + PD, lane);
-    } else {
-      seg_load(pre, j + PD - NKB, nxt, lane);
-    }
     if (j + 1 < NKB) {
       xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
       xq[j + 1][1] = lfrag(arow + 32 * ald + (j + 1) * 16);
     }
 #pragma unroll
     for (int ft = 0; ft < 4; ++ft) {
-      acc[ft][0] = mfma32(a[ft], xq[j][0], acc[ft][0]);
-      acc[ft][1] = mfma32(a[ft], xq[j][1], acc[ft][1]);
+      const bf16x8 a = stream_frag<NKB, 4>(wq, pre, j, ft);
+      acc[ft][0] = mfma32(a, xq[j][0], acc[ft][0]);
+      acc[ft][1] = mfma32(a, xq[j][1], acc[ft][1]);
     }
+    stream_fetch<NKB, 4, NRN>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 }
 
 // ---------------------------------------------------------------- LayerNorm
+// The sublayer's bias, gain and offset (3 x DM floats) reach LDS through
+// registers: each thread loads its three values before the sublayer's last GEMM
+// phase and stores them after it, so the loads are older than that phase's
+// look-ahead loads of the next weights and waiting for them never waits for the
+// weight stream (vector memory loads complete in issue order).
+struct LnParams {
+  float bias, gain, off;
+};
+static_assert(NT == DM, "one LayerNorm parameter triple per thread");
+__device__ __forceinline__ LnParams ln_params_load(const float* bias, const float* g,
+                                                   const float* b) {
+  const int t = otid();
+  return LnParams{bias[t], g[t], b[t]};
+}
+__device__ __forceinline__ void ln_params_store(const LnParams& q, float* P) {
+  const int t = otid();
+  P[t] = q.bias;
+  P[DM + t] = q.gain;
+  P[2 * DM + t] = q.off;
+}
+
 // x <- LN(acc + bias) with gain g and offset b over the 256 features of every
-// token; Xs <- bf16(x).  Ends with a barrier.
-__device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* bias,
-                                           const float* g, const float* b, float* red,
+// token, with P = [bias | g | b] in LDS; Xs <- bf16(x).  Ends with a barrier.
+__device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* P, float* red,
                                            bf16_t* Xs) {
   FZ_LANE_VARS
   float s[2] = {0.f, 0.f}, ss[2] = {0.f, 0.f};
@@ -242,7 +316,7 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* bia
   for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const float4 bi = *reinterpret_cast<const float4*>(bias + fh * 128 + ft * 32 + 8 * j + 4 * hf);
+      const float4 bi = *reinterpret_cast<const float4*>(P + fh * 128 + ft * 32 + 8 * j + 4 * hf);
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
         const float v0 = acc[ft][tt][4 * j] + bi.x;
@@ -270,28 +344,29 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* bia
     }
   }
   __syncthreads();
-  float mean[2], rstd[2];
+  float rstd[2], shift[2];   // x_hat = x rstd + shift
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt) {
     const int tok = th * 64 + tt * 32 + l32;
     const float4 a = *reinterpret_cast<const float4*>(red + tok * 4);
-    mean[tt] = (a.x + a.z) * (1.f / DM);
-    const float var = fmaxf((a.y + a.w) * (1.f / DM) - mean[tt] * mean[tt], 0.f);
+    const float mean = (a.x + a.z) * (1.f / DM);
+    const float var = fmaxf((a.y + a.w) * (1.f / DM) - mean * mean, 0.f);
     rstd[tt] = rsqrtf(var + 1e-5f);
+    shift[tt] = -mean * rstd[tt];
   }
 #pragma unroll
   for (int ft = 0; ft < 4; ++ft)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int f = fh * 128 + ft * 32 + 8 * j + 4 * hf;
-      const float4 gg = *reinterpret_cast<const float4*>(g + f);
-      const float4 bb = *reinterpret_cast<const float4*>(b + f);
+      const float4 gg = *reinterpret_cast<const float4*>(P + DM + f);
+      const float4 bb = *reinterpret_cast<const float4*>(P + 2 * DM + f);
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
-        const float v0 = (acc[ft][tt][4 * j] - mean[tt]) * rstd[tt] * gg.x + bb.x;
-        const float v1 = (acc[ft][tt][4 * j + 1] - mean[tt]) * rstd[tt] * gg.y + bb.y;
-        const float v2 = (acc[ft][tt][4 * j + 2] - mean[tt]) * rstd[tt] * gg.z + bb.z;
-        const float v3 = (acc[ft][tt][4 * j + 3] - mean[tt]) * rstd[tt] * gg.w + bb.w;
+        const float v0 = fmaf(fmaf(acc[ft][tt][4 * j], rstd[tt], shift[tt]), gg.x, bb.x);
+        const float v1 = fmaf(fmaf(acc[ft][tt][4 * j + 1], rstd[tt], shift[tt]), gg.y, bb.y);
+        const float v2 = fmaf(fmaf(acc[ft][tt][4 * j + 2], rstd[tt], shift[tt]), gg.z, bb.z);
+        const float v3 = fmaf(fmaf(acc[ft][tt][4 * j + 3], rstd[tt], shift[tt]), gg.w, bb.w);
         acc[ft][tt][4 * j] = v0;
         acc[ft][tt][4 * j + 1] = v1;
         acc[ft][tt][4 * j + 2] = v2;
@@ -303,8 +378,9 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* bia
 }
 
 // ---------------------------------------------------------------- pooling
-// Max over the block's valid tokens (token < nvalid) of Y^T = acc + b_pool, folded
-// into pmax.  The 64 per-lane features are max-reduced across the 32 lanes of a
+// Max over the block's valid tokens (token < nvalid) of Y^T = acc, folded into
+// pmax (b_pool is added to the final max: rounding is monotonic, so
+// max(y + b) = max(y) + b exactly).  The 64 per-lane features are max-reduced across the 32 lanes of a
 // half with a transposing butterfly (each step halves the values a lane keeps).
 // Ends with a barrier.
 #define FZ_TMAX(HALF, MASK)                                                   \
@@ -315,8 +391,8 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* bia
     v[k] = fmaxf(keep, __shfl_xor(send, (MASK), WAVE));                       \
   }
 
-__device__ __forceinline__ void pool_block(f32x16 (&acc)[4][2], const float* b_pool, float* pmax,
-                                           float* red, int nvalid) {
+__device__ __forceinline__ void pool_block(f32x16 (&acc)[4][2], float* pmax, float* red,
+                                           int nvalid) {
   FZ_LANE_VARS
   float v[64];
 #pragma unroll
@@ -341,7 +417,7 @@ __device__ __forceinline__ void pool_block(f32x16 (&acc)[4][2], const float* b_p
   for (int u = 0; u < 2; ++u) {
     const int k = base + u;
     const int f = fh * 128 + (k >> 4) * 32 + 8 * ((k & 15) >> 2) + 4 * hf + (k & 3);
-    red[th * DM + f] = v[u] + b_pool[f];
+    red[th * DM + f] = v[u];
   }
   __syncthreads();
   {
@@ -385,16 +461,20 @@ __device__ __forceinline__ void attn_init(AttnState<DH>& st, const bf16_t* Qs, i
 // [dim][vld]) for query tile qt.  S^T tile t holds keys k0 + 16t + 4gq + i; the P^T
 // fragment takes them in that order (keys 4gq.., then 16 + 4gq..) and V^T is read
 // to match.  CAUSAL masks keys above the lane's query row (only a step that
-// reaches past the tile's first query has any).  Scores stay unscaled until the
-// exponent: max(s) scaled equals the max of the scaled scores, and the scale and
-// the max are applied by one fma.  exp2 is the hardware instruction (results
-// below 2^-126 flush to zero, far under the bf16 resolution of P).
+// reaches past the tile's first query has any).
+// Online softmax with a lazily raised reference: p = 2^(s sc - m) is accumulated
+// against the query's reference m, which is only raised (rescaling l and O) when
+// a score would exceed it by more than 2^8.  Any reference gives the same O / l;
+// bounding p by 2^8 keeps the sums far from overflow, and the common step needs
+// no cross-lane max.  exp2 is the hardware instruction (results below 2^-126
+// flush to zero, far under the bf16 resolution of P).
 template <int DH, bool CAUSAL>
 __device__ __forceinline__ void attn_step(AttnState<DH>& st, const bf16_t* Kl, int kld,
                                           const bf16_t* Vl, int vld, int col0, int k0, int qt,
                                           int lane) {
   const int gq = lane / 16, c16 = lane % 16;
   constexpr float sc = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
+  constexpr float HEADROOM = 8.f;
   f32x4v s[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
@@ -417,25 +497,29 @@ __device__ __forceinline__ void attn_step(AttnState<DH>& st, const bf16_t* Kl, i
       for (int i = 0; i < 4; ++i)
         if (k0 + 16 * t + 4 * gq + i > qrow) s[t][i] = -__builtin_inff();
   }
-  float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                   fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-  mx = xmax32(xmax16(mx));
-  const float mnew = fmaxf(st.m, mx * sc);
-  const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
+  const float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+  if (__builtin_amdgcn_ballot_w64(mx * sc > st.m + HEADROOM) != 0) {   // wave-uniform
+    const float mnew = fmaxf(st.m, xmax32(xmax16(mx)) * sc);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
+    st.l *= alpha;
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] *= alpha;
+    st.m = mnew;
+  }
   bf16x8 pb;
   float psum = 0.f;
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float p = __builtin_amdgcn_exp2f(fmaf(s[t][i], sc, -mnew));
+      const float p = __builtin_amdgcn_exp2f(fmaf(s[t][i], sc, -st.m));
       psum += p;
       pb[4 * t + i] = static_cast<__bf16>(p);
     }
-  st.l = st.l * alpha + psum;
-  st.m = mnew;
+  st.l += psum;
 #pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = mfma16(vf[dt], pb, st.o[dt] * alpha);
+  for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = mfma16(vf[dt], pb, st.o[dt]);
 }
 
 // O = O^T / l into the tile's rows of Qs (the tile's Q is already in registers).
@@ -557,7 +641,7 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
   {
     const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
-    resid_phase<KIN / 16>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), nxt, Xs, XLD);
+    resid_phase<KIN / 16, 3>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), nxt, Xs, XLD);
   }
   {
     FZ_LANE_VARS
@@ -618,6 +702,21 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
   constexpr int NKB = DM / 16;
   constexpr int cs = CS;
   const int tp = w & 1;
+  // epilogue biases, loaded before this phase issues the next phase's weight
+  // loads (vector memory loads complete in order)
+  float4 bq[3][4];
+  float bv[3];
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const int ct = 3 * cs + t;
+    const float* bias = b_qkv + (ct >> 1) * DM + g * 64 + (ct & 1) * 32;
+    if ((ct >> 1) < 2) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bq[t][j] = *reinterpret_cast<const float4*>(bias + 8 * j + 4 * hf);
+    } else {
+      bv[t] = bias[l32];
+    }
+  }
   f32x16 qa[3][2];
 #pragma unroll
   for (int t = 0; t < 3; ++t) qa[t][0] = qa[t][1] = f32x16{};
@@ -628,15 +727,6 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
   xq[0][1] = lfrag(arow + 32 * XLD);
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
-    bf16x8 a[3];
-#pragma unroll
-    for (int f = 0; f < 3; ++f) a[f] = j < PD ? pre[j][f] : wq[j][f];
-    if (j + PD < NKB) {
-#pragma unroll
-      for (int f = 0; f < 3; ++f) wq[j + PD][f] = gfrag(cur.P, cur.nkb, seg_rt(cur, f), j + PD, lane);
-    } else {
-      seg_load(pre, j + PD - NKB, nxt, lane);
-    }
     if (j + 1 < NKB) {
       xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
       xq[j + 1][1] = lfrag(arow + 32 * XLD + (j + 1) * 16);
@@ -644,25 +734,28 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
     if constexpr (CS == 0) {   // q0 q1 k0: transposed
 #pragma unroll
       for (int t = 0; t < 3; ++t) {
-        qa[t][0] = mfma32(a[t], xq[j][0], qa[t][0]);
-        qa[t][1] = mfma32(a[t], xq[j][1], qa[t][1]);
+        const bf16x8 a = stream_frag<NKB, 3>(wq, pre, j, t);
+        qa[t][0] = mfma32(a, xq[j][0], qa[t][0]);
+        qa[t][1] = mfma32(a, xq[j][1], qa[t][1]);
       }
     } else {         // k1 transposed; v0 v1 untransposed
-      qa[0][0] = mfma32(a[0], xq[j][0], qa[0][0]);
-      qa[0][1] = mfma32(a[0], xq[j][1], qa[0][1]);
+      const bf16x8 a0 = stream_frag<NKB, 3>(wq, pre, j, 0);
+      qa[0][0] = mfma32(a0, xq[j][0], qa[0][0]);
+      qa[0][1] = mfma32(a0, xq[j][1], qa[0][1]);
 #pragma unroll
       for (int t = 1; t < 3; ++t) {
-        qa[t][0] = mfma32(xq[j][0], a[t], qa[t][0]);
-        qa[t][1] = mfma32(xq[j][1], a[t], qa[t][1]);
+        const bf16x8 a = stream_frag<NKB, 3>(wq, pre, j, t);
+        qa[t][0] = mfma32(xq[j][0], a, qa[t][0]);
+        qa[t][1] = mfma32(xq[j][1], a, qa[t][1]);
       }
     }
+    stream_fetch<NKB, 3, 4>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
   for (int t = 0; t < 3; ++t) {
     const int ct = 3 * cs + t;
     const int part = ct >> 1, dt = ct & 1;
-    const float* bias = b_qkv + part * DM + g * 64 + dt * 32;
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int tt = 2 * tp + u;
@@ -671,16 +764,16 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int dim = 8 * j + 4 * hf;
-          const float4 bv = *reinterpret_cast<const float4*>(bias + dim);
-          st4(dst + (tt * 32 + l32) * QLD + dt * 32 + dim, qa[t][u][4 * j] + bv.x,
-              qa[t][u][4 * j + 1] + bv.y, qa[t][u][4 * j + 2] + bv.z, qa[t][u][4 * j + 3] + bv.w);
+          const float4 b4 = bq[t][j];
+          st4(dst + (tt * 32 + l32) * QLD + dt * 32 + dim, qa[t][u][4 * j] + b4.x,
+              qa[t][u][4 * j + 1] + b4.y, qa[t][u][4 * j + 2] + b4.z, qa[t][u][4 * j + 3] + b4.w);
         }
       } else {
-        const float bv = bias[l32];
+        const float b1 = bv[t];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j] + bv,
-              qa[t][u][4 * j + 1] + bv, qa[t][u][4 * j + 2] + bv, qa[t][u][4 * j + 3] + bv);
+          st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j] + b1,
+              qa[t][u][4 * j + 1] + b1, qa[t][u][4 * j + 2] + b1, qa[t][u][4 * j + 3] + b1);
       }
     }
   }
@@ -693,6 +786,12 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
   FZ_LANE_VARS
   constexpr int NKB = DM / 16;
   const int hp = w & 1, tp = w >> 1;
+  float4 bh[2][4];   // epilogue biases, loaded before the next phase's weight loads
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      bh[t][j] = *reinterpret_cast<const float4*>(b_1 + c * FC + (2 * hp + t) * 32 + 8 * j + 4 * hf);
   f32x16 ha[2][2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) ha[t][0] = ha[t][1] = f32x16{};
@@ -703,24 +802,17 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
   xq[0][1] = lfrag(arow + 32 * XLD);
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
-    bf16x8 a[2];
-#pragma unroll
-    for (int f = 0; f < 2; ++f) a[f] = j < PD ? pre[j][f] : wq[j][f];
-    if (j + PD < NKB) {
-#pragma unroll
-      for (int f = 0; f < 2; ++f) wq[j + PD][f] = gfrag(cur.P, cur.nkb, seg_rt(cur, f), j + PD, lane);
-    } else {
-      seg_load(pre, j + PD - NKB, nxt, lane);
-    }
     if (j + 1 < NKB) {
       xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
       xq[j + 1][1] = lfrag(arow + 32 * XLD + (j + 1) * 16);
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      ha[t][0] = mfma32(a[t], xq[j][0], ha[t][0]);
-      ha[t][1] = mfma32(a[t], xq[j][1], ha[t][1]);
+      const bf16x8 a = stream_frag<NKB, 2>(wq, pre, j, t);
+      ha[t][0] = mfma32(a, xq[j][0], ha[t][0]);
+      ha[t][1] = mfma32(a, xq[j][1], ha[t][1]);
     }
+    stream_fetch<NKB, 2, 4>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
@@ -730,7 +822,7 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int hid = (2 * hp + t) * 32 + 8 * j + 4 * hf;
-        const float4 bv = *reinterpret_cast<const float4*>(b_1 + c * FC + hid);
+        const float4 bv = bh[t][j];
         st4(Hs + ((2 * tp + u) * 32 + l32) * HLD + hid, fmaxf(ha[t][u][4 * j] + bv.x, 0.f),
             fmaxf(ha[t][u][4 * j + 1] + bv.y, 0.f), fmaxf(ha[t][u][4 * j + 2] + bv.z, 0.f),
             fmaxf(ha[t][u][4 * j + 3] + bv.w, 0.f));
@@ -739,11 +831,11 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
 
 // Attention sublayer of one layer for the block: per 64-dim head group, Q / K /
 // V^T into LDS (and K / V^T into the cache for later blocks), causal attention
-// per head, and acc += O_g W_o[:, group]^T.  `after` is the phase that follows
-// the sublayer (the first FFN chunk).
+// per head, and acc += O_g W_o[:, group]^T.  The stream leaves primed with the
+// first FFN chunk of the layer.
 __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_layer& L,
                                                    const LayerPk& pk, f32x16 (&acc)[4][2],
-                                                   Pre& pre, const WSeg& after, bf16_t* Xs,
+                                                   Pre& pre, bf16_t* Xs,
                                                    bf16_t* Qs, bf16_t* Ks, bf16_t* Vts, bf16_t* Kc,
                                                    bf16_t* Vc, bf16_t* kc, bf16_t* vc, int p0,
                                                    bool keep) {
@@ -777,18 +869,25 @@ __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_lay
     else
       attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
     __syncthreads();
-    const WSeg nq = g + 1 < DM / 64 ? seg_qkv(pk.qkv, g + 1, w) : after;
-    resid_phase<4>(acc, pre, so, nq, Qs, QLD);
+    if (g + 1 < DM / 64) {
+      resid_phase<4, 3>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD);
+    } else {   // Ks is free now: it receives the LayerNorm parameters
+      const LnParams q = ln_params_load(L.b_o, L.ln1_g, L.ln1_b);
+      resid_phase<4, 2>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
+      ln_params_store(q, reinterpret_cast<float*>(Ks));
+    }
     __syncthreads();   // Qs (O) and Ks / Vts are rewritten by the next group
   }
 }
 
 // FFN sublayer: per chunk of 128 hidden units, H^T into LDS, then
 // acc += W_2[:, chunk] H^T.  The stream enters primed with chunk 0 and leaves
-// primed with `after`.
+// primed with `after`: the next layer's first Q / K / V phase, or (last layer)
+// the pooling projection.
 __device__ __forceinline__ void ffn_sublayer(const Args& A, const tav2_layer& L,
                                              const LayerPk& pk, f32x16 (&acc)[4][2], Pre& pre,
-                                             const WSeg& after, bf16_t* Xs, bf16_t* Hs) {
+                                             const WSeg& after, bool after_is_qkv, bf16_t* Xs,
+                                             bf16_t* Hs) {
   const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
   const int ffn = A.ffn;
   const int nch = ffn / FC;
@@ -796,8 +895,16 @@ __device__ __forceinline__ void ffn_sublayer(const Args& A, const tav2_layer& L,
     const WSeg s2 = seg_resid(pk.w2, ffn / 16, c * (FC / 16), w);
     ffn1_phase(pre, seg_ffn1(pk.w1, c, w), s2, L.b_1, c, Xs, Hs);
     __syncthreads();
-    const WSeg nx = c + 1 < nch ? seg_ffn1(pk.w1, c + 1, w) : after;
-    resid_phase<FC / 16>(acc, pre, s2, nx, Hs, HLD);
+    if (c + 1 < nch) {
+      resid_phase<FC / 16, 2>(acc, pre, s2, seg_ffn1(pk.w1, c + 1, w), Hs, HLD);
+    } else {   // the LayerNorm parameters go past the hidden chunk
+      const LnParams q = ln_params_load(L.b_2, L.ln2_g, L.ln2_b);
+      if (after_is_qkv)
+        resid_phase<FC / 16, 3>(acc, pre, s2, after, Hs, HLD);
+      else
+        resid_phase<FC / 16, 4>(acc, pre, s2, after, Hs, HLD);
+      ln_params_store(q, reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(Hs) + BT * HLD * 2));
+    }
     __syncthreads();   // Hs is rewritten by the next chunk
   }
 }
@@ -815,6 +922,8 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
   bf16_t* Vts = reinterpret_cast<bf16_t*>(Sc + 2 * QS_BYTES);    // [64][VLD]
   bf16_t* Hs = reinterpret_cast<bf16_t*>(Sc);                    // [BT][HLD]
   float* red = reinterpret_cast<float*>(Sc);                     // reductions
+  float* lnp1 = reinterpret_cast<float*>(Sc + QS_BYTES);         // LayerNorm 1 parameters
+  float* lnp2 = reinterpret_cast<float*>(Sc + BT * HLD * 2);     // LayerNorm 2 parameters
   int* tinfo = reinterpret_cast<int*>(Sc);                       // [BT] during encoding
   const uint8_t** rowptr = reinterpret_cast<const uint8_t**>(Sc + BT * 8);   // [BT]
 
@@ -835,7 +944,7 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
   const WSeg s_embed = seg_resid(A.pk_in, KIN / 16, 0, wv);
   const WSeg s_pool = seg_resid(A.pk_pool, DM / 16, 0, wv);
   Pre pre;
-  seg_prime(pre, s_embed, otid() % WAVE);
+  seg_prime<4>(pre, s_embed, otid() % WAVE);
   f32x16 acc[4][2];
   for (int blk = 0; blk < nblk; ++blk) {
     const int p0 = blk * BT;
@@ -847,12 +956,13 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
       const LayerPk pk = AK->pk[li];
       bf16_t* kc = A.kcache ? A.kcache + (nl * A.n_layers + li) * int64_t(A.tpad) * DM : nullptr;
       bf16_t* vc = A.vcache ? A.vcache + (nl * A.n_layers + li) * int64_t(DM) * A.tpad : nullptr;
-      attention_sublayer(A, L, pk, acc, pre, seg_ffn1(pk.w1, 0, wv), Xs, Qs, Ks, Vts, Kc, Vc, kc,
-                         vc, p0, blk + 1 < nblk);
-      layer_norm(acc, L.b_o, L.ln1_g, L.ln1_b, red, Xs);
-      const WSeg after = li + 1 < A.n_layers ? seg_qkv(AK->pk[li + 1].qkv, 0, wv) : s_pool;
-      ffn_sublayer(A, L, pk, acc, pre, after, Xs, Hs);
-      layer_norm(acc, L.b_2, L.ln2_g, L.ln2_b, red, Xs);
+      attention_sublayer(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0,
+                         blk + 1 < nblk);
+      layer_norm(acc, lnp1, red, Xs);
+      const bool more = li + 1 < A.n_layers;
+      const WSeg after = more ? seg_qkv(AK->pk[li + 1].qkv, 0, wv) : s_pool;
+      ffn_sublayer(A, L, pk, acc, pre, after, more, Xs, Hs);
+      layer_norm(acc, lnp2, red, Xs);
     }
     // ---- head: out[DM:] = X of the last valid token; running max of the pool
     {
@@ -880,10 +990,10 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
       for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
     // the pool phase prefetches the next block's input projection (also after the
     // last block, where the loads are simply unused)
-    resid_phase<DM / 16>(acc, pre, s_pool, s_embed, Xs, XLD);
-    pool_block(acc, A.b_pool, pmax, red, Tv - p0);
+    resid_phase<DM / 16, 4>(acc, pre, s_pool, s_embed, Xs, XLD);
+    pool_block(acc, pmax, red, Tv - p0);
   }
-  for (int c = threadIdx.x; c < DM; c += NT) out[c] = pmax[c];
+  for (int c = threadIdx.x; c < DM; c += NT) out[c] = pmax[c] + A.b_pool[c];
 }
 
 // ---------------------------------------------------------------- candidate half
@@ -1016,10 +1126,13 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
     J.kvalid = kvalid;
     J.first = items;
     items += int64_t(rows) * K / 8;
+    const int frag = int(off / 512);   // 512 bf16 per fragment; every matrix is whole fragments
     off += size_t(rows) * K;
-    return static_cast<const bf16_t*>(J.dst);
+    return frag;
   };
   fz::Args a{};
+  a.pkw = pk;
+  a.pk_bytes = unsigned(packed_bytes(w));
   a.pk_in = add(w.W_in, dm, fz::KIN, 2 * d, d);
   a.pk_pool = add(w.W_pool, dm, dm, dm, dm);
   for (int i = 0; i < w.n_layers; ++i) {
