@@ -50,6 +50,9 @@ constexpr int FC = 128;          // FFN hidden units per chunk
 constexpr int HLD = FC + 8;      // Hs row stride
 constexpr int MAX_LAYERS = 8;
 constexpr int KIN = 256;         // packed width of the token half of W_in (d zero-padded)
+constexpr int N_ACT = 8;         // action-type table rows (types are clamped to 0..7)
+constexpr int N_TIME = 64;       // time-bucket table rows (buckets are clamped to 0..63)
+constexpr int AT_COLS = 80;      // packed [E_act^T | 0 | E_time^T] columns: 0..7, 16..79
 
 constexpr int XS_BYTES = BT * XLD * 2;                 // 67584
 constexpr int QS_BYTES = BT * QLD * 2;                 // 18432
@@ -61,7 +64,7 @@ constexpr int LDS_BYTES = XS_BYTES + SC_BYTES + CS_BYTES + PM_BYTES;
 static_assert(LDS_BYTES <= 163840, "fused encoder exceeds the 160 KiB of LDS");
 static_assert(BT * HLD * 2 <= SC_BYTES, "FFN chunk does not fit the scratch region");
 static_assert(BT * HLD * 2 + 3 * DM * 4 <= SC_BYTES, "LayerNorm 2 parameters do not fit");
-static_assert(BT * 4 * 4 <= QS_BYTES && 3 * DM * 4 <= QS_BYTES, "LayerNorm 1 buffers do not fit");
+static_assert(BT * 4 * 4 <= QS_BYTES && 3 * DM * 4 <= CS_BYTES, "LayerNorm 1 buffers do not fit");
 static_assert(BT * 8 + BT * 8 <= SC_BYTES, "encoding buffers do not fit");
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -139,6 +142,9 @@ struct Args {
   unsigned pk_bytes;
   int pk_in;                // packed token half of W_in, [256][KIN / 16]
   int pk_pool;              // packed W_pool
+  int pk_at;                // packed [E_act^T | E_time^T], [256][AT_COLS / 16]
+  int pk_pos;               // packed E_pos^T, [256][pos_nkb]
+  int pos_nkb;
   tav2_layer layers[MAX_LAYERS];   // biases and LayerNorm vectors
   LayerPk pk[MAX_LAYERS];
   int n_layers;
@@ -279,6 +285,73 @@ __device__ __forceinline__ void resid_phase(f32x16 (&acc)[4][2], Pre& pre, const
       acc[ft][0] = mfma32(a, xq[j][0], acc[ft][0]);
       acc[ft][1] = mfma32(a, xq[j][1], acc[ft][1]);
     }
+    stream_fetch<NKB, 4, NRN>(wq, pre, cur, nxt, j, lane);
+    sched_fence();
+  }
+}
+
+// ---------------------------------------------------------------- table rows
+// The side tables enter the encoding as products with one-hot matrices built in
+// registers: acc^T += E^T onehot, with E^T streamed like the weights.  For the
+// 32x32x16 B operand a lane holds column l % 32 (a token) and k-rows
+// 8 (l / 32) .. +7, so each fragment has at most one 1.0.
+__device__ __forceinline__ bf16x8 onehot8(int idx) {   // 1.0 at element idx (none if outside 0..7)
+  const unsigned one = 0x3F80u;                          // bf16 1.0
+  u32x4 v;
+  v.x = idx == 0 ? one : idx == 1 ? (one << 16) : 0u;
+  v.y = idx == 2 ? one : idx == 3 ? (one << 16) : 0u;
+  v.z = idx == 4 ? one : idx == 5 ? (one << 16) : 0u;
+  v.w = idx == 6 ? one : idx == 7 ? (one << 16) : 0u;
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// acc += E_act[act_t] + E_time[time_t] for the block's tokens: k-block 0 holds the
+// 8 action types, k-blocks 1..4 the 64 time buckets (at columns 16 + bucket).
+template <int NRN>
+__device__ __forceinline__ void table_phase(f32x16 (&acc)[4][2], Pre& pre, const WSeg& cur,
+                                            const WSeg& nxt, const int* tinfo) {
+  FZ_LANE_VARS
+  constexpr int NKB = AT_COLS / 16;
+  bf16x8 wq[NKB][4];
+  int ka[2], kt[2];   // the token's one-hot column, relative to this lane's k-rows
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    const int info = tinfo[th * 64 + tt * 32 + l32];
+    ka[tt] = (info & 0xFF) - 8 * hf;
+    kt[tt] = 16 + ((info >> 8) & 0xFF) - 8 * hf;
+  }
+#pragma unroll
+  for (int j = 0; j < NKB; ++j) {
+    bf16x8 b[2];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) b[tt] = onehot8(j == 0 ? ka[tt] : kt[tt] - 16 * j);
+#pragma unroll
+    for (int ft = 0; ft < 4; ++ft) {
+      const bf16x8 a = stream_frag<NKB, 4>(wq, pre, j, ft);
+      acc[ft][0] = mfma32(a, b[0], acc[ft][0]);
+      acc[ft][1] = mfma32(a, b[1], acc[ft][1]);
+    }
+    stream_fetch<NKB, 4, NRN>(wq, pre, cur, nxt, j, lane);
+    sched_fence();
+  }
+}
+
+// acc += E_pos[p0 + r] for the block's tokens r: the wave's 64 tokens are the
+// 4 k-blocks of E_pos^T from position p0 + 64 (w >> 1); k-block j only meets
+// token tile j / 2.
+template <int NRN>
+__device__ __forceinline__ void pos_phase(f32x16 (&acc)[4][2], Pre& pre, const WSeg& cur,
+                                          const WSeg& nxt) {
+  FZ_LANE_VARS
+  constexpr int NKB = 4;
+  bf16x8 wq[NKB][4];
+#pragma unroll
+  for (int j = 0; j < NKB; ++j) {
+    const int tt = j >> 1;
+    const bf16x8 b = onehot8(l32 - 16 * (j & 1) - 8 * hf);
+#pragma unroll
+    for (int ft = 0; ft < 4; ++ft)
+      acc[ft][tt] = mfma32(stream_frag<NKB, 4>(wq, pre, j, ft), b, acc[ft][tt]);
     stream_fetch<NKB, 4, NRN>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
@@ -591,11 +664,12 @@ __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf
 __device__ __forceinline__ int64_t nl_of(const Args& A, int64_t n) { return n - A.c0; }
 
 // ---------------------------------------------------------------- block input
-// Feature encoding of block rows [p0, p0 + BT): token rows into Xs (zeros past the
-// valid length and past d), then acc = X0^T = W_in[:, :d] Xs^T + cvec + E_act +
-// E_time + E_pos (zero for padding positions), Xs <- bf16(X0).  cvec (the
-// candidate half of the projection plus b_in) is computed once per candidate by
-// cand_proj_kernel.
+// Feature encoding of block rows [p0, p0 + BT) (Eq. 4 with early fusion):
+// acc = X0^T = cvec + W_in[:, :d] Xs^T + E_act^T onehot(act) + E_time^T
+// onehot(time) + E_pos^T onehot(position), and Xs <- bf16(X0).  cvec (the
+// candidate half of the projection plus b_in) comes from cand_proj_kernel.  Rows
+// past the valid length get whatever these give (token rows of zeros): no valid
+// row ever reads them (causal mask, per-token sublayers, pooling over valid rows).
 __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int p0, int Tv,
                                                    f32x16 (&acc)[4][2], bf16_t* Xs,
                                                    int* tinfo, const uint8_t** rowptr, Pre& pre,
@@ -616,8 +690,11 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
       tinfo[tid] = info;
     }
     __syncthreads();
+  }
+  {
     // all of the thread's row pieces in flight at once, then into LDS
     constexpr int PER = BT * (KIN / 8) / NT;
+    const int tid = otid();
     u32x4 v[PER];
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
@@ -627,6 +704,23 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
       v[q] = u32x4{0u, 0u, 0u, 0u};
       if (rp && c < d / 8) v[q] = reinterpret_cast<const u32x4*>(rp)[c];
     }
+    {   // accumulators <- cvec
+      FZ_LANE_VARS
+      const float* cv = A.cvec + nl_of(A, n) * DM;
+#pragma unroll
+      for (int ft = 0; ft < 4; ++ft)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float4 c4 = *reinterpret_cast<const float4*>(cv + fh * 128 + ft * 32 + 8 * j + 4 * hf);
+#pragma unroll
+          for (int tt = 0; tt < 2; ++tt) {
+            acc[ft][tt][4 * j] = c4.x;
+            acc[ft][tt][4 * j + 1] = c4.y;
+            acc[ft][tt][4 * j + 2] = c4.z;
+            acc[ft][tt][4 * j + 3] = c4.w;
+          }
+        }
+    }
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
       const int e = tid + q * NT;
@@ -635,45 +729,16 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
     }
     __syncthreads();
   }
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
   {
     const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
-    resid_phase<KIN / 16, 3>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), nxt, Xs, XLD);
+    const WSeg s_at = seg_resid(A.pk_at, AT_COLS / 16, 0, w);
+    const WSeg s_pos = seg_resid(A.pk_pos, A.pos_nkb, p0 / 16 + 4 * (w >> 1), w);
+    resid_phase<KIN / 16, 4>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), s_at, Xs, XLD);
+    table_phase<4>(acc, pre, s_at, s_pos, tinfo);
+    pos_phase<3>(acc, pre, s_pos, nxt);
   }
   {
     FZ_LANE_VARS
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      const int r = th * 64 + tt * 32 + l32;
-      const int info = tinfo[r];
-      const bool valid = (info >> 16) & 1;
-      const int act = info & 0xFF, tim = (info >> 8) & 0xFF;
-      const int p = valid ? p0 + r : 0;
-#pragma unroll
-      for (int ft = 0; ft < 4; ++ft)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int f = fh * 128 + ft * 32 + 8 * j + 4 * hf;
-          const uint2 ea = *reinterpret_cast<const uint2*>(A.E_act + act * DM + f);
-          const uint2 ep = *reinterpret_cast<const uint2*>(A.E_pos + int64_t(p) * DM + f);
-          uint2 et = make_uint2(0, 0);
-          if (A.E_time) et = *reinterpret_cast<const uint2*>(A.E_time + tim * DM + f);
-          const float4 cv = *reinterpret_cast<const float4*>(A.cvec + nl_of(A, n) * DM + f);
-          const bf16_t* eap = reinterpret_cast<const bf16_t*>(&ea);
-          const bf16_t* epp = reinterpret_cast<const bf16_t*>(&ep);
-          const bf16_t* etp = reinterpret_cast<const bf16_t*>(&et);
-          const float cva[4] = {cv.x, cv.y, cv.z, cv.w};
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float v = acc[ft][tt][4 * j + i];
-            acc[ft][tt][4 * j + i] =
-                valid ? v + cva[i] + bf2f(eap[i]) + bf2f(epp[i]) + bf2f(etp[i]) : 0.f;
-          }
-        }
-    }
     __syncthreads();   // every wave is past Xs (tokens) and tinfo
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt)
@@ -829,6 +894,27 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
       }
 }
 
+// This block's K and V^T of head group g into the candidate's cache (read by the
+// candidate's later blocks).
+__device__ __forceinline__ void cache_store(const Args& A, int g, int p0, const bf16_t* Ks,
+                                            const bf16_t* Vts, bf16_t* kc, bf16_t* vc) {
+  const int tid = otid();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = tid + q * NT;
+    const int r = e >> 3, c = (e & 7) * 8;
+    *reinterpret_cast<u32x4*>(kc + int64_t(p0 + r) * DM + g * 64 + c) =
+        *reinterpret_cast<const u32x4*>(Ks + r * QLD + c);
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = tid + q * NT;
+    const int r = e >> 4, c = (e & 15) * 8;
+    *reinterpret_cast<u32x4*>(vc + int64_t(g * 64 + r) * A.tpad + p0 + c) =
+        *reinterpret_cast<const u32x4*>(Vts + r * VLD + c);
+  }
+}
+
 // Attention sublayer of one layer for the block: per 64-dim head group, Q / K /
 // V^T into LDS (and K / V^T into the cache for later blocks), causal attention
 // per head, and acc += O_g W_o[:, group]^T.  The stream leaves primed with the
@@ -847,34 +933,21 @@ __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_lay
     else
       qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
     __syncthreads();
-    if (keep) {   // this block's K and V^T for the later blocks of the candidate
-      const int tid = otid();
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int e = tid + q * NT;
-        const int r = e >> 3, c = (e & 7) * 8;
-        *reinterpret_cast<u32x4*>(kc + int64_t(p0 + r) * DM + g * 64 + c) =
-            *reinterpret_cast<const u32x4*>(Ks + r * QLD + c);
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int e = tid + q * NT;
-        const int r = e >> 4, c = (e & 15) * 8;
-        *reinterpret_cast<u32x4*>(vc + int64_t(g * 64 + r) * A.tpad + p0 + c) =
-            *reinterpret_cast<const u32x4*>(Vts + r * VLD + c);
-      }
-    }
     if (A.dh == 64)
       attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
     else
       attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
     __syncthreads();
+    // the cache stores follow the phase's weight loads, so the next phase's first
+    // wait on its weights does not also wait for the stores
     if (g + 1 < DM / 64) {
       resid_phase<4, 3>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD);
-    } else {   // Ks is free now: it receives the LayerNorm parameters
+      if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
+    } else {   // the staging area is free now: it receives the LayerNorm parameters
       const LnParams q = ln_params_load(L.b_o, L.ln1_g, L.ln1_b);
       resid_phase<4, 2>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
-      ln_params_store(q, reinterpret_cast<float*>(Ks));
+      if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
+      ln_params_store(q, reinterpret_cast<float*>(Kc));
     }
     __syncthreads();   // Qs (O) and Ks / Vts are rewritten by the next group
   }
@@ -922,7 +995,7 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
   bf16_t* Vts = reinterpret_cast<bf16_t*>(Sc + 2 * QS_BYTES);    // [64][VLD]
   bf16_t* Hs = reinterpret_cast<bf16_t*>(Sc);                    // [BT][HLD]
   float* red = reinterpret_cast<float*>(Sc);                     // reductions
-  float* lnp1 = reinterpret_cast<float*>(Sc + QS_BYTES);         // LayerNorm 1 parameters
+  float* lnp1 = reinterpret_cast<float*>(Kc);                    // LayerNorm 1 parameters
   float* lnp2 = reinterpret_cast<float*>(Sc + BT * HLD * 2);     // LayerNorm 2 parameters
   int* tinfo = reinterpret_cast<int*>(Sc);                       // [BT] during encoding
   const uint8_t** rowptr = reinterpret_cast<const uint8_t**>(Sc + BT * 8);   // [BT]
@@ -1039,11 +1112,16 @@ __global__ __launch_bounds__(DM) void cand_proj_kernel(const bf16_t* __restrict_
 // 16 kb + 8 (l / 32) .. +7.
 struct PackJob {
   const bf16_t* src;
-  bf16_t* dst;
-  int rows, K, ld, kvalid;
-  int64_t first;   // first item (16-byte piece) of this job
+  bf16_t* dst;       // first fragment of the destination matrix
+  int rows;          // destination rows (multiple of 32)
+  int nkb;           // k-blocks per destination row
+  int kb0, nkbj;     // k-blocks [kb0, kb0 + nkbj) of the destination written by this job
+  int ld;            // source row stride (elements)
+  int kvalid;        // job columns >= kvalid are zero
+  int trans;         // destination (row r, job column k) = src[k * ld + r] instead of src[r * ld + k]
+  int64_t first;     // first item (16-byte piece) of this job
 };
-constexpr int MAX_JOBS = 2 + 4 * MAX_LAYERS;
+constexpr int MAX_JOBS = 4 + 4 * MAX_LAYERS;
 struct PackArgs {
   PackJob job[MAX_JOBS];
   int njobs;
@@ -1059,12 +1137,18 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(PackArgs P) {
   const int64_t e = it - J.first;               // piece within the job
   const int lane = int(e % 64);
   const int64_t frag = e / 64;
-  const int nkb = J.K / 16;
-  const int rt = int(frag / nkb), kb = int(frag % nkb);
-  const int row = rt * 32 + lane % 32, col = kb * 16 + 8 * (lane / 32);
+  const int rt = int(frag / J.nkbj), kbj = int(frag % J.nkbj);
+  const int row = rt * 32 + lane % 32, col = kbj * 16 + 8 * (lane / 32);   // job column
   uint4 v = make_uint4(0, 0, 0, 0);
-  if (col < J.kvalid) v = *reinterpret_cast<const uint4*>(J.src + int64_t(row) * J.ld + col);
-  *reinterpret_cast<uint4*>(J.dst + e * 8) = v;
+  if (!J.trans) {
+    if (col < J.kvalid) v = *reinterpret_cast<const uint4*>(J.src + int64_t(row) * J.ld + col);
+  } else {
+    bf16_t x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = col + u < J.kvalid ? J.src[int64_t(col + u) * J.ld + row] : bf16_t(0);
+    v = *reinterpret_cast<const uint4*>(x);
+  }
+  *reinterpret_cast<uint4*>(J.dst + ((int64_t(rt) * J.nkb + J.kb0 + kbj) * 64 + lane) * 8) = v;
 }
 
 }  // namespace fz
@@ -1088,10 +1172,14 @@ int64_t fused_chunk(int64_t total, int T, const tav2_weights& w) {
   return c < total ? c : (total > 0 ? total : 1);
 }
 
+// packed E_pos^T columns: every position of any 128-position block below max_pos
+int pos_cols(const tav2_weights& w) { return (w.max_pos + fz::BT - 1) / fz::BT * fz::BT; }
+
 size_t packed_bytes(const tav2_weights& w) {
   const size_t dm = fz::DM, ff = size_t(w.d_ffn);
   const size_t per_layer = 3 * dm * dm + dm * dm + ff * dm + dm * ff;
-  return align_up((dm * fz::KIN + dm * dm + size_t(w.n_layers) * per_layer) * 2, 256);
+  const size_t tables = dm * (fz::AT_COLS + size_t(pos_cols(w)));
+  return align_up((dm * fz::KIN + dm * dm + size_t(w.n_layers) * per_layer + tables) * 2, 256);
 }
 }  // namespace
 
@@ -1116,19 +1204,28 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
   fz::PackArgs P{};
   int64_t items = 0;
   size_t off = 0;
-  auto add = [&](const void* srcm, int rows, int K, int ld, int kvalid) {
+  // matrix m of rows x (16 nkb) columns at fragment `off`; add_cols fills k-blocks
+  // [kb0, kb0 + nkbj) from a row-major (or transposed) source
+  auto add_cols = [&](size_t mat, int rows, int nkb, int kb0, int nkbj, const void* srcm, int ld,
+                      int kvalid, int trans) {
     fz::PackJob& J = P.job[P.njobs++];
     J.src = static_cast<const bf16_t*>(srcm);
-    J.dst = pk + off;
+    J.dst = pk + mat;
     J.rows = rows;
-    J.K = K;
+    J.nkb = nkb;
+    J.kb0 = kb0;
+    J.nkbj = nkbj;
     J.ld = ld;
     J.kvalid = kvalid;
+    J.trans = trans;
     J.first = items;
-    items += int64_t(rows) * K / 8;
-    const int frag = int(off / 512);   // 512 bf16 per fragment; every matrix is whole fragments
+    items += int64_t(rows) * nkbj * 2;   // 16-byte pieces: 2 per row per k-block
+  };
+  auto add = [&](const void* srcm, int rows, int K, int ld, int kvalid) {
+    const size_t mat = off;
+    add_cols(mat, rows, K / 16, 0, K / 16, srcm, ld, kvalid, 0);
     off += size_t(rows) * K;
-    return frag;
+    return int(mat / 512);   // 512 bf16 per fragment; every matrix is whole fragments
   };
   fz::Args a{};
   a.pkw = pk;
@@ -1142,6 +1239,18 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
     a.pk[i].w1 = add(L.W_1, ff, dm, dm, dm);
     a.pk[i].w2 = add(L.W_2, dm, ff, ff, ff);
   }
+  // side tables as [feature][row] matrices for the one-hot products of the input
+  // encoding: E_act^T in columns 0..7, E_time^T in columns 16..79 (zero without
+  // a time table); E_pos^T in its own matrix of pos_cols(w) columns
+  a.pk_at = int(off / 512);
+  add_cols(off, dm, fz::AT_COLS / 16, 0, 1, w.E_act, dm, fz::N_ACT, 1);
+  add_cols(off, dm, fz::AT_COLS / 16, 1, 4, w.E_time ? w.E_time : w.E_act, dm,
+           w.E_time ? fz::N_TIME : 0, 1);
+  off += size_t(dm) * fz::AT_COLS;
+  a.pk_pos = int(off / 512);
+  a.pos_nkb = pos_cols(w) / 16;
+  add_cols(off, dm, pos_cols(w) / 16, 0, pos_cols(w) / 16, w.E_pos, dm, w.max_pos, 1);
+  off += size_t(dm) * pos_cols(w);
   P.items = items;
   {
     ProfScope prof("pack_weights", st);
