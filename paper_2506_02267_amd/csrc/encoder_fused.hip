@@ -608,28 +608,47 @@ __device__ __forceinline__ void attn_finish(AttnState<DH>& st, bf16_t* Qs, int c
         st.o[dt][2] * inv, st.o[dt][3] * inv);
 }
 
-// Cached keys [c0, c0 + 128) of head group g (K rows and V^T columns) into LDS.
-// Ends with a barrier.
-__device__ __forceinline__ void stage_cached(const bf16_t* kc, const bf16_t* vc, int tpad, int g,
-                                             int c0, bf16_t* Kc, bf16_t* Vc) {
+// Cached keys [c0, c0 + 128) of head group g (K rows and V^T columns): the loads
+// into registers, and (after the work they overlap) the copy into LDS.
+struct CacheChunk {
+  u32x4 k[4], v[4];
+};
+__device__ __forceinline__ void cache_load(CacheChunk& ch, const bf16_t* kc, const bf16_t* vc,
+                                           int tpad, int g, int c0) {
   const int tid = otid();
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = tid + q * NT;                      // K: 128 keys x 8 pieces
     const int r = e >> 3, c = (e & 7) * 8;
-    *reinterpret_cast<u32x4*>(Kc + r * QLD + c) =
-        *reinterpret_cast<const u32x4*>(kc + int64_t(c0 + r) * DM + g * 64 + c);
+    ch.k[q] = *reinterpret_cast<const u32x4*>(kc + int64_t(c0 + r) * DM + g * 64 + c);
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = tid + q * NT;                      // V^T: 64 dims x 16 pieces
     const int r = e >> 4, c = (e & 15) * 8;
-    *reinterpret_cast<u32x4*>(Vc + r * VLD + c) =
-        *reinterpret_cast<const u32x4*>(vc + int64_t(g * 64 + r) * tpad + c0 + c);
+    ch.v[q] = *reinterpret_cast<const u32x4*>(vc + int64_t(g * 64 + r) * tpad + c0 + c);
+  }
+}
+// Ends with a barrier.
+__device__ __forceinline__ void cache_put(const CacheChunk& ch, bf16_t* Kc, bf16_t* Vc) {
+  const int tid = otid();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = tid + q * NT;
+    *reinterpret_cast<u32x4*>(Kc + (e >> 3) * QLD + (e & 7) * 8) = ch.k[q];
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = tid + q * NT;
+    *reinterpret_cast<u32x4*>(Vc + (e >> 4) * VLD + (e & 15) * 8) = ch.v[q];
   }
   __syncthreads();
 }
 
+// Causal attention of the block's queries for head group g: first the block's
+// own keys (Ks / Vts), then the keys of earlier blocks from the cache, whose
+// first chunk is loaded while the block's own keys are processed (the softmax is
+// independent of the key order).
 template <int DH>
 __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf16_t* Ks,
                                              const bf16_t* Vts, const bf16_t* kc,
@@ -643,18 +662,21 @@ __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf
     AttnState<DH> sa, sb;
     attn_init<DH>(sa, Qs, hd * DH, qa);
     attn_init<DH>(sb, Qs, hd * DH, qb);
+    CacheChunk ch;
+    if (p0 > 0) cache_load(ch, kc, vc, tpad, g, 0);
+    const int na = 16 * qa + 16, nb = 16 * qb + 16;
+    for (int k0 = 0; k0 < nb; k0 += 32) {
+      if (k0 < na) attn_step<DH, true>(sa, Ks, QLD, Vts, VLD, hd * DH, k0, qa, lane);
+      attn_step<DH, true>(sb, Ks, QLD, Vts, VLD, hd * DH, k0, qb, lane);
+    }
     for (int c0 = 0; c0 < p0; c0 += BT) {     // earlier blocks: every key visible
-      stage_cached(kc, vc, tpad, g, c0, Kc, Vc);
+      if (c0 > 0) cache_load(ch, kc, vc, tpad, g, c0);
+      cache_put(ch, Kc, Vc);
       for (int k0 = 0; k0 < BT; k0 += 32) {
         attn_step<DH, false>(sa, Kc, QLD, Vc, VLD, hd * DH, k0, qa, lane);
         attn_step<DH, false>(sb, Kc, QLD, Vc, VLD, hd * DH, k0, qb, lane);
       }
       __syncthreads();
-    }
-    const int na = 16 * qa + 16, nb = 16 * qb + 16;
-    for (int k0 = 0; k0 < nb; k0 += 32) {
-      if (k0 < na) attn_step<DH, true>(sa, Ks, QLD, Vts, VLD, hd * DH, k0, qa, lane);
-      attn_step<DH, true>(sb, Ks, QLD, Vts, VLD, hd * DH, k0, qb, lane);
     }
     attn_finish<DH>(sa, Qs, hd * DH, qa);
     attn_finish<DH>(sb, Qs, hd * DH, qb);
