@@ -37,8 +37,12 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint2& lo, const uint2& hi) {
   uint4 v = make_uint4(lo.x, lo.y, hi.x, hi.y);
   return __builtin_bit_cast(bf16x8, v);
 }
+// Two floats -> packed bf16 pair (a in the low half), round to nearest even: the
+// gfx950 conversion instruction, one per pair.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-  return uint32_t(f2bf(a)) | (uint32_t(f2bf(b)) << 16);
+  const bf16x2_t v = {static_cast<__bf16>(a), static_cast<__bf16>(b)};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // Order-preserving 32-bit key of an fp32 score: larger score <=> larger key,
