@@ -176,7 +176,7 @@ constexpr int NSLOT = 16;
 typedef bf16x8 Pre[NSLOT];
 // k-blocks of look-ahead for a phase with nr row tiles, and the slots it fills
 constexpr int depth(int nr) { return nr == 2 ? FZ_D2 : nr == 3 ? FZ_D3 : FZ_D4; }
-constexpr int used_slots(int nr) { return depth(nr) * nr; }
+constexpr int used_slots(int nr) { return depth(nr) * nr; }   // nr = 0: no next phase
 static_assert(used_slots(2) <= NSLOT && used_slots(3) <= NSLOT && used_slots(4) <= NSLOT, "look-ahead");
 
 struct WSeg {                            // a phase's weight fragments (all wave-uniform)
@@ -530,69 +530,104 @@ __device__ __forceinline__ void attn_init(AttnState<DH>& st, const bf16_t* Qs, i
   st.l = 0.f;
 }
 
-// One 32-key step at key k0 of K (LDS [key][kld], head dims at col0) and V^T (LDS
-// [dim][vld]) for query tile qt.  S^T tile t holds keys k0 + 16t + 4gq + i; the P^T
-// fragment takes them in that order (keys 4gq.., then 16 + 4gq..) and V^T is read
-// to match.  CAUSAL masks keys above the lane's query row (only a step that
-// reaches past the tile's first query has any).
-// Online softmax with a lazily raised reference: p = 2^(s sc - m) is accumulated
-// against the query's reference m, which is only raised (rescaling l and O) when
-// a score would exceed it by more than 2^8.  Any reference gives the same O / l;
-// bounding p by 2^8 keeps the sums far from overflow, and the common step needs
-// no cross-lane max.  exp2 is the hardware instruction (results below 2^-126
-// flush to zero, far under the bf16 resolution of P).
-template <int DH, bool CAUSAL>
-__device__ __forceinline__ void attn_step(AttnState<DH>& st, const bf16_t* Kl, int kld,
-                                          const bf16_t* Vl, int vld, int col0, int k0, int qt,
-                                          int lane) {
+// One segment of up to 128 keys of K (LDS [key][kld], head dims at col0) and V^T
+// (LDS [dim][vld]) for the wave's two query tiles qa and qb, which see NPA and NPB
+// pairs of 32 keys: S^T for the whole segment first, one row max and one rescale
+// of l and O per segment, then P and O^T += V^T P^T per pair.  The pair counts are
+// template parameters, so both tiles' work is one branch-free block the scheduler
+// can interleave.  S^T tile 2 kp + t holds keys 32 kp + 16 t + 4 gq + i; the P^T
+// fragment of pair kp takes them in that order (keys 4gq.., then 16 + 4gq..) and
+// V^T is read to match.  DIAG masks keys above the lane's query row (only the
+// last pair of a tile reaches past its first query).  exp2 is the hardware
+// instruction (results below 2^-126 flush to zero, far under the bf16
+// resolution of P).
+template <int DH, bool DIAG, int NP>
+__device__ __forceinline__ void seg_scores(f32x4v (&s)[8], const AttnState<DH>& st,
+                                           const bf16_t* Kl, int kld, int col0, int qt, int lane) {
   const int gq = lane / 16, c16 = lane % 16;
-  constexpr float sc = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
-  constexpr float HEADROOM = 8.f;
-  f32x4v s[2];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    s[t] = f32x4v{0.f, 0.f, 0.f, 0.f};
+  for (int kp = 0; kp < NP; ++kp)
 #pragma unroll
-    for (int kb = 0; kb < DH / 32; ++kb)
-      s[t] = mfma16(lfrag(Kl + (k0 + 16 * t + c16) * kld + col0 + 32 * kb + 8 * gq), st.qf[kb], s[t]);
-  }
-  bf16x8 vf[DH / 16];
+    for (int t = 0; t < 2; ++t) {
+      f32x4v acc = f32x4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) {
-    const bf16_t* vr = Vl + (col0 + 16 * dt + c16) * vld + k0 + 4 * gq;
-    vf[dt] = as_bf16x8(*reinterpret_cast<const uint2*>(vr), *reinterpret_cast<const uint2*>(vr + 16));
-  }
-  if (CAUSAL && k0 + 32 > 16 * qt) {   // wave-uniform
+      for (int kb = 0; kb < DH / 32; ++kb)
+        acc = mfma16(lfrag(Kl + (32 * kp + 16 * t + c16) * kld + col0 + 32 * kb + 8 * gq),
+                     st.qf[kb], acc);
+      s[2 * kp + t] = acc;
+    }
+  if (DIAG) {
     const int qrow = 16 * qt + c16;
+    constexpr int kp = NP - 1;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (k0 + 16 * t + 4 * gq + i > qrow) s[t][i] = -__builtin_inff();
+        if (32 * kp + 16 * t + 4 * gq + i > qrow) s[2 * kp + t][i] = -__builtin_inff();
   }
-  const float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-  if (__builtin_amdgcn_ballot_w64(mx * sc > st.m + HEADROOM) != 0) {   // wave-uniform
-    const float mnew = fmaxf(st.m, xmax32(xmax16(mx)) * sc);
-    const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
-    st.l *= alpha;
+}
+template <int DH, int NP>
+__device__ __forceinline__ float seg_rescale(AttnState<DH>& st, const f32x4v (&s)[8]) {
+  constexpr float sc = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
+  float mx = -__builtin_inff();
 #pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] *= alpha;
-    st.m = mnew;
-  }
-  bf16x8 pb;
+  for (int q = 0; q < 2 * NP; ++q)
+    mx = fmaxf(mx, fmaxf(fmaxf(s[q][0], s[q][1]), fmaxf(s[q][2], s[q][3])));
+  mx = xmax32(xmax16(mx));
+  const float mnew = fmaxf(st.m, mx * sc);   // finite: every segment has a visible key
+  const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
+  st.m = mnew;
+  st.l *= alpha;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] *= alpha;
+  return mnew;
+}
+template <int DH, int NP>
+__device__ __forceinline__ void seg_pv(AttnState<DH>& st, const f32x4v (&s)[8], float mnew,
+                                       const bf16_t* Vl, int vld, int col0, int lane) {
+  const int gq = lane / 16, c16 = lane % 16;
+  constexpr float sc = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
   float psum = 0.f;
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int kp = 0; kp < NP; ++kp) {
+    bf16x8 pb;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float p = __builtin_amdgcn_exp2f(fmaf(s[t][i], sc, -st.m));
-      psum += p;
-      pb[4 * t + i] = static_cast<__bf16>(p);
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float pv = __builtin_amdgcn_exp2f(fmaf(s[2 * kp + t][i], sc, -mnew));
+        psum += pv;
+        pb[4 * t + i] = static_cast<__bf16>(pv);
+      }
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt) {
+      const bf16_t* vr = Vl + (col0 + 16 * dt + c16) * vld + 32 * kp + 4 * gq;
+      const bf16x8 vf = as_bf16x8(*reinterpret_cast<const uint2*>(vr),
+                                  *reinterpret_cast<const uint2*>(vr + 16));
+      st.o[dt] = mfma16(vf, pb, st.o[dt]);
     }
+  }
   st.l += psum;
-#pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = mfma16(vf[dt], pb, st.o[dt]);
+}
+template <int DH, bool DIAG, int NPA, int NPB>
+__device__ __forceinline__ void attn_segment2(AttnState<DH>& sa, AttnState<DH>& sb,
+                                              const bf16_t* Kl, int kld, const bf16_t* Vl,
+                                              int vld, int col0, int qa, int qb, int lane) {
+  f32x4v s_a[8], s_b[8];
+  seg_scores<DH, DIAG, NPA>(s_a, sa, Kl, kld, col0, qa, lane);
+  seg_scores<DH, DIAG, NPB>(s_b, sb, Kl, kld, col0, qb, lane);
+  const float ma = seg_rescale<DH, NPA>(sa, s_a);
+  const float mb = seg_rescale<DH, NPB>(sb, s_b);
+  seg_pv<DH, NPA>(sa, s_a, ma, Vl, vld, col0, lane);
+  seg_pv<DH, NPB>(sb, s_b, mb, Vl, vld, col0, lane);
+}
+// The block's own keys for wave W: tiles W and 7 - W see W / 2 + 1 and
+// (7 - W) / 2 + 1 pairs.
+template <int DH, int W>
+__device__ __forceinline__ void attn_own(AttnState<DH>& sa, AttnState<DH>& sb, const bf16_t* Ks,
+                                         const bf16_t* Vts, int col0, int lane) {
+  attn_segment2<DH, true, W / 2 + 1, (7 - W) / 2 + 1>(sa, sb, Ks, QLD, Vts, VLD, col0, W, 7 - W,
+                                                      lane);
 }
 
 // O = O^T / l into the tile's rows of Qs (the tile's Q is already in registers).
@@ -664,18 +699,19 @@ __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf
     attn_init<DH>(sb, Qs, hd * DH, qb);
     CacheChunk ch;
     if (p0 > 0) cache_load(ch, kc, vc, tpad, g, 0);
-    const int na = 16 * qa + 16, nb = 16 * qb + 16;
-    for (int k0 = 0; k0 < nb; k0 += 32) {
-      if (k0 < na) attn_step<DH, true>(sa, Ks, QLD, Vts, VLD, hd * DH, k0, qa, lane);
-      attn_step<DH, true>(sb, Ks, QLD, Vts, VLD, hd * DH, k0, qb, lane);
-    }
+    // the block's own keys (one specialisation per wave: its pair counts)
+    if (w == 0)
+      attn_own<DH, 0>(sa, sb, Ks, Vts, hd * DH, lane);
+    else if (w == 1)
+      attn_own<DH, 1>(sa, sb, Ks, Vts, hd * DH, lane);
+    else if (w == 2)
+      attn_own<DH, 2>(sa, sb, Ks, Vts, hd * DH, lane);
+    else
+      attn_own<DH, 3>(sa, sb, Ks, Vts, hd * DH, lane);
     for (int c0 = 0; c0 < p0; c0 += BT) {     // earlier blocks: every key visible
       if (c0 > 0) cache_load(ch, kc, vc, tpad, g, c0);
       cache_put(ch, Kc, Vc);
-      for (int k0 = 0; k0 < BT; k0 += 32) {
-        attn_step<DH, false>(sa, Kc, QLD, Vc, VLD, hd * DH, k0, qa, lane);
-        attn_step<DH, false>(sb, Kc, QLD, Vc, VLD, hd * DH, k0, qb, lane);
-      }
+      attn_segment2<DH, false, 4, 4>(sa, sb, Kc, QLD, Vc, VLD, hd * DH, qa, qb, lane);
       __syncthreads();
     }
     attn_finish<DH>(sa, Qs, hd * DH, qa);
@@ -778,7 +814,8 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
 // ---------------------------------------------------------------- sublayers
 // Q / K / V of head group g: wave w computes token tiles 2(w & 1), 2(w & 1) + 1 of
 // column tiles 3 CS .. +2 of [q0 q1 k0 k1 v0 v1] (CS = w >> 1); Q and K
-// transposed ([dim][token]), V untransposed.  Prefetches `nxt` at its end.  The
+// transposed ([dim][token]), V untransposed.  Leaves the look-ahead empty (the
+// output projection primes its own after the attention).  The
 // column split is a template parameter so that each wave runs a branch-free
 // loop with fixed accumulator registers.
 template <int CS>
@@ -836,7 +873,7 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
         qa[t][1] = mfma32(xq[j][1], a, qa[t][1]);
       }
     }
-    stream_fetch<NKB, 3, 4>(wq, pre, cur, nxt, j, lane);
+    stream_fetch<NKB, 3, 0>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
@@ -959,6 +996,9 @@ __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_lay
       attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
     else
       attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
+    // the output projection's look-ahead starts here rather than across the
+    // attention, whose own registers it would otherwise crowd
+    seg_prime<4>(pre, so, otid() % WAVE);
     __syncthreads();
     // the cache stores follow the phase's weight loads, so the next phase's first
     // wait on its weights does not also wait for the stores
