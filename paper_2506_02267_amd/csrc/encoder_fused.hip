@@ -904,21 +904,38 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
 }
 
 // FFN first layer, chunk c: H^T = ReLU(W_1[chunk] Xs^T + b_1) into Hs (wave w:
-// hidden tiles 2(w & 1) + {0,1}, token tiles 2(w >> 1) + {0,1}).
-__device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
-                                           const float* b_1, int c, const bf16_t* Xs, bf16_t* Hs) {
+// hidden tiles 2(w & 1) + {0,1}, token tiles 2(w >> 1) + {0,1}).  The
+// accumulators start at the chunk's biases bh (loaded by the caller ahead of
+// time); ReLU acts on the packed bf16 pairs (for bf16 bit patterns the signed
+// 16-bit max with zero is exactly ReLU, and rounding commutes with it).
+__device__ __forceinline__ void b1_load(float4 (&bh)[2][4], const float* b_1, int c) {
   FZ_LANE_VARS
-  constexpr int NKB = DM / 16;
-  const int hp = w & 1, tp = w >> 1;
-  float4 bh[2][4];   // epilogue biases, loaded before the next phase's weight loads
+  const int hp = w & 1;
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       bh[t][j] = *reinterpret_cast<const float4*>(b_1 + c * FC + (2 * hp + t) * 32 + 8 * j + 4 * hf);
+}
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t relu2(uint32_t x) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, x), s16x2{0, 0}));
+}
+__device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
+                                           const float4 (&bh)[2][4], const bf16_t* Xs,
+                                           bf16_t* Hs) {
+  FZ_LANE_VARS
+  constexpr int NKB = DM / 16;
+  const int hp = w & 1, tp = w >> 1;
   f32x16 ha[2][2];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) ha[t][0] = ha[t][1] = f32x16{};
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float bb[4] = {bh[t][j].x, bh[t][j].y, bh[t][j].z, bh[t][j].w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) ha[t][0][4 * j + i] = ha[t][1][4 * j + i] = bb[i];
+    }
   bf16x8 wq[NKB][2];
   bf16x8 xq[NKB][2];
   const bf16_t* arow = Xs + (tp * 64 + l32) * XLD + 8 * hf;
@@ -946,10 +963,9 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int hid = (2 * hp + t) * 32 + 8 * j + 4 * hf;
-        const float4 bv = bh[t][j];
-        st4(Hs + ((2 * tp + u) * 32 + l32) * HLD + hid, fmaxf(ha[t][u][4 * j] + bv.x, 0.f),
-            fmaxf(ha[t][u][4 * j + 1] + bv.y, 0.f), fmaxf(ha[t][u][4 * j + 2] + bv.z, 0.f),
-            fmaxf(ha[t][u][4 * j + 3] + bv.w, 0.f));
+        *reinterpret_cast<uint2*>(Hs + ((2 * tp + u) * 32 + l32) * HLD + hid) =
+            make_uint2(relu2(pack2(ha[t][u][4 * j], ha[t][u][4 * j + 1])),
+                       relu2(pack2(ha[t][u][4 * j + 2], ha[t][u][4 * j + 3])));
       }
 }
 
@@ -1026,10 +1042,14 @@ __device__ __forceinline__ void ffn_sublayer(const Args& A, const tav2_layer& L,
   const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
   const int ffn = A.ffn;
   const int nch = ffn / FC;
+  float4 bh[2][4];   // the next chunk's first-layer biases
+  b1_load(bh, L.b_1, 0);
   for (int c = 0; c < nch; ++c) {
     const WSeg s2 = seg_resid(pk.w2, ffn / 16, c * (FC / 16), w);
-    ffn1_phase(pre, seg_ffn1(pk.w1, c, w), s2, L.b_1, c, Xs, Hs);
+    ffn1_phase(pre, seg_ffn1(pk.w1, c, w), s2, bh, Xs, Hs);
     __syncthreads();
+    // loaded before the second layer's weight loads, consumed by the next chunk
+    if (c + 1 < nch) b1_load(bh, L.b_1, c + 1);
     if (c + 1 < nch) {
       resid_phase<FC / 16, 2>(acc, pre, s2, seg_ffn1(pk.w1, c + 1, w), Hs, HLD);
     } else {   // the LayerNorm parameters go past the hidden chunk
