@@ -117,13 +117,37 @@ __global__ __launch_bounds__(256) void score_f32_kernel(
 // ---------------------------------------------------------------- top-k
 constexpr int TK_THREADS = 512;
 
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v, int lane) {
+// Exclusive prefix (in thread order) and block total of NV 64-bit values per
+// thread; sw holds NV per wave.  Ends with a barrier.
+template <int NV>
+__device__ __forceinline__ void block_excl_scan(const uint64_t (&v)[NV], uint64_t (&excl)[NV],
+                                                uint64_t (&total)[NV], uint64_t* sw, int lane,
+                                                int wid) {
+  uint64_t incl[NV];
 #pragma unroll
-  for (int o = 1; o < WAVE; o <<= 1) {
-    uint32_t t = __shfl_up(v, o, WAVE);
-    if (lane >= o) v += t;
+  for (int q = 0; q < NV; ++q) {
+    uint64_t x = v[q];
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) {
+      const uint64_t t = __shfl_up(x, o, WAVE);
+      if (lane >= o) x += t;
+    }
+    incl[q] = x;
+    if (lane == WAVE - 1) sw[wid * NV + q] = x;
   }
-  return v;
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < NV; ++q) {
+    uint64_t pre = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < TK_THREADS / WAVE; ++w) {
+      const uint64_t t = sw[w * NV + q];
+      pre += w < wid ? t : 0;
+      all += t;
+    }
+    excl[q] = pre + incl[q] - v[q];
+    total[q] = all;
+  }
 }
 
 template <int PT>
@@ -132,7 +156,7 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     const int32_t* __restrict__ seq_len, int max_len, int k, int32_t* __restrict__ out_idx,
     float* __restrict__ out_score) {
   __shared__ int red[2][TK_THREADS / WAVE];
-  __shared__ uint32_t wtot[TK_THREADS / WAVE];
+  __shared__ uint64_t scan_w[(TK_THREADS / WAVE) * 5];
   __shared__ uint64_t sel[TAV2_K_MAX];
 
   const int r = blockIdx.y;
@@ -149,21 +173,25 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
   }
   if (kk == 0) return;
 
-  // this thread's rows: [base, base + PT), key 0 (below every score) past L
+  // this thread's rows: chunk c (0 .. PT / 4 - 1) holds rows CH c + 4 tid + u, so
+  // that every load instruction reads 1 KB of consecutive scores per wave; rows
+  // past L get key 0 (below every score)
+  constexpr int NC = PT / 4;
+  constexpr int CH = TK_THREADS * 4;
   const float* srow = scores + n * ld;
-  const int base = tid * PT;
-  uint32_t key[PT];
+  uint32_t key[PT];   // key[4 c + u]: row CH c + 4 tid + u
 #pragma unroll
-  for (int j = 0; j < PT; j += 4) {
-    if (base + j + 4 <= L) {
-      float4 v = *reinterpret_cast<const float4*>(srow + base + j);
-      key[j] = score_key(v.x);
-      key[j + 1] = score_key(v.y);
-      key[j + 2] = score_key(v.z);
-      key[j + 3] = score_key(v.w);
+  for (int c = 0; c < NC; ++c) {
+    const int r0 = c * CH + tid * 4;
+    if (r0 + 4 <= L) {
+      const float4 v = *reinterpret_cast<const float4*>(srow + r0);
+      key[4 * c] = score_key(v.x);
+      key[4 * c + 1] = score_key(v.y);
+      key[4 * c + 2] = score_key(v.z);
+      key[4 * c + 3] = score_key(v.w);
     } else {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) key[j + u] = (base + j + u < L) ? score_key(srow[base + j + u]) : 0u;
+      for (int u = 0; u < 4; ++u) key[4 * c + u] = (r0 + u < L) ? score_key(srow[r0 + u]) : 0u;
     }
   }
 
@@ -171,10 +199,10 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
   uint32_t thr = 0;
   for (int b = 31; b >= 0; --b) {
     const uint32_t probe = thr | (1u << b);
+    // wave-level count: one compare per key, the lane mask counted on the scalar unit
     int cnt = 0;
 #pragma unroll
-    for (int j = 0; j < PT; ++j) cnt += key[j] >= probe ? 1 : 0;
-    cnt = wave_sum_i(cnt);
+    for (int j = 0; j < PT; ++j) cnt += __popcll(__builtin_amdgcn_ballot_w64(key[j] >= probe));
     if (lane == 0) red[b & 1][wid] = cnt;
     __syncthreads();
     int tot = 0;
@@ -183,35 +211,43 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     if (tot >= kk) thr = probe;
   }
 
-  // ordered compaction: keys above thr anywhere, then the lowest rows equal to thr
-  uint32_t gt = 0, eq = 0;
+  // compaction: keys above thr anywhere in sel[0, count_gt) (the rank sort orders
+  // them), then the need_eq lowest rows whose key equals thr.  Rows are ordered by
+  // (chunk, thread, u), so the equal keys are counted per chunk: 16-bit fields,
+  // four chunks per 64-bit word, summed in one block scan with the above count.
+  constexpr int NW = (NC + 3) / 4;
+  uint64_t word[NW + 1];   // word[0]: keys above thr; word[1 + c / 4]: equal keys of chunk c
 #pragma unroll
-  for (int j = 0; j < PT; ++j) {
-    gt += key[j] > thr ? 1u : 0u;
-    eq += key[j] == thr ? 1u : 0u;
-  }
-  const uint32_t mine = (gt << 16) | eq;
-  const uint32_t incl = wave_incl_scan(mine, lane);
-  if (lane == WAVE - 1) wtot[wid] = incl;
-  __syncthreads();
-  uint32_t pre = 0, all = 0;
+  for (int q = 0; q <= NW; ++q) word[q] = 0;
 #pragma unroll
-  for (int w = 0; w < TK_THREADS / WAVE; ++w) {
-    pre += w < wid ? wtot[w] : 0u;
-    all += wtot[w];
-  }
-  const uint32_t excl = pre + incl - mine;
-  const int count_gt = int(all >> 16);
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      word[0] += key[4 * c + u] > thr ? 1u : 0u;
+      word[1 + c / 4] += key[4 * c + u] == thr ? (uint64_t(1) << (16 * (c % 4))) : 0u;
+    }
+  uint64_t excl[NW + 1], total[NW + 1];
+  block_excl_scan<NW + 1>(word, excl, total, scan_w, lane, wid);
+  const int count_gt = int(total[0]);
   const int need_eq = kk - count_gt;
-  int gpos = int(excl >> 16), epos = int(excl & 0xFFFFu);
+  int gpos = int(excl[0]);
+  int eq_before = 0;   // equal keys in chunks before c, over all threads
 #pragma unroll
-  for (int j = 0; j < PT; ++j) {
-    const uint64_t packed = (uint64_t(key[j]) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(base + j));
-    if (key[j] > thr) {
-      sel[gpos++] = packed;
-    } else if (key[j] == thr) {
-      if (epos < need_eq) sel[count_gt + epos] = packed;
-      ++epos;
+  for (int c = 0; c < NC; ++c) {
+    const int sh = 16 * (c % 4);
+    int e = eq_before + int((excl[1 + c / 4] >> sh) & 0xFFFFu);
+    eq_before += int((total[1 + c / 4] >> sh) & 0xFFFFu);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t kv = key[4 * c + u];
+      const uint32_t row = uint32_t(c * CH + tid * 4 + u);
+      const uint64_t packed = (uint64_t(kv) << 32) | uint64_t(0xFFFFFFFFu - row);
+      if (kv > thr) {
+        sel[gpos++] = packed;
+      } else if (kv == thr) {
+        if (e < need_eq) sel[count_gt + e] = packed;
+        ++e;
+      }
     }
   }
   __syncthreads();
@@ -220,7 +256,14 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
   for (int s = tid; s < kk; s += TK_THREADS) {
     const uint64_t me = sel[s];
     int rank = 0;
-    for (int t = 0; t < kk; ++t) rank += sel[t] > me ? 1 : 0;
+    // 8 independent LDS reads per iteration (the survivor count is not a
+    // multiple of 8 in general: the tail is handled one by one)
+    int t = 0;
+    for (; t + 8 <= kk; t += 8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) rank += sel[t + u] > me ? 1 : 0;
+    }
+    for (; t < kk; ++t) rank += sel[t] > me ? 1 : 0;
     oi[rank] = int32_t(0xFFFFFFFFu - uint32_t(me));
     os[rank] = key_score(uint32_t(me >> 32));
   }
