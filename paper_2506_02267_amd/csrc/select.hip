@@ -18,57 +18,71 @@
 namespace tav2 {
 
 // ---------------------------------------------------------------- scores, bf16
-// Block: 4 waves, 64 candidates x 256 rows; wave w covers rows [64w, 64w + 64).
-// Candidates are the MFMA rows (A), sequence rows the MFMA columns (B), so each
-// D register holds one candidate and 32 consecutive lanes 32 consecutive rows.
-constexpr int SC_CANDS = 64;
+// Block: 4 waves, 128 candidates x 256 rows; wave w covers rows [64w, 64w + 64)
+// of all 128 candidates.  Candidates are the MFMA rows (A) and come from LDS (the
+// block's 128 x d tile, loaded once), sequence rows the MFMA columns (B) and come
+// straight from global memory (each wave its own rows), so each D register holds
+// one candidate and 32 consecutive lanes 32 consecutive rows.  The tile sizes keep
+// the re-reads of both operands small next to the score rows written.
+constexpr int SC_CANDS = 128;
 constexpr int SC_ROWS = 256;
+constexpr int SC_PAD = 8;   // LDS row padding (bf16) of the candidate tile
 
 __global__ __launch_bounds__(256) void score_bf16_kernel(
     const bf16_t* __restrict__ emb, const int64_t* __restrict__ seq_off,
     const int32_t* __restrict__ seq_len, const bf16_t* __restrict__ cand,
     const int64_t* __restrict__ cand_off, int d, int max_len, float* __restrict__ scores,
     int64_t ld) {
+  extern __shared__ __attribute__((aligned(16))) bf16_t ctile[];   // [SC_CANDS][d + SC_PAD]
   const int r = blockIdx.z;
   const int64_t c_begin = cand_off[r], c_end = cand_off[r + 1];
   const int64_t n0 = c_begin + int64_t(blockIdx.y) * SC_CANDS;
   if (n0 >= c_end) return;
   const int L = min(seq_len[r], max_len);
+  if (int(blockIdx.x) * SC_ROWS >= L) return;
+  const int cld = d + SC_PAD;
+  // candidate tile into LDS (rows past the request's candidates: its last one)
+  for (int e = threadIdx.x; e < SC_CANDS * (d / 8); e += 256) {
+    const int row = e / (d / 8), c = e % (d / 8);
+    int64_t n = n0 + row;
+    n = n < c_end ? n : c_end - 1;
+    *reinterpret_cast<uint4*>(ctile + row * cld + c * 8) =
+        *reinterpret_cast<const uint4*>(cand + n * d + c * 8);
+  }
+  __syncthreads();
   const int row0 = blockIdx.x * SC_ROWS + (threadIdx.x / WAVE) * 64;
   if (row0 >= L) return;
   const int lane = threadIdx.x % WAVE;
   const int h = lane / 32, l32 = lane % 32;
   const bf16_t* seq = emb + seq_off[r] * int64_t(d);
-
-  // clamp out-of-range candidates / rows to a valid one; their results are not stored
-  const bf16_t* arow[2];
   const bf16_t* brow[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    int64_t n = n0 + t * 32 + l32;
-    n = n < c_end ? n : c_end - 1;
-    arow[t] = cand + n * d + 8 * h;
     int i = row0 + t * 32 + l32;
-    i = i < L ? i : L - 1;
+    i = i < L ? i : L - 1;   // clamped; not stored
     brow[t] = seq + int64_t(i) * d + 8 * h;
   }
-  f32x16 acc[2][2];
+  const bf16_t* arow = ctile + l32 * cld + 8 * h;
+  f32x16 acc[4][2];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
-
-  for (int k0 = 0; k0 < d; k0 += 16) {
-    bf16x8 av[2], bv[2];
+  bf16x8 bv[2], bn[2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      av[t] = as_bf16x8(*reinterpret_cast<const uint4*>(arow[t] + k0));
-      bv[t] = as_bf16x8(*reinterpret_cast<const uint4*>(brow[t] + k0));
+  for (int t = 0; t < 2; ++t) bv[t] = as_bf16x8(*reinterpret_cast<const uint4*>(brow[t]));
+  for (int k0 = 0; k0 < d; k0 += 16) {
+    const int kn = k0 + 16 < d ? k0 + 16 : k0;   // next k-block (the last one reloads itself)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) bn[t] = as_bf16x8(*reinterpret_cast<const uint4*>(brow[t] + kn));
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const bf16x8 av = as_bf16x8(*reinterpret_cast<const uint4*>(arow + a * 32 * cld + k0));
+#pragma unroll
+      for (int b = 0; b < 2; ++b) acc[a][b] = mfma32(av, bv[b], acc[a][b]);
     }
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < 2; ++b) acc[a][b] = mfma32(av[a], bv[b], acc[a][b]);
+    for (int t = 0; t < 2; ++t) bv[t] = bn[t];
   }
 
 #pragma unroll
@@ -76,7 +90,7 @@ __global__ __launch_bounds__(256) void score_bf16_kernel(
     const int i = row0 + b * 32 + l32;
     if (i >= L) continue;
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
+    for (int a = 0; a < 4; ++a) {
 #pragma unroll
       for (int reg = 0; reg < 16; ++reg) {
         const int64_t n = n0 + a * 32 + 8 * (reg / 4) + 4 * h + (reg % 4);
@@ -277,7 +291,11 @@ hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores
     dim3 grid(unsigned(cdiv(seq.max_len, SC_ROWS)), unsigned(cdiv(c.max_count, SC_CANDS)),
               unsigned(seq.num_requests));
     ProfScope prof("score_bf16", st);
-    score_bf16_kernel<<<grid, 256, 0, st>>>(
+    const size_t lds = size_t(SC_CANDS) * size_t(seq.d + SC_PAD) * 2;   // d <= 512: <= 133 KB
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(score_bf16_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+    score_bf16_kernel<<<grid, 256, lds, st>>>(
         static_cast<const bf16_t*>(seq.emb), seq.offset, seq.len,
         static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
   } else {
