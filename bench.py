@@ -69,6 +69,36 @@ def site_work(w, total, valid_tokens, max_len, launches_per_step):
     return out
 
 
+TRAFFIC_FILES = {"encoder_fused": "encoder_fused_{workload}_traffic.md"}
+KERNEL_SOURCES = {"encoder_fused": "paper_2506_02267_amd/csrc/encoder_fused.hip"}
+
+
+def measured_traffic(site, workload):
+    """HBM bytes per launch of `site` from the committed counter summary, or None.
+
+    The summary (profiles/) records FETCH_SIZE + WRITE_SIZE per dispatch scaled by
+    a plain copy of known size, and the SHA-256 of the kernel source it was taken
+    on; a different source (the kernel changed since) gives None.
+    """
+    import hashlib
+    name = TRAFFIC_FILES.get(site)
+    if name is None:
+        return None
+    path = os.path.join(ROOT, "profiles", name.format(workload=workload))
+    src = os.path.join(ROOT, KERNEL_SOURCES[site])
+    if not (os.path.exists(path) and os.path.exists(src)):
+        return None
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    fields = {}
+    for line in open(path):
+        if line.startswith("<!-- ") and ":" in line:
+            key, val = line[5:].split("-->")[0].split(":", 1)
+            fields[key.strip()] = val.strip()
+    if fields.get("kernel_sha256") != sha or "hbm_bytes_per_launch" not in fields:
+        return None
+    return float(fields["hbm_bytes_per_launch"])
+
+
 def cpu_baseline(inp, W, k, budget_s):
     """The oracle, untuned, on a bounded sample of the same workload."""
     import oracle
@@ -110,6 +140,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle encoder work in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed region, copy 256 MiB device to device three times "
+                         "(a plain copy of known size for scaling memory counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the path runs on one MI355X and this build has no "
@@ -169,6 +202,14 @@ def main():
     ms_per_step = ms / args.steps
     value = total * args.steps / (ms / 1000.0)
 
+    if args.copy_calibration:
+        src = torch.empty(64 << 20, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1.0)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
     work = site_work(w, total, valid_tokens, int(lengths.max()), launches)
     cnt, dom_ms = dom.get(dominant, (0, 0.0))
     avg_s = dom_ms / max(cnt, 1) / 1000.0
@@ -183,6 +224,7 @@ def main():
         achieved = amount / avg_s / 1e9 if avg_s > 0 else 0.0
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
+    roof["traffic"] = measured_traffic(dominant, w.name)
     roof["kernel"] = dominant
     roof["avg_launch_us"] = round(avg_s * 1e6, 2)
     roof["work_per_launch"] = amount

@@ -14,19 +14,27 @@
 //    128 (w & 1) .. +127 of tokens 64 (w >> 1) .. +63.  LayerNorm over features is
 //    an in-lane sum, one cross-half exchange and a 2-way exchange through LDS.
 //  * Weights stream from L2 straight into registers: each call first packs every
-//    matrix into MFMA-fragment order (one 32 x 16 fragment = 1 KB contiguous,
-//    lane-major), so every fragment load is one coalesced 16-byte-per-lane load
-//    and no weight tile passes through LDS or a barrier.
+//    matrix (and the side tables, transposed) into MFMA-fragment order (one
+//    32 x 16 fragment = 1 KB contiguous, lane-major), so every fragment load is one
+//    buffer load of 16 bytes per lane with the fragment offset in a scalar
+//    register, and no weight tile passes through LDS or a barrier.  Each phase
+//    keeps a fixed look-ahead of 16 fragments in flight and, in its last
+//    iterations, starts the next phase's.
 //  * LDS holds only activations: the bf16 copy of the block (MFMA operand), the
 //    head group's Q / K / V^T, the attention output, the FFN hidden chunk, and
 //    cached keys/values of earlier blocks during attention.  Every activation
 //    write is 4 consecutive bf16 of one row: products whose consumer needs
 //    [token][feature] are computed transposed (weights as MFMA A operand); V is
 //    computed untransposed to give V^T [dim][token].
-//  * Attention: 32x32x16 MFMAs, wave w owns queries 32w .. 32w+31 of the block;
-//    S^T = K Q^T puts one query per lane, so the softmax reductions are in-lane
-//    plus one exchange between lane halves, and P^T feeds O^T = V^T P^T straight
-//    from its accumulator registers with the matching key order.
+//  * Attention: 16x16x32 MFMAs; wave w owns query tiles w and 7 - w (16 queries
+//    each, equal causal work for every wave).  S^T = K Q^T puts one query per lane
+//    column, so softmax reductions are in-lane plus two lane-half exchanges, and
+//    P^T feeds O^T = V^T P^T straight from the score registers with the matching
+//    key order.  Keys are taken 128 at a time (one softmax max and rescale per
+//    segment); the block's own keys come first, then earlier blocks' from the cache.
+//  * Global loads complete in issue order, so loads whose data is needed soon are
+//    issued before the weight look-ahead of the next phase (biases, LayerNorm
+//    parameters, table rows), and stores of the K/V cache after it.
 #include "common.h"
 #include "internal.h"
 #include "token_source.h"

@@ -292,9 +292,16 @@ hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores
               unsigned(seq.num_requests));
     ProfScope prof("score_bf16", st);
     const size_t lds = size_t(SC_CANDS) * size_t(seq.d + SC_PAD) * 2;   // d <= 512: <= 133 KB
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(score_bf16_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    static size_t lds_set[64] = {};   // per device: largest dynamic LDS allowed so far
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64 || lds_set[dev] < lds) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(score_bf16_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+      if (e != hipSuccess) return e;
+      if (dev >= 0 && dev < 64) lds_set[dev] = lds;
+    }
     score_bf16_kernel<<<grid, 256, lds, st>>>(
         static_cast<const bf16_t*>(seq.emb), seq.offset, seq.len,
         static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
