@@ -1162,8 +1162,9 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
 // ---------------------------------------------------------------- candidate half
 // cvec[i] = c W_in[:, d:]^T + b_in for candidates c0 + i (the candidate's part of
 // the Eq. 4 input projection, the same for every position of the candidate);
-// CB candidates per workgroup, thread f computes output feature f.
-constexpr int CB = 16;
+// CB candidates per workgroup (enough workgroups to cover the chip), thread f
+// computes output feature f.
+constexpr int CB = 4;
 __global__ __launch_bounds__(DM) void cand_proj_kernel(const bf16_t* __restrict__ cand,
                                                        const bf16_t* __restrict__ W_in,
                                                        const float* __restrict__ b_in, int d,
@@ -1182,6 +1183,7 @@ __global__ __launch_bounds__(DM) void cand_proj_kernel(const bf16_t* __restrict_
 #pragma unroll
   for (int r = 0; r < CB; ++r) acc[r] = b_in[f];
   const bf16_t* wr = W_in + int64_t(f) * 2 * d + d;
+#pragma unroll 4
   for (int j = 0; j < d; j += 8) {
     const uint4 wv = *reinterpret_cast<const uint4*>(wr + j);
     const bf16_t* wp = reinterpret_cast<const bf16_t*>(&wv);
