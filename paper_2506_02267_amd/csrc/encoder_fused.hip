@@ -10,9 +10,10 @@
 //  * 4 waves, one per SIMD, each with the full 512-register budget.  The fp32
 //    residual stream of the block lives in registers as the transposed product
 //    X^T [feature x token] (MFMA accumulator layout: one token per lane, 4
-//    consecutive features per register group); wave w owns features
-//    128 (w & 1) .. +127 of tokens 64 (w >> 1) .. +63.  LayerNorm over features is
-//    an in-lane sum, one cross-half exchange and a 2-way exchange through LDS.
+//    consecutive features per register group); wave w owns features 64 w .. +63
+//    of all 128 tokens, so each weight fragment of these products is loaded by
+//    one wave only.  LayerNorm over features is an in-lane sum, one cross-half
+//    exchange and a 4-way exchange through LDS.
 //  * Weights stream from L2 straight into registers: each call first packs every
 //    matrix (and the side tables, transposed) into MFMA-fragment order (one
 //    32 x 16 fragment = 1 KB contiguous, lane-major), so every fragment load is one
@@ -39,12 +40,6 @@
 #include "internal.h"
 #include "token_source.h"
 
-#ifndef FZ_D2
-#define FZ_D2 8
-#define FZ_D3 5
-#define FZ_D4 4
-#endif
-
 namespace tav2 {
 namespace fz {
 
@@ -67,12 +62,11 @@ constexpr int QS_BYTES = BT * QLD * 2;                 // 18432
 constexpr int VS_BYTES = 64 * VLD * 2;                 // 17408
 constexpr int SC_BYTES = 2 * QS_BYTES + VS_BYTES;      // 54272
 constexpr int CS_BYTES = QS_BYTES + VS_BYTES;          // 35840: cached K / V^T chunk
-constexpr int PM_BYTES = DM * 4;                       // running pooled max
-constexpr int LDS_BYTES = XS_BYTES + SC_BYTES + CS_BYTES + PM_BYTES;
+constexpr int LDS_BYTES = XS_BYTES + SC_BYTES + CS_BYTES;
 static_assert(LDS_BYTES <= 163840, "fused encoder exceeds the 160 KiB of LDS");
 static_assert(BT * HLD * 2 <= SC_BYTES, "FFN chunk does not fit the scratch region");
 static_assert(BT * HLD * 2 + 3 * DM * 4 <= SC_BYTES, "LayerNorm 2 parameters do not fit");
-static_assert(BT * 4 * 4 <= QS_BYTES && 3 * DM * 4 <= CS_BYTES, "LayerNorm 1 buffers do not fit");
+static_assert(2 * BT * 4 * 4 <= QS_BYTES && 3 * DM * 4 <= CS_BYTES, "LayerNorm 1 buffers do not fit");
 static_assert(BT * 8 + BT * 8 <= SC_BYTES, "encoding buffers do not fit");
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -178,45 +172,65 @@ __device__ __forceinline__ bf16x8 wfrag(int frag, int lane) {
 // use, and its last iterations already load the head of the NEXT phase's stream
 // into `pre`, so the stream keeps running across phase boundaries (attention,
 // LayerNorm and block boundaries included).  The look-ahead is a fixed number of
-// fragments (NSLOT), i.e. NSLOT / nr k-blocks for a phase with nr row tiles,
+// fragments (NSLOT), i.e. NSLOT / NR k-blocks for a phase with NR row tiles,
 // which gives every phase about the same look-ahead in MFMA time.
 constexpr int NSLOT = 16;
 typedef bf16x8 Pre[NSLOT];
-// k-blocks of look-ahead for a phase with nr row tiles, and the slots it fills
-constexpr int depth(int nr) { return nr == 2 ? FZ_D2 : nr == 3 ? FZ_D3 : FZ_D4; }
-constexpr int used_slots(int nr) { return depth(nr) * nr; }   // nr = 0: no next phase
-static_assert(used_slots(2) <= NSLOT && used_slots(3) <= NSLOT && used_slots(4) <= NSLOT, "look-ahead");
+
+// Shape of a GEMM phase: NR weight fragments (row tiles) per k-block, NKB
+// k-blocks.  Its look-ahead covers its first D k-blocks (by default as many as
+// NSLOT fragments hold): slot i holds k-block i / NR, row tile i % NR, for i < U.
+// NR = 0 stands for "no next phase".
+constexpr int default_depth(int nr, int nkb) {
+  return nr == 0 ? 0 : (NSLOT / nr < nkb ? NSLOT / nr : nkb);
+}
+template <int NR_, int NKB_, int D_ = default_depth(NR_, NKB_)>
+struct Shape {
+  static constexpr int NR = NR_, NKB = NKB_, D = D_;
+  static constexpr int U = D * NR;
+  static_assert(U <= NSLOT && D <= NKB, "look-ahead");
+};
+using NoPhase = Shape<0, 0>;
+using ShEmb = Shape<2, KIN / 16>;       // token half of W_in
+using ShTab = Shape<2, AT_COLS / 16>;   // [E_act | E_time]
+using ShPos = Shape<2, BT / 16>;        // E_pos rows of the block's positions
+using ShQkv = Shape<3, DM / 16>;        // Q / K / V of one head group
+using ShWo = Shape<2, 64 / 16>;         // W_o columns of one head group
+using ShF1 = Shape<2, DM / 16>;         // W_1 rows of one hidden chunk
+// W_2 columns of one hidden chunk: half of it ahead, so that the L2 traffic of
+// the two FFN phases is the same (each loads half of its own weights and half of
+// the other's)
+using ShF2 = Shape<2, FC / 16, FC / 32>;
+using ShPool = Shape<2, DM / 16>;       // W_pool
 
 struct WSeg {                            // a phase's weight fragments (all wave-uniform)
   int P;                                 // first fragment of the packed matrix
   int nkb;                               // k-blocks per row of P
   int kb0;                               // first k-block of the phase
-  int r0, r1, r2, r3;                    // packed row tiles (the phase uses nr of them)
+  int r0, r1, r2, r3;                    // packed row tiles (the phase uses NR of them)
 };
 
 __device__ __forceinline__ int seg_rt(const WSeg& s, int f) {
   return f == 0 ? s.r0 : f == 1 ? s.r1 : f == 2 ? s.r2 : s.r3;
 }
-// slot i of the look-ahead of a segment with NR row tiles holds k-block i / NR,
-// row tile i % NR (slots past the last whole k-block stay unused)
-template <int NR>
+template <class Sh>
 __device__ __forceinline__ void seg_slot(Pre& pre, int i, const WSeg& s, int lane) {
-  if (i < used_slots(NR)) pre[i] = wfrag(s.P + seg_rt(s, i % NR) * s.nkb + s.kb0 + i / NR, lane);
+  if constexpr (Sh::NR > 0)
+    if (i < Sh::U) pre[i] = wfrag(s.P + seg_rt(s, i % Sh::NR) * s.nkb + s.kb0 + i / Sh::NR, lane);
 }
-template <int NR>
+template <class Sh>
 __device__ __forceinline__ void seg_prime(Pre& pre, const WSeg& s, int lane) {
 #pragma unroll
-  for (int i = 0; i < NSLOT; ++i) seg_slot<NR>(pre, i, s, lane);
+  for (int i = 0; i < NSLOT; ++i) seg_slot<Sh>(pre, i, s, lane);
 }
-// residual-shaped phase of wave w: row tiles 4 (w & 1) + 0..3
+// residual-shaped phase of wave w: row tiles 2w, 2w + 1 (features 64 w .. +63)
 __device__ __forceinline__ WSeg seg_resid(int P, int nkb, int kb0, int w) {
-  const int r = 4 * (w & 1);
-  return WSeg{P, nkb, kb0, r, r + 1, r + 2, r + 3};
+  return WSeg{P, nkb, kb0, 2 * w, 2 * w + 1, 0, 0};
 }
 // FFN first layer, chunk c: hidden row tiles 4c + 2(w & 1) + 0..1
 __device__ __forceinline__ WSeg seg_ffn1(int P, int c, int w) {
-  const int r = c * (128 / 32) + 2 * (w & 1);
-  return WSeg{P, 256 / 16, 0, r, r + 1, 0, 0};
+  const int r = c * (FC / 32) + 2 * (w & 1);
+  return WSeg{P, DM / 16, 0, r, r + 1, 0, 0};
 }
 // Q / K / V of head group g: column tiles 3(w >> 1) + 0..2 of [q0 q1 k0 k1 v0 v1]
 // are packed row tiles 8 part + 2g + dt
@@ -227,73 +241,72 @@ __device__ __forceinline__ WSeg seg_qkv(int P, int g, int w) {
     const int ct = 3 * (w >> 1) + t;
     r[t] = 8 * (ct >> 1) + 2 * g + (ct & 1);
   }
-  return WSeg{P, 256 / 16, 0, r[0], r[1], r[2], 0};
+  return WSeg{P, DM / 16, 0, r[0], r[1], r[2], 0};
 }
 
-// Whether refilling the look-ahead (slots of a next phase with NRN row tiles)
-// during the last iterations of an NKB-block phase with NR row tiles never
-// overwrites a slot before this phase has read it.
-constexpr bool stream_ok(int NKB, int NR, int NRN) {
-  const int D = depth(NR), NU = used_slots(NRN);
-  if (NKB < D) return false;
-  for (int q = 0; q < D; ++q)
-    for (int i = NU * q / D; i < NU * (q + 1) / D; ++i)
-      if (i < used_slots(NR) && q + NKB - D < i / NR) return false;
-  return true;
+// Iteration of phase Cur after whose MFMAs slot i of the next phase's look-ahead
+// is loaded: spread evenly over Cur's last D iterations, but never before Cur has
+// read the fragment the slot still holds.
+template <class Cur, class Nxt>
+constexpr int refill_at(int i) {
+  int q = 0;
+  while (Nxt::U * (q + 1) / Cur::D <= i) ++q;   // i in [U q / D, U (q + 1) / D)
+  int j = Cur::NKB - Cur::D + q;
+  if (i < Cur::U && i / Cur::NR > j) j = i / Cur::NR;
+  return j;
 }
 // Weight fragment (k-block j, row tile f) of the running phase, by value (an
 // array copy out of the look-ahead would merge into one wide copy that keeps the
 // look-ahead in scratch memory).
-template <int NKB, int NR>
-__device__ __forceinline__ bf16x8 stream_frag(const bf16x8 (&wq)[NKB][NR], const Pre& pre, int j,
-                                              int f) {
-  constexpr int D = depth(NR);
+template <class Cur>
+__device__ __forceinline__ bf16x8 stream_frag(const bf16x8 (&wq)[Cur::NKB][Cur::NR],
+                                              const Pre& pre, int j, int f) {
+  constexpr int D = Cur::D, NR = Cur::NR;
   return j < D ? pre[(j < D ? j : 0) * NR + f] : wq[j][f];
 }
 // Loads issued at k-block j: k-block j + D of this phase, or (in the last D
-// iterations) this iteration's share of the look-ahead of the next phase, which
-// has NRN row tiles.
-template <int NKB, int NR, int NRN>
-__device__ __forceinline__ void stream_fetch(bf16x8 (&wq)[NKB][NR], Pre& pre, const WSeg& cur,
-                                             const WSeg& nxt, int j, int lane) {
-  constexpr int D = depth(NR), NU = used_slots(NRN);
-  static_assert(stream_ok(NKB, NR, NRN), "phase too short for the weight look-ahead");
+// iterations) this iteration's share of the next phase's look-ahead.
+template <class Cur, class Nxt>
+__device__ __forceinline__ void stream_fetch(bf16x8 (&wq)[Cur::NKB][Cur::NR], Pre& pre,
+                                             const WSeg& cur, const WSeg& nxt, int j, int lane) {
+  constexpr int D = Cur::D, NKB = Cur::NKB;
   if (j + D < NKB) {
 #pragma unroll
-    for (int f = 0; f < NR; ++f)
+    for (int f = 0; f < Cur::NR; ++f)
       wq[j + D][f] = wfrag(cur.P + seg_rt(cur, f) * cur.nkb + cur.kb0 + j + D, lane);
   } else {
-    const int q = j - (NKB - D);
 #pragma unroll
     for (int i = 0; i < NSLOT; ++i)   // constant bounds: unrolled before j is known
-      if (i >= NU * q / D && i < NU * (q + 1) / D) seg_slot<NRN>(pre, i, nxt, lane);
+      if (i < Nxt::U && refill_at<Cur, Nxt>(i) == j) seg_slot<Nxt>(pre, i, nxt, lane);
   }
 }
 
-// acc[ft][tt] += C^T: features 128 fh + 32 ft (packed rows of cur), tokens
-// 64 th + 32 tt (rows of ACT in LDS, columns 16 j), over NKB k-blocks.
-template <int NKB, int NRN>
-__device__ __forceinline__ void resid_phase(f32x16 (&acc)[4][2], Pre& pre, const WSeg& cur,
+// acc[ft][tt] += C^T: features 64 w + 32 ft (packed rows of cur), tokens 32 tt
+// (rows of ACT in LDS, columns 16 j), over Cur::NKB k-blocks.
+template <class Cur, class Nxt>
+__device__ __forceinline__ void resid_phase(f32x16 (&acc)[2][4], Pre& pre, const WSeg& cur,
                                             const WSeg& nxt, const bf16_t* ACT, int ald) {
+  static_assert(Cur::NR == 2, "residual phases have two row tiles per wave");
   FZ_LANE_VARS
-  bf16x8 wq[NKB][4];
-  bf16x8 xq[NKB][2];
-  const bf16_t* arow = ACT + (th * 64 + l32) * ald + 8 * hf;
-  xq[0][0] = lfrag(arow);
-  xq[0][1] = lfrag(arow + 32 * ald);
+  constexpr int NKB = Cur::NKB;
+  bf16x8 wq[NKB][2];
+  bf16x8 xq[NKB][4];
+  const bf16_t* arow = ACT + l32 * ald + 8 * hf;
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt) xq[0][tt] = lfrag(arow + 32 * tt * ald);
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
     if (j + 1 < NKB) {
-      xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
-      xq[j + 1][1] = lfrag(arow + 32 * ald + (j + 1) * 16);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) xq[j + 1][tt] = lfrag(arow + 32 * tt * ald + (j + 1) * 16);
     }
 #pragma unroll
-    for (int ft = 0; ft < 4; ++ft) {
-      const bf16x8 a = stream_frag<NKB, 4>(wq, pre, j, ft);
-      acc[ft][0] = mfma32(a, xq[j][0], acc[ft][0]);
-      acc[ft][1] = mfma32(a, xq[j][1], acc[ft][1]);
+    for (int ft = 0; ft < 2; ++ft) {
+      const bf16x8 a = stream_frag<Cur>(wq, pre, j, ft);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) acc[ft][tt] = mfma32(a, xq[j][tt], acc[ft][tt]);
     }
-    stream_fetch<NKB, 4, NRN>(wq, pre, cur, nxt, j, lane);
+    stream_fetch<Cur, Nxt>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 }
@@ -315,52 +328,51 @@ __device__ __forceinline__ bf16x8 onehot8(int idx) {   // 1.0 at element idx (no
 
 // acc += E_act[act_t] + E_time[time_t] for the block's tokens: k-block 0 holds the
 // 8 action types, k-blocks 1..4 the 64 time buckets (at columns 16 + bucket).
-template <int NRN>
-__device__ __forceinline__ void table_phase(f32x16 (&acc)[4][2], Pre& pre, const WSeg& cur,
+template <class Nxt>
+__device__ __forceinline__ void table_phase(f32x16 (&acc)[2][4], Pre& pre, const WSeg& cur,
                                             const WSeg& nxt, const int* tinfo) {
   FZ_LANE_VARS
-  constexpr int NKB = AT_COLS / 16;
-  bf16x8 wq[NKB][4];
-  int ka[2], kt[2];   // the token's one-hot column, relative to this lane's k-rows
+  constexpr int NKB = ShTab::NKB;
+  bf16x8 wq[NKB][2];
+  int ka[4], kt[4];   // the token's one-hot column, relative to this lane's k-rows
 #pragma unroll
-  for (int tt = 0; tt < 2; ++tt) {
-    const int info = tinfo[th * 64 + tt * 32 + l32];
+  for (int tt = 0; tt < 4; ++tt) {
+    const int info = tinfo[tt * 32 + l32];
     ka[tt] = (info & 0xFF) - 8 * hf;
     kt[tt] = 16 + ((info >> 8) & 0xFF) - 8 * hf;
   }
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
-    bf16x8 b[2];
+    bf16x8 b[4];
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt) b[tt] = onehot8(j == 0 ? ka[tt] : kt[tt] - 16 * j);
+    for (int tt = 0; tt < 4; ++tt) b[tt] = onehot8(j == 0 ? ka[tt] : kt[tt] - 16 * j);
 #pragma unroll
-    for (int ft = 0; ft < 4; ++ft) {
-      const bf16x8 a = stream_frag<NKB, 4>(wq, pre, j, ft);
-      acc[ft][0] = mfma32(a, b[0], acc[ft][0]);
-      acc[ft][1] = mfma32(a, b[1], acc[ft][1]);
+    for (int ft = 0; ft < 2; ++ft) {
+      const bf16x8 a = stream_frag<ShTab>(wq, pre, j, ft);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) acc[ft][tt] = mfma32(a, b[tt], acc[ft][tt]);
     }
-    stream_fetch<NKB, 4, NRN>(wq, pre, cur, nxt, j, lane);
+    stream_fetch<ShTab, Nxt>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 }
 
-// acc += E_pos[p0 + r] for the block's tokens r: the wave's 64 tokens are the
-// 4 k-blocks of E_pos^T from position p0 + 64 (w >> 1); k-block j only meets
-// token tile j / 2.
-template <int NRN>
-__device__ __forceinline__ void pos_phase(f32x16 (&acc)[4][2], Pre& pre, const WSeg& cur,
+// acc += E_pos[p0 + r] for the block's tokens r: the block's 128 positions are
+// the 8 k-blocks of E_pos^T from position p0; k-block j only meets token tile j / 2.
+template <class Nxt>
+__device__ __forceinline__ void pos_phase(f32x16 (&acc)[2][4], Pre& pre, const WSeg& cur,
                                           const WSeg& nxt) {
   FZ_LANE_VARS
-  constexpr int NKB = 4;
-  bf16x8 wq[NKB][4];
+  constexpr int NKB = ShPos::NKB;
+  bf16x8 wq[NKB][2];
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
     const int tt = j >> 1;
     const bf16x8 b = onehot8(l32 - 16 * (j & 1) - 8 * hf);
 #pragma unroll
-    for (int ft = 0; ft < 4; ++ft)
-      acc[ft][tt] = mfma32(stream_frag<NKB, 4>(wq, pre, j, ft), b, acc[ft][tt]);
-    stream_fetch<NKB, 4, NRN>(wq, pre, cur, nxt, j, lane);
+    for (int ft = 0; ft < 2; ++ft)
+      acc[ft][tt] = mfma32(stream_frag<ShPos>(wq, pre, j, ft), b, acc[ft][tt]);
+    stream_fetch<ShPos, Nxt>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 }
@@ -388,71 +400,67 @@ __device__ __forceinline__ void ln_params_store(const LnParams& q, float* P) {
 }
 
 // x <- LN(acc + bias) with gain g and offset b over the 256 features of every
-// token, with P = [bias | g | b] in LDS; Xs <- bf16(x).  Ends with a barrier.
-__device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* P, float* red,
+// token, with P = [bias | g | b] in LDS; Xs <- bf16(x).  Each wave holds 64
+// features of every token: per-token partial sums meet in LDS (red: [BT][4] sums,
+// then [BT][4] sums of squares).  Ends with a barrier.
+__device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][4], const float* P, float* red,
                                            bf16_t* Xs) {
   FZ_LANE_VARS
-  float s[2] = {0.f, 0.f}, ss[2] = {0.f, 0.f};
+  float s[4] = {0.f, 0.f, 0.f, 0.f}, ss[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int ft = 0; ft < 4; ++ft)
+  for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const float4 bi = *reinterpret_cast<const float4*>(P + fh * 128 + ft * 32 + 8 * j + 4 * hf);
+      const float4 bi = *reinterpret_cast<const float4*>(P + 64 * w + ft * 32 + 8 * j + 4 * hf);
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
+      for (int tt = 0; tt < 4; ++tt) {   // (the biased values are formed again below)
         const float v0 = acc[ft][tt][4 * j] + bi.x;
         const float v1 = acc[ft][tt][4 * j + 1] + bi.y;
         const float v2 = acc[ft][tt][4 * j + 2] + bi.z;
         const float v3 = acc[ft][tt][4 * j + 3] + bi.w;
-        acc[ft][tt][4 * j] = v0;
-        acc[ft][tt][4 * j + 1] = v1;
-        acc[ft][tt][4 * j + 2] = v2;
-        acc[ft][tt][4 * j + 3] = v3;
         s[tt] += (v0 + v1) + (v2 + v3);
         ss[tt] += (v0 * v0 + v1 * v1) + (v2 * v2 + v3 * v3);
       }
     }
 #pragma unroll
-  for (int tt = 0; tt < 2; ++tt) {
+  for (int tt = 0; tt < 4; ++tt) {   // both lane halves end with the full sums
     s[tt] = xsum32(s[tt]);
     ss[tt] = xsum32(ss[tt]);
   }
-  if (hf == 0) {   // red[tok][fh] = (sum, sumsq) over this wave's 128 features
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      const int tok = th * 64 + tt * 32 + l32;
-      *reinterpret_cast<float2*>(red + (tok * 2 + fh) * 2) = make_float2(s[tt], ss[tt]);
-    }
-  }
+  for (int tt = 0; tt < 4; ++tt)     // half 0 stores the sums, half 1 the squares
+    red[hf * BT * 4 + (tt * 32 + l32) * 4 + w] = hf ? ss[tt] : s[tt];
   __syncthreads();
-  float rstd[2], shift[2];   // x_hat = x rstd + shift
+  float rstd[4], shift[4];   // x_hat = x rstd + shift
 #pragma unroll
-  for (int tt = 0; tt < 2; ++tt) {
-    const int tok = th * 64 + tt * 32 + l32;
+  for (int tt = 0; tt < 4; ++tt) {
+    const int tok = tt * 32 + l32;
     const float4 a = *reinterpret_cast<const float4*>(red + tok * 4);
-    const float mean = (a.x + a.z) * (1.f / DM);
-    const float var = fmaxf((a.y + a.w) * (1.f / DM) - mean * mean, 0.f);
+    const float4 b = *reinterpret_cast<const float4*>(red + BT * 4 + tok * 4);
+    const float mean = ((a.x + a.y) + (a.z + a.w)) * (1.f / DM);
+    const float var = fmaxf(((b.x + b.y) + (b.z + b.w)) * (1.f / DM) - mean * mean, 0.f);
     rstd[tt] = rsqrtf(var + 1e-5f);
     shift[tt] = -mean * rstd[tt];
   }
 #pragma unroll
-  for (int ft = 0; ft < 4; ++ft)
+  for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int f = fh * 128 + ft * 32 + 8 * j + 4 * hf;
+      const int f = 64 * w + ft * 32 + 8 * j + 4 * hf;
+      const float4 bi = *reinterpret_cast<const float4*>(P + f);
       const float4 gg = *reinterpret_cast<const float4*>(P + DM + f);
       const float4 bb = *reinterpret_cast<const float4*>(P + 2 * DM + f);
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
-        const float v0 = fmaf(fmaf(acc[ft][tt][4 * j], rstd[tt], shift[tt]), gg.x, bb.x);
-        const float v1 = fmaf(fmaf(acc[ft][tt][4 * j + 1], rstd[tt], shift[tt]), gg.y, bb.y);
-        const float v2 = fmaf(fmaf(acc[ft][tt][4 * j + 2], rstd[tt], shift[tt]), gg.z, bb.z);
-        const float v3 = fmaf(fmaf(acc[ft][tt][4 * j + 3], rstd[tt], shift[tt]), gg.w, bb.w);
+      for (int tt = 0; tt < 4; ++tt) {
+        const float v0 = fmaf(fmaf(acc[ft][tt][4 * j] + bi.x, rstd[tt], shift[tt]), gg.x, bb.x);
+        const float v1 = fmaf(fmaf(acc[ft][tt][4 * j + 1] + bi.y, rstd[tt], shift[tt]), gg.y, bb.y);
+        const float v2 = fmaf(fmaf(acc[ft][tt][4 * j + 2] + bi.z, rstd[tt], shift[tt]), gg.z, bb.z);
+        const float v3 = fmaf(fmaf(acc[ft][tt][4 * j + 3] + bi.w, rstd[tt], shift[tt]), gg.w, bb.w);
         acc[ft][tt][4 * j] = v0;
         acc[ft][tt][4 * j + 1] = v1;
         acc[ft][tt][4 * j + 2] = v2;
         acc[ft][tt][4 * j + 3] = v3;
-        st4(Xs + (th * 64 + tt * 32 + l32) * XLD + f, v0, v1, v2, v3);
+        st4(Xs + (tt * 32 + l32) * XLD + f, v0, v1, v2, v3);
       }
     }
   __syncthreads();
@@ -460,10 +468,11 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* P, 
 
 // ---------------------------------------------------------------- pooling
 // Max over the block's valid tokens (token < nvalid) of Y^T = acc, folded into
-// pmax (b_pool is added to the final max: rounding is monotonic, so
-// max(y + b) = max(y) + b exactly).  The 64 per-lane features are max-reduced across the 32 lanes of a
-// half with a transposing butterfly (each step halves the values a lane keeps).
-// Ends with a barrier.
+// the lane's running maximum pm (b_pool is added to the final max: rounding is
+// monotonic, so max(y + b) = max(y) + b exactly).  A lane's 32 values (its
+// features' maxima over its 4 tokens) are max-reduced across the 32 lanes of its
+// half with a transposing butterfly (each step halves the values a lane keeps),
+// which leaves feature pool_feature() of the wave's 64 in each lane.
 #define FZ_TMAX(HALF, MASK)                                                   \
   _Pragma("unroll") for (int k = 0; k < (HALF); ++k) {                        \
     const bool up = (l32 & (MASK)) != 0;                                      \
@@ -472,40 +481,33 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[4][2], const float* P, 
     v[k] = fmaxf(keep, __shfl_xor(send, (MASK), WAVE));                       \
   }
 
-__device__ __forceinline__ void pool_block(f32x16 (&acc)[4][2], float* pmax, float* red,
-                                           int nvalid) {
+__device__ __forceinline__ int pool_feature() {
   FZ_LANE_VARS
-  float v[64];
+  // value index kept by the butterfly: bit i of l32 selected the upper half at
+  // the step that halved 32 values to 16 >> i
+  const int k = ((l32 & 1) << 4) | ((l32 & 2) << 2) | (l32 & 4) | ((l32 & 8) >> 2) |
+                ((l32 & 16) >> 4);
+  return 64 * w + (k >> 4) * 32 + 8 * ((k & 15) >> 2) + 4 * hf + (k & 3);
+}
+__device__ __forceinline__ float pool_block(f32x16 (&acc)[2][4], float pm, int nvalid) {
+  FZ_LANE_VARS
+  float v[32];
 #pragma unroll
-  for (int ft = 0; ft < 4; ++ft)
+  for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       float m = -__builtin_inff();
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-        if (th * 64 + tt * 32 + l32 < nvalid) m = fmaxf(m, acc[ft][tt][r]);
+      for (int tt = 0; tt < 4; ++tt)
+        if (tt * 32 + l32 < nvalid) m = fmaxf(m, acc[ft][tt][r]);
       v[ft * 16 + r] = m;
     }
-  FZ_TMAX(32, 1)
-  FZ_TMAX(16, 2)
-  FZ_TMAX(8, 4)
-  FZ_TMAX(4, 8)
-  FZ_TMAX(2, 16)
-  // this lane now holds value indices base and base + 1 of its 64
-  const int base = ((l32 & 1) << 5) | ((l32 & 2) << 3) | ((l32 & 4) << 1) | ((l32 & 8) >> 1) |
-                   ((l32 & 16) >> 3);
-#pragma unroll
-  for (int u = 0; u < 2; ++u) {
-    const int k = base + u;
-    const int f = fh * 128 + (k >> 4) * 32 + 8 * ((k & 15) >> 2) + 4 * hf + (k & 3);
-    red[th * DM + f] = v[u];
-  }
-  __syncthreads();
-  {
-    const int c = tid_;
-    pmax[c] = fmaxf(pmax[c], fmaxf(red[c], red[DM + c]));
-  }
-  __syncthreads();
+  FZ_TMAX(16, 1)
+  FZ_TMAX(8, 2)
+  FZ_TMAX(4, 4)
+  FZ_TMAX(2, 8)
+  FZ_TMAX(1, 16)
+  return fmaxf(pm, v[0]);
 }
 
 // ---------------------------------------------------------------- attention
@@ -737,7 +739,7 @@ __device__ __forceinline__ int64_t nl_of(const Args& A, int64_t n) { return n - 
 // past the valid length get whatever these give (token rows of zeros): no valid
 // row ever reads them (causal mask, per-token sublayers, pooling over valid rows).
 __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int p0, int Tv,
-                                                   f32x16 (&acc)[4][2], bf16_t* Xs,
+                                                   f32x16 (&acc)[2][4], bf16_t* Xs,
                                                    int* tinfo, const uint8_t** rowptr, Pre& pre,
                                                    const WSeg& nxt) {
   const int d = A.d;
@@ -774,12 +776,12 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
       FZ_LANE_VARS
       const float* cv = A.cvec + nl_of(A, n) * DM;
 #pragma unroll
-      for (int ft = 0; ft < 4; ++ft)
+      for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float4 c4 = *reinterpret_cast<const float4*>(cv + fh * 128 + ft * 32 + 8 * j + 4 * hf);
+          const float4 c4 = *reinterpret_cast<const float4*>(cv + 64 * w + ft * 32 + 8 * j + 4 * hf);
 #pragma unroll
-          for (int tt = 0; tt < 2; ++tt) {
+          for (int tt = 0; tt < 4; ++tt) {
             acc[ft][tt][4 * j] = c4.x;
             acc[ft][tt][4 * j + 1] = c4.y;
             acc[ft][tt][4 * j + 2] = c4.z;
@@ -798,21 +800,21 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
   {
     const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
     const WSeg s_at = seg_resid(A.pk_at, AT_COLS / 16, 0, w);
-    const WSeg s_pos = seg_resid(A.pk_pos, A.pos_nkb, p0 / 16 + 4 * (w >> 1), w);
-    resid_phase<KIN / 16, 4>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), s_at, Xs, XLD);
-    table_phase<4>(acc, pre, s_at, s_pos, tinfo);
-    pos_phase<3>(acc, pre, s_pos, nxt);
+    const WSeg s_pos = seg_resid(A.pk_pos, A.pos_nkb, p0 / 16, w);
+    resid_phase<ShEmb, ShTab>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), s_at, Xs, XLD);
+    table_phase<ShPos>(acc, pre, s_at, s_pos, tinfo);
+    pos_phase<ShQkv>(acc, pre, s_pos, nxt);
   }
   {
     FZ_LANE_VARS
     __syncthreads();   // every wave is past Xs (tokens) and tinfo
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
+    for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-      for (int ft = 0; ft < 4; ++ft)
+      for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          st4(Xs + (th * 64 + tt * 32 + l32) * XLD + fh * 128 + ft * 32 + 8 * j + 4 * hf,
+          st4(Xs + (tt * 32 + l32) * XLD + 64 * w + ft * 32 + 8 * j + 4 * hf,
               acc[ft][tt][4 * j], acc[ft][tt][4 * j + 1], acc[ft][tt][4 * j + 2],
               acc[ft][tt][4 * j + 3]);
     __syncthreads();
@@ -866,22 +868,22 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
     if constexpr (CS == 0) {   // q0 q1 k0: transposed
 #pragma unroll
       for (int t = 0; t < 3; ++t) {
-        const bf16x8 a = stream_frag<NKB, 3>(wq, pre, j, t);
+        const bf16x8 a = stream_frag<ShQkv>(wq, pre, j, t);
         qa[t][0] = mfma32(a, xq[j][0], qa[t][0]);
         qa[t][1] = mfma32(a, xq[j][1], qa[t][1]);
       }
     } else {         // k1 transposed; v0 v1 untransposed
-      const bf16x8 a0 = stream_frag<NKB, 3>(wq, pre, j, 0);
+      const bf16x8 a0 = stream_frag<ShQkv>(wq, pre, j, 0);
       qa[0][0] = mfma32(a0, xq[j][0], qa[0][0]);
       qa[0][1] = mfma32(a0, xq[j][1], qa[0][1]);
 #pragma unroll
       for (int t = 1; t < 3; ++t) {
-        const bf16x8 a = stream_frag<NKB, 3>(wq, pre, j, t);
+        const bf16x8 a = stream_frag<ShQkv>(wq, pre, j, t);
         qa[t][0] = mfma32(xq[j][0], a, qa[t][0]);
         qa[t][1] = mfma32(xq[j][1], a, qa[t][1]);
       }
     }
-    stream_fetch<NKB, 3, 0>(wq, pre, cur, nxt, j, lane);
+    stream_fetch<ShQkv, NoPhase>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
@@ -957,11 +959,11 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const bf16x8 a = stream_frag<NKB, 2>(wq, pre, j, t);
+      const bf16x8 a = stream_frag<ShF1>(wq, pre, j, t);
       ha[t][0] = mfma32(a, xq[j][0], ha[t][0]);
       ha[t][1] = mfma32(a, xq[j][1], ha[t][1]);
     }
-    stream_fetch<NKB, 2, 4>(wq, pre, cur, nxt, j, lane);
+    stream_fetch<ShF1, ShF2>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
@@ -1003,7 +1005,7 @@ __device__ __forceinline__ void cache_store(const Args& A, int g, int p0, const 
 // per head, and acc += O_g W_o[:, group]^T.  The stream leaves primed with the
 // first FFN chunk of the layer.
 __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_layer& L,
-                                                   const LayerPk& pk, f32x16 (&acc)[4][2],
+                                                   const LayerPk& pk, f32x16 (&acc)[2][4],
                                                    Pre& pre, bf16_t* Xs,
                                                    bf16_t* Qs, bf16_t* Ks, bf16_t* Vts, bf16_t* Kc,
                                                    bf16_t* Vc, bf16_t* kc, bf16_t* vc, int p0,
@@ -1022,16 +1024,16 @@ __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_lay
       attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
     // the output projection's look-ahead starts here rather than across the
     // attention, whose own registers it would otherwise crowd
-    seg_prime<4>(pre, so, otid() % WAVE);
+    seg_prime<ShWo>(pre, so, otid() % WAVE);
     __syncthreads();
     // the cache stores follow the phase's weight loads, so the next phase's first
     // wait on its weights does not also wait for the stores
     if (g + 1 < DM / 64) {
-      resid_phase<4, 3>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD);
+      resid_phase<ShWo, ShQkv>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD);
       if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
     } else {   // the staging area is free now: it receives the LayerNorm parameters
       const LnParams q = ln_params_load(L.b_o, L.ln1_g, L.ln1_b);
-      resid_phase<4, 2>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
+      resid_phase<ShWo, ShF1>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
       if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
       ln_params_store(q, reinterpret_cast<float*>(Kc));
     }
@@ -1044,7 +1046,7 @@ __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_lay
 // primed with `after`: the next layer's first Q / K / V phase, or (last layer)
 // the pooling projection.
 __device__ __forceinline__ void ffn_sublayer(const Args& A, const tav2_layer& L,
-                                             const LayerPk& pk, f32x16 (&acc)[4][2], Pre& pre,
+                                             const LayerPk& pk, f32x16 (&acc)[2][4], Pre& pre,
                                              const WSeg& after, bool after_is_qkv, bf16_t* Xs,
                                              bf16_t* Hs) {
   const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
@@ -1059,13 +1061,13 @@ __device__ __forceinline__ void ffn_sublayer(const Args& A, const tav2_layer& L,
     // loaded before the second layer's weight loads, consumed by the next chunk
     if (c + 1 < nch) b1_load(bh, L.b_1, c + 1);
     if (c + 1 < nch) {
-      resid_phase<FC / 16, 2>(acc, pre, s2, seg_ffn1(pk.w1, c + 1, w), Hs, HLD);
+      resid_phase<ShF2, ShF1>(acc, pre, s2, seg_ffn1(pk.w1, c + 1, w), Hs, HLD);
     } else {   // the LayerNorm parameters go past the hidden chunk
       const LnParams q = ln_params_load(L.b_2, L.ln2_g, L.ln2_b);
       if (after_is_qkv)
-        resid_phase<FC / 16, 3>(acc, pre, s2, after, Hs, HLD);
+        resid_phase<ShF2, ShQkv>(acc, pre, s2, after, Hs, HLD);
       else
-        resid_phase<FC / 16, 4>(acc, pre, s2, after, Hs, HLD);
+        resid_phase<ShF2, ShPool>(acc, pre, s2, after, Hs, HLD);
       ln_params_store(q, reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(Hs) + BT * HLD * 2));
     }
     __syncthreads();   // Hs is rewritten by the next chunk
@@ -1079,7 +1081,6 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
   uint8_t* Sc = smem + XS_BYTES;
   bf16_t* Kc = reinterpret_cast<bf16_t*>(smem + XS_BYTES + SC_BYTES);
   bf16_t* Vc = reinterpret_cast<bf16_t*>(smem + XS_BYTES + SC_BYTES + QS_BYTES);
-  float* pmax = reinterpret_cast<float*>(smem + XS_BYTES + SC_BYTES + CS_BYTES);
   bf16_t* Qs = reinterpret_cast<bf16_t*>(Sc);                    // [BT][QLD], then O
   bf16_t* Ks = reinterpret_cast<bf16_t*>(Sc + QS_BYTES);         // [BT][QLD]
   bf16_t* Vts = reinterpret_cast<bf16_t*>(Sc + 2 * QS_BYTES);    // [64][VLD]
@@ -1099,7 +1100,6 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
     return;
   }
   const int nblk = (Tv + BT - 1) / BT;
-  for (int c = threadIdx.x; c < DM; c += NT) pmax[c] = -__builtin_inff();
   // layer records are read through the kernel-argument segment so the runtime
   // layer index stays a scalar load instead of a private copy of the array
   const Args* AK = (const Args*)(__builtin_amdgcn_kernarg_segment_ptr());
@@ -1107,8 +1107,9 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
   const WSeg s_embed = seg_resid(A.pk_in, KIN / 16, 0, wv);
   const WSeg s_pool = seg_resid(A.pk_pool, DM / 16, 0, wv);
   Pre pre;
-  seg_prime<4>(pre, s_embed, otid() % WAVE);
-  f32x16 acc[4][2];
+  seg_prime<ShEmb>(pre, s_embed, otid() % WAVE);
+  f32x16 acc[2][4];
+  float pm = -__builtin_inff();   // running pooled max of feature pool_feature()
   for (int blk = 0; blk < nblk; ++blk) {
     const int p0 = blk * BT;
     __syncthreads();
@@ -1133,13 +1134,13 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
       const int last = Tv - 1 - p0;
       if (last >= 0 && last < BT) {
 #pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-          if (th * 64 + tt * 32 + l32 == last) {
+        for (int tt = 0; tt < 4; ++tt)
+          if (tt * 32 + l32 == last) {
 #pragma unroll
-            for (int ft = 0; ft < 4; ++ft)
+            for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
               for (int j = 0; j < 4; ++j) {
-                const int f = fh * 128 + ft * 32 + 8 * j + 4 * hf;
+                const int f = 64 * w + ft * 32 + 8 * j + 4 * hf;
                 *reinterpret_cast<float4*>(out + DM + f) =
                     make_float4(acc[ft][tt][4 * j], acc[ft][tt][4 * j + 1],
                                 acc[ft][tt][4 * j + 2], acc[ft][tt][4 * j + 3]);
@@ -1148,15 +1149,18 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
       }
     }
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+      for (int b = 0; b < 4; ++b) acc[a][b] = f32x16{};
     // the pool phase prefetches the next block's input projection (also after the
     // last block, where the loads are simply unused)
-    resid_phase<DM / 16, 4>(acc, pre, s_pool, s_embed, Xs, XLD);
-    pool_block(acc, pmax, red, Tv - p0);
+    resid_phase<ShPool, ShEmb>(acc, pre, s_pool, s_embed, Xs, XLD);
+    pm = pool_block(acc, pm, Tv - p0);
   }
-  for (int c = threadIdx.x; c < DM; c += NT) out[c] = pmax[c] + A.b_pool[c];
+  {
+    const int f = pool_feature();
+    out[f] = pm + A.b_pool[f];
+  }
 }
 
 // ---------------------------------------------------------------- candidate half
