@@ -56,6 +56,7 @@ constexpr int KIN = 256;         // packed width of the token half of W_in (d ze
 constexpr int N_ACT = 8;         // action-type table rows (types are clamped to 0..7)
 constexpr int N_TIME = 64;       // time-bucket table rows (buckets are clamped to 0..63)
 constexpr int AT_COLS = 80;      // packed [E_act^T | 0 | E_time^T] columns: 0..7, 16..79
+constexpr int MAX_FFN = 4096;    // largest d_ffn (its first-layer biases are staged in LDS)
 
 constexpr int XS_BYTES = BT * XLD * 2;                 // 67584
 constexpr int QS_BYTES = BT * QLD * 2;                 // 18432
@@ -66,7 +67,8 @@ constexpr int LDS_BYTES = XS_BYTES + SC_BYTES + CS_BYTES;
 static_assert(LDS_BYTES <= 163840, "fused encoder exceeds the 160 KiB of LDS");
 static_assert(BT * HLD * 2 <= SC_BYTES, "FFN chunk does not fit the scratch region");
 static_assert(BT * HLD * 2 + 3 * DM * 4 <= SC_BYTES, "LayerNorm 2 parameters do not fit");
-static_assert(2 * BT * 4 * 4 <= QS_BYTES && 3 * DM * 4 <= CS_BYTES, "LayerNorm 1 buffers do not fit");
+static_assert(2 * BT * 4 * 4 <= QS_BYTES && (3 * DM + MAX_FFN) * 4 <= CS_BYTES,
+              "LayerNorm 1 and first-layer bias buffers do not fit");
 static_assert(BT * 8 + BT * 8 <= SC_BYTES, "encoding buffers do not fit");
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -386,6 +388,30 @@ __device__ __forceinline__ void pos_phase(f32x16 (&acc)[2][4], Pre& pre, const W
 struct LnParams {
   float bias, gain, off;
 };
+// The FFN's first-layer biases (up to 4096) go to LDS the same way, with the
+// first LayerNorm's parameters.
+struct FfnBias {
+  float4 v[4];
+};
+static_assert(MAX_FFN == 4 * 4 * NT, "first-layer bias staging: 4 float4 per thread");
+__device__ __forceinline__ FfnBias ffn_bias_load(const float* b_1, int ffn) {
+  const int t = otid();
+  FfnBias q;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = 4 * (t + i * NT);
+    q.v[i] = e < ffn ? *reinterpret_cast<const float4*>(b_1 + e) : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  return q;
+}
+__device__ __forceinline__ void ffn_bias_store(const FfnBias& q, float* P, int ffn) {
+  const int t = otid();
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int e = 4 * (t + i * NT);
+    if (e < ffn) *reinterpret_cast<float4*>(P + e) = q.v[i];
+  }
+}
 static_assert(NT == DM, "one LayerNorm parameter triple per thread");
 __device__ __forceinline__ LnParams ln_params_load(const float* bias, const float* g,
                                                    const float* b) {
@@ -824,9 +850,9 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
 // ---------------------------------------------------------------- sublayers
 // Q / K / V of head group g: wave w computes token tiles 2(w & 1), 2(w & 1) + 1 of
 // column tiles 3 CS .. +2 of [q0 q1 k0 k1 v0 v1] (CS = w >> 1); Q and K
-// transposed ([dim][token]), V untransposed.  Leaves the look-ahead empty (the
-// output projection primes its own after the attention).  The
-// column split is a template parameter so that each wave runs a branch-free
+// transposed ([dim][token]), V untransposed.  Its last iterations load the
+// look-ahead of the group's output projection, which arrives during the
+// attention.  The column split is a template parameter so that each wave runs a branch-free
 // loop with fixed accumulator registers.
 template <int CS>
 __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
@@ -883,7 +909,7 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
         qa[t][1] = mfma32(xq[j][1], a, qa[t][1]);
       }
     }
-    stream_fetch<ShQkv, NoPhase>(wq, pre, cur, nxt, j, lane);
+    stream_fetch<ShQkv, ShWo>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
@@ -915,25 +941,14 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
 
 // FFN first layer, chunk c: H^T = ReLU(W_1[chunk] Xs^T + b_1) into Hs (wave w:
 // hidden tiles 2(w & 1) + {0,1}, token tiles 2(w >> 1) + {0,1}).  The
-// accumulators start at the chunk's biases bh (loaded by the caller ahead of
-// time); ReLU acts on the packed bf16 pairs (for bf16 bit patterns the signed
+// accumulators start at the chunk's biases b1c (in LDS); ReLU acts on the packed bf16 pairs (for bf16 bit patterns the signed
 // 16-bit max with zero is exactly ReLU, and rounding commutes with it).
-__device__ __forceinline__ void b1_load(float4 (&bh)[2][4], const float* b_1, int c) {
-  FZ_LANE_VARS
-  const int hp = w & 1;
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      bh[t][j] = *reinterpret_cast<const float4*>(b_1 + c * FC + (2 * hp + t) * 32 + 8 * j + 4 * hf);
-}
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t relu2(uint32_t x) {
   return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, x), s16x2{0, 0}));
 }
 __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
-                                           const float4 (&bh)[2][4], const bf16_t* Xs,
-                                           bf16_t* Hs) {
+                                           const float* b1c, const bf16_t* Xs, bf16_t* Hs) {
   FZ_LANE_VARS
   constexpr int NKB = DM / 16;
   const int hp = w & 1, tp = w >> 1;
@@ -942,7 +957,8 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const float bb[4] = {bh[t][j].x, bh[t][j].y, bh[t][j].z, bh[t][j].w};
+      const float4 b4 = *reinterpret_cast<const float4*>(b1c + (2 * hp + t) * 32 + 8 * j + 4 * hf);
+      const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
       for (int i = 0; i < 4; ++i) ha[t][0][4 * j + i] = ha[t][1][4 * j + i] = bb[i];
     }
@@ -1004,79 +1020,98 @@ __device__ __forceinline__ void cache_store(const Args& A, int g, int p0, const 
 // V^T into LDS (and K / V^T into the cache for later blocks), causal attention
 // per head, and acc += O_g W_o[:, group]^T.  The stream leaves primed with the
 // first FFN chunk of the layer.
+template <bool LAST>
+__device__ __forceinline__ void attention_group(const Args& A, const tav2_layer& L,
+                                                const LayerPk& pk, f32x16 (&acc)[2][4], Pre& pre,
+                                                bf16_t* Xs, bf16_t* Qs, bf16_t* Ks, bf16_t* Vts,
+                                                bf16_t* Kc, bf16_t* Vc, bf16_t* kc, bf16_t* vc,
+                                                int p0, bool keep, int g) {
+  const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
+  const WSeg so = seg_resid(pk.o, DM / 16, 4 * g, w);
+  if (w < 2)
+    qkv_phase<0>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
+  else
+    qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
+  __syncthreads();
+  if (A.dh == 64)
+    attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
+  else
+    attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
+  __syncthreads();
+  // the cache stores follow the phase's weight loads, so the next phase's first
+  // wait on its weights does not also wait for the stores
+  if constexpr (!LAST) {
+    resid_phase<ShWo, ShQkv>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD);
+    if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
+  } else {   // the staging area is free now: it receives the LayerNorm parameters
+    const LnParams q = ln_params_load(L.b_o, L.ln1_g, L.ln1_b);   // and the FFN biases
+    const FfnBias fb = ffn_bias_load(L.b_1, A.ffn);
+    resid_phase<ShWo, ShF1>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
+    if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
+    ln_params_store(q, reinterpret_cast<float*>(Kc));
+    ffn_bias_store(fb, reinterpret_cast<float*>(Kc) + 3 * DM, A.ffn);
+  }
+  __syncthreads();   // Qs (O) and Ks / Vts are rewritten by the next group
+}
+// The last head group is peeled out of the loop: the code after it (LayerNorm)
+// then sees exactly which weight loads are still in flight.
 __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_layer& L,
                                                    const LayerPk& pk, f32x16 (&acc)[2][4],
                                                    Pre& pre, bf16_t* Xs,
                                                    bf16_t* Qs, bf16_t* Ks, bf16_t* Vts, bf16_t* Kc,
                                                    bf16_t* Vc, bf16_t* kc, bf16_t* vc, int p0,
                                                    bool keep) {
-  const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
-  for (int g = 0; g < DM / 64; ++g) {
-    const WSeg so = seg_resid(pk.o, DM / 16, 4 * g, w);
-    if (w < 2)
-      qkv_phase<0>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
-    else
-      qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
-    __syncthreads();
-    if (A.dh == 64)
-      attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
-    else
-      attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
-    // the output projection's look-ahead starts here rather than across the
-    // attention, whose own registers it would otherwise crowd
-    seg_prime<ShWo>(pre, so, otid() % WAVE);
-    __syncthreads();
-    // the cache stores follow the phase's weight loads, so the next phase's first
-    // wait on its weights does not also wait for the stores
-    if (g + 1 < DM / 64) {
-      resid_phase<ShWo, ShQkv>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD);
-      if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
-    } else {   // the staging area is free now: it receives the LayerNorm parameters
-      const LnParams q = ln_params_load(L.b_o, L.ln1_g, L.ln1_b);
-      resid_phase<ShWo, ShF1>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
-      if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
-      ln_params_store(q, reinterpret_cast<float*>(Kc));
-    }
-    __syncthreads();   // Qs (O) and Ks / Vts are rewritten by the next group
-  }
+  for (int g = 0; g + 1 < DM / 64; ++g)
+    attention_group<false>(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep, g);
+  attention_group<true>(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep, DM / 64 - 1);
 }
 
 // FFN sublayer: per chunk of 128 hidden units, H^T into LDS, then
 // acc += W_2[:, chunk] H^T.  The stream enters primed with chunk 0 and leaves
 // primed with `after`: the next layer's first Q / K / V phase, or (last layer)
-// the pooling projection.
+// the pooling projection (shape After).  The first-layer biases are in LDS at
+// b1s.  The last chunk is peeled out of the loop (see attention_sublayer).
+template <bool LAST, class After>
+__device__ __forceinline__ void ffn_chunk(const Args& A, const tav2_layer& L, const LayerPk& pk,
+                                          f32x16 (&acc)[2][4], Pre& pre, const WSeg& after,
+                                          const bf16_t* Xs, bf16_t* Hs, const float* b1s, int c) {
+  const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
+  const WSeg s2 = seg_resid(pk.w2, A.ffn / 16, c * (FC / 16), w);
+  // last chunk: the LayerNorm parameters are loaded ahead of the first layer's
+  // weight loads and go past the hidden chunk before the second layer
+  LnParams q;
+  if constexpr (LAST) q = ln_params_load(L.b_2, L.ln2_g, L.ln2_b);
+  ffn1_phase(pre, seg_ffn1(pk.w1, c, w), s2, b1s + c * FC, Xs, Hs);
+  if constexpr (LAST)
+    ln_params_store(q, reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(Hs) + BT * HLD * 2));
+  __syncthreads();
+  if constexpr (!LAST)
+    resid_phase<ShF2, ShF1>(acc, pre, s2, seg_ffn1(pk.w1, c + 1, w), Hs, HLD);
+  else
+    resid_phase<ShF2, After>(acc, pre, s2, after, Hs, HLD);
+  __syncthreads();   // Hs is rewritten by the next chunk
+}
+template <class After>
 __device__ __forceinline__ void ffn_sublayer(const Args& A, const tav2_layer& L,
                                              const LayerPk& pk, f32x16 (&acc)[2][4], Pre& pre,
-                                             const WSeg& after, bool after_is_qkv, bf16_t* Xs,
-                                             bf16_t* Hs) {
-  const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
-  const int ffn = A.ffn;
-  const int nch = ffn / FC;
-  float4 bh[2][4];   // the next chunk's first-layer biases
-  b1_load(bh, L.b_1, 0);
-  for (int c = 0; c < nch; ++c) {
-    const WSeg s2 = seg_resid(pk.w2, ffn / 16, c * (FC / 16), w);
-    ffn1_phase(pre, seg_ffn1(pk.w1, c, w), s2, bh, Xs, Hs);
-    __syncthreads();
-    // loaded before the second layer's weight loads, consumed by the next chunk
-    if (c + 1 < nch) b1_load(bh, L.b_1, c + 1);
-    if (c + 1 < nch) {
-      resid_phase<ShF2, ShF1>(acc, pre, s2, seg_ffn1(pk.w1, c + 1, w), Hs, HLD);
-    } else {   // the LayerNorm parameters go past the hidden chunk
-      const LnParams q = ln_params_load(L.b_2, L.ln2_g, L.ln2_b);
-      if (after_is_qkv)
-        resid_phase<ShF2, ShQkv>(acc, pre, s2, after, Hs, HLD);
-      else
-        resid_phase<ShF2, ShPool>(acc, pre, s2, after, Hs, HLD);
-      ln_params_store(q, reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(Hs) + BT * HLD * 2));
-    }
-    __syncthreads();   // Hs is rewritten by the next chunk
-  }
+                                             const WSeg& after, bf16_t* Xs, bf16_t* Hs,
+                                             const float* b1s) {
+  const int nch = A.ffn / FC;
+  for (int c = 0; c + 1 < nch; ++c)
+    ffn_chunk<false, After>(A, L, pk, acc, pre, after, Xs, Hs, b1s, c);
+  ffn_chunk<true, After>(A, L, pk, acc, pre, after, Xs, Hs, b1s, nch - 1);
 }
 
-// ---------------------------------------------------------------- the kernel
-__global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
+// One encoder layer of the block: attention, LayerNorm 1, FFN, LayerNorm 2.  The
+// last layer is a separate instance (its FFN leaves the stream primed with the
+// pooling projection instead of the next layer's Q / K / V), so that no code
+// joins two different look-ahead states.
+template <bool LASTL>
+__device__ __forceinline__ void encoder_layer(const Args& A, int li, f32x16 (&acc)[2][4],
+                                              Pre& pre, uint8_t* smem, int64_t nl, int p0,
+                                              bool keep) {
+  const Args* AK = (const Args*)(__builtin_amdgcn_kernarg_segment_ptr());
+  const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
   bf16_t* Xs = reinterpret_cast<bf16_t*>(smem);
   uint8_t* Sc = smem + XS_BYTES;
   bf16_t* Kc = reinterpret_cast<bf16_t*>(smem + XS_BYTES + SC_BYTES);
@@ -1088,6 +1123,28 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
   float* red = reinterpret_cast<float*>(Sc);                     // reductions
   float* lnp1 = reinterpret_cast<float*>(Kc);                    // LayerNorm 1 parameters
   float* lnp2 = reinterpret_cast<float*>(Sc + BT * HLD * 2);     // LayerNorm 2 parameters
+  // layer records are read through the kernel-argument segment so the runtime
+  // layer index stays a scalar load instead of a private copy of the array
+  const tav2_layer L = AK->layers[li];
+  const LayerPk pk = AK->pk[li];
+  bf16_t* kc = A.kcache ? A.kcache + (nl * A.n_layers + li) * int64_t(A.tpad) * DM : nullptr;
+  bf16_t* vc = A.vcache ? A.vcache + (nl * A.n_layers + li) * int64_t(DM) * A.tpad : nullptr;
+  attention_sublayer(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep);
+  layer_norm(acc, lnp1, red, Xs);
+  if constexpr (LASTL)
+    ffn_sublayer<ShPool>(A, L, pk, acc, pre, seg_resid(A.pk_pool, DM / 16, 0, w), Xs, Hs,
+                         lnp1 + 3 * DM);
+  else
+    ffn_sublayer<ShQkv>(A, L, pk, acc, pre, seg_qkv(AK->pk[li + 1].qkv, 0, w), Xs, Hs,
+                        lnp1 + 3 * DM);
+  layer_norm(acc, lnp2, red, Xs);
+}
+
+// ---------------------------------------------------------------- the kernel
+__global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[LDS_BYTES];
+  bf16_t* Xs = reinterpret_cast<bf16_t*>(smem);
+  uint8_t* Sc = smem + XS_BYTES;
   int* tinfo = reinterpret_cast<int*>(Sc);                       // [BT] during encoding
   const uint8_t** rowptr = reinterpret_cast<const uint8_t**>(Sc + BT * 8);   // [BT]
 
@@ -1100,8 +1157,6 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
     return;
   }
   const int nblk = (Tv + BT - 1) / BT;
-  // layer records are read through the kernel-argument segment so the runtime
-  // layer index stays a scalar load instead of a private copy of the array
   const Args* AK = (const Args*)(__builtin_amdgcn_kernarg_segment_ptr());
   const int wv = __builtin_amdgcn_readfirstlane(otid() / WAVE);
   const WSeg s_embed = seg_resid(A.pk_in, KIN / 16, 0, wv);
@@ -1115,19 +1170,9 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
     __syncthreads();
     encode_block_input(A, n, p0, Tv, acc, Xs, tinfo, rowptr, pre,
                        seg_qkv(AK->pk[0].qkv, 0, wv));
-    for (int li = 0; li < A.n_layers; ++li) {
-      const tav2_layer L = AK->layers[li];
-      const LayerPk pk = AK->pk[li];
-      bf16_t* kc = A.kcache ? A.kcache + (nl * A.n_layers + li) * int64_t(A.tpad) * DM : nullptr;
-      bf16_t* vc = A.vcache ? A.vcache + (nl * A.n_layers + li) * int64_t(DM) * A.tpad : nullptr;
-      attention_sublayer(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0,
-                         blk + 1 < nblk);
-      layer_norm(acc, lnp1, red, Xs);
-      const bool more = li + 1 < A.n_layers;
-      const WSeg after = more ? seg_qkv(AK->pk[li + 1].qkv, 0, wv) : s_pool;
-      ffn_sublayer(A, L, pk, acc, pre, after, more, Xs, Hs);
-      layer_norm(acc, lnp2, red, Xs);
-    }
+    for (int li = 0; li + 1 < A.n_layers; ++li)
+      encoder_layer<false>(A, li, acc, pre, smem, nl, p0, blk + 1 < nblk);
+    encoder_layer<true>(A, A.n_layers - 1, acc, pre, smem, nl, p0, blk + 1 < nblk);
     // ---- head: out[DM:] = X of the last valid token; running max of the pool
     {
       FZ_LANE_VARS
