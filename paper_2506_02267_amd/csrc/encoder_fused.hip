@@ -850,9 +850,8 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
 // ---------------------------------------------------------------- sublayers
 // Q / K / V of head group g: wave w computes token tiles 2(w & 1), 2(w & 1) + 1 of
 // column tiles 3 CS .. +2 of [q0 q1 k0 k1 v0 v1] (CS = w >> 1); Q and K
-// transposed ([dim][token]), V untransposed.  Its last iterations load the
-// look-ahead of the group's output projection, which arrives during the
-// attention.  The column split is a template parameter so that each wave runs a branch-free
+// transposed ([dim][token]), V untransposed.  Leaves the look-ahead empty.  The
+// column split is a template parameter so that each wave runs a branch-free
 // loop with fixed accumulator registers.
 template <int CS>
 __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
@@ -909,7 +908,7 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
         qa[t][1] = mfma32(xq[j][1], a, qa[t][1]);
       }
     }
-    stream_fetch<ShQkv, ShWo>(wq, pre, cur, nxt, j, lane);
+    stream_fetch<ShQkv, NoPhase>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
@@ -1032,6 +1031,11 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
     qkv_phase<0>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
   else
     qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
+  // the output projection's look-ahead, issued after the two Q / K / V variants
+  // join (loads issued inside them would land in registers that differ between
+  // the variants, and the copies at the join would wait for them); it arrives
+  // during the attention
+  seg_prime<ShWo>(pre, so, otid() % WAVE);
   __syncthreads();
   if (A.dh == 64)
     attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
