@@ -49,7 +49,7 @@ constexpr int NT = 256;          // threads (4 waves)
 constexpr int XLD = DM + 8;      // Xs row stride (bf16 elements)
 constexpr int QLD = 64 + 8;      // Qs / Ks / Os row stride (one 64-dim head group)
 constexpr int VLD = BT + 8;      // Vts row stride
-constexpr int FC = 128;          // FFN hidden units per chunk
+constexpr int FC = 256;          // FFN hidden units per chunk
 constexpr int HLD = FC + 8;      // Hs row stride
 constexpr int MAX_LAYERS = 8;
 constexpr int KIN = 256;         // packed width of the token half of W_in (d zero-padded)
@@ -65,8 +65,11 @@ constexpr int SC_BYTES = 2 * QS_BYTES + VS_BYTES;      // 54272
 constexpr int CS_BYTES = QS_BYTES + VS_BYTES;          // 35840: cached K / V^T chunk
 constexpr int LDS_BYTES = XS_BYTES + SC_BYTES + CS_BYTES;
 static_assert(LDS_BYTES <= 163840, "fused encoder exceeds the 160 KiB of LDS");
-static_assert(BT * HLD * 2 <= SC_BYTES, "FFN chunk does not fit the scratch region");
-static_assert(BT * HLD * 2 + 3 * DM * 4 <= SC_BYTES, "LayerNorm 2 parameters do not fit");
+// During the FFN the hidden chunk fills the scratch region and runs on into the
+// (then free) cache staging area, followed by the second LayerNorm's parameters;
+// the first-layer biases sit at the end of the staging area.
+constexpr int B1_OFF = CS_BYTES - MAX_FFN * 4;   // first-layer biases, from Kc
+static_assert(BT * HLD * 2 + 3 * DM * 4 <= SC_BYTES + B1_OFF, "FFN chunk buffers do not fit");
 static_assert(2 * BT * 4 * 4 <= QS_BYTES && (3 * DM + MAX_FFN) * 4 <= CS_BYTES,
               "LayerNorm 1 and first-layer bias buffers do not fit");
 static_assert(BT * 8 + BT * 8 <= SC_BYTES, "encoding buffers do not fit");
@@ -203,6 +206,7 @@ using ShF1 = Shape<2, DM / 16>;         // W_1 rows of one hidden chunk
 // the two FFN phases is the same (each loads half of its own weights and half of
 // the other's)
 using ShF2 = Shape<2, FC / 16, FC / 32>;
+static_assert(ShF1::D == DM / 32, "FFN look-ahead balance");
 using ShPool = Shape<2, DM / 16>;       // W_pool
 
 struct WSeg {                            // a phase's weight fragments (all wave-uniform)
@@ -229,9 +233,10 @@ __device__ __forceinline__ void seg_prime(Pre& pre, const WSeg& s, int lane) {
 __device__ __forceinline__ WSeg seg_resid(int P, int nkb, int kb0, int w) {
   return WSeg{P, nkb, kb0, 2 * w, 2 * w + 1, 0, 0};
 }
-// FFN first layer, chunk c: hidden row tiles 4c + 2(w & 1) + 0..1
+// FFN first layer, chunk c: hidden row tiles (FC / 32) c + 2w + 0..1
 __device__ __forceinline__ WSeg seg_ffn1(int P, int c, int w) {
-  const int r = c * (FC / 32) + 2 * (w & 1);
+  static_assert(FC == 4 * 64, "one pair of hidden tiles per wave");
+  const int r = c * (FC / 32) + 2 * w;
   return WSeg{P, DM / 16, 0, r, r + 1, 0, 0};
 }
 // Q / K / V of head group g: column tiles 3(w >> 1) + 0..2 of [q0 q1 k0 k1 v0 v1]
@@ -938,10 +943,11 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
   }
 }
 
-// FFN first layer, chunk c: H^T = ReLU(W_1[chunk] Xs^T + b_1) into Hs (wave w:
-// hidden tiles 2(w & 1) + {0,1}, token tiles 2(w >> 1) + {0,1}).  The
-// accumulators start at the chunk's biases b1c (in LDS); ReLU acts on the packed bf16 pairs (for bf16 bit patterns the signed
-// 16-bit max with zero is exactly ReLU, and rounding commutes with it).
+// FFN first layer, chunk c: H^T = ReLU(W_1[chunk] Xs^T + b_1) into Hs; wave w
+// computes hidden tiles 2w, 2w + 1 of the chunk for all 4 token tiles, so each
+// weight fragment is loaded by one wave.  The accumulators start at the chunk's
+// biases b1c (in LDS); ReLU acts on the packed bf16 pairs (for bf16 bit patterns
+// the signed 16-bit max with zero is exactly ReLU, and rounding commutes with it).
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t relu2(uint32_t x) {
   return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, x), s16x2{0, 0}));
@@ -949,34 +955,35 @@ __device__ __forceinline__ uint32_t relu2(uint32_t x) {
 __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
                                            const float* b1c, const bf16_t* Xs, bf16_t* Hs) {
   FZ_LANE_VARS
-  constexpr int NKB = DM / 16;
-  const int hp = w & 1, tp = w >> 1;
-  f32x16 ha[2][2];
+  constexpr int NKB = ShF1::NKB;
+  f32x16 ha[2][4];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const float4 b4 = *reinterpret_cast<const float4*>(b1c + (2 * hp + t) * 32 + 8 * j + 4 * hf);
+      const float4 b4 = *reinterpret_cast<const float4*>(b1c + (2 * w + t) * 32 + 8 * j + 4 * hf);
       const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) ha[t][0][4 * j + i] = ha[t][1][4 * j + i] = bb[i];
+      for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ha[t][tt][4 * j + i] = bb[i];
     }
   bf16x8 wq[NKB][2];
-  bf16x8 xq[NKB][2];
-  const bf16_t* arow = Xs + (tp * 64 + l32) * XLD + 8 * hf;
-  xq[0][0] = lfrag(arow);
-  xq[0][1] = lfrag(arow + 32 * XLD);
+  bf16x8 xq[NKB][4];
+  const bf16_t* arow = Xs + l32 * XLD + 8 * hf;
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt) xq[0][tt] = lfrag(arow + 32 * tt * XLD);
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
     if (j + 1 < NKB) {
-      xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
-      xq[j + 1][1] = lfrag(arow + 32 * XLD + (j + 1) * 16);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) xq[j + 1][tt] = lfrag(arow + 32 * tt * XLD + (j + 1) * 16);
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const bf16x8 a = stream_frag<ShF1>(wq, pre, j, t);
-      ha[t][0] = mfma32(a, xq[j][0], ha[t][0]);
-      ha[t][1] = mfma32(a, xq[j][1], ha[t][1]);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) ha[t][tt] = mfma32(a, xq[j][tt], ha[t][tt]);
     }
     stream_fetch<ShF1, ShF2>(wq, pre, cur, nxt, j, lane);
     sched_fence();
@@ -984,13 +991,13 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+    for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int hid = (2 * hp + t) * 32 + 8 * j + 4 * hf;
-        *reinterpret_cast<uint2*>(Hs + ((2 * tp + u) * 32 + l32) * HLD + hid) =
-            make_uint2(relu2(pack2(ha[t][u][4 * j], ha[t][u][4 * j + 1])),
-                       relu2(pack2(ha[t][u][4 * j + 2], ha[t][u][4 * j + 3])));
+        const int hid = (2 * w + t) * 32 + 8 * j + 4 * hf;
+        *reinterpret_cast<uint2*>(Hs + (tt * 32 + l32) * HLD + hid) =
+            make_uint2(relu2(pack2(ha[t][tt][4 * j], ha[t][tt][4 * j + 1])),
+                       relu2(pack2(ha[t][tt][4 * j + 2], ha[t][tt][4 * j + 3])));
       }
 }
 
@@ -1053,7 +1060,7 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
     resid_phase<ShWo, ShF1>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
     if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
     ln_params_store(q, reinterpret_cast<float*>(Kc));
-    ffn_bias_store(fb, reinterpret_cast<float*>(Kc) + 3 * DM, A.ffn);
+    ffn_bias_store(fb, reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(Kc) + B1_OFF), A.ffn);
   }
   __syncthreads();   // Qs (O) and Ks / Vts are rewritten by the next group
 }
@@ -1070,7 +1077,7 @@ __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_lay
   attention_group<true>(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep, DM / 64 - 1);
 }
 
-// FFN sublayer: per chunk of 128 hidden units, H^T into LDS, then
+// FFN sublayer: per chunk of FC hidden units, H^T into LDS, then
 // acc += W_2[:, chunk] H^T.  The stream enters primed with chunk 0 and leaves
 // primed with `after`: the next layer's first Q / K / V phase, or (last layer)
 // the pooling projection (shape After).  The first-layer biases are in LDS at
@@ -1127,6 +1134,7 @@ __device__ __forceinline__ void encoder_layer(const Args& A, int li, f32x16 (&ac
   float* red = reinterpret_cast<float*>(Sc);                     // reductions
   float* lnp1 = reinterpret_cast<float*>(Kc);                    // LayerNorm 1 parameters
   float* lnp2 = reinterpret_cast<float*>(Sc + BT * HLD * 2);     // LayerNorm 2 parameters
+  const float* b1s = reinterpret_cast<const float*>(smem + XS_BYTES + SC_BYTES + B1_OFF);
   // layer records are read through the kernel-argument segment so the runtime
   // layer index stays a scalar load instead of a private copy of the array
   const tav2_layer L = AK->layers[li];
@@ -1136,11 +1144,9 @@ __device__ __forceinline__ void encoder_layer(const Args& A, int li, f32x16 (&ac
   attention_sublayer(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep);
   layer_norm(acc, lnp1, red, Xs);
   if constexpr (LASTL)
-    ffn_sublayer<ShPool>(A, L, pk, acc, pre, seg_resid(A.pk_pool, DM / 16, 0, w), Xs, Hs,
-                         lnp1 + 3 * DM);
+    ffn_sublayer<ShPool>(A, L, pk, acc, pre, seg_resid(A.pk_pool, DM / 16, 0, w), Xs, Hs, b1s);
   else
-    ffn_sublayer<ShQkv>(A, L, pk, acc, pre, seg_qkv(AK->pk[li + 1].qkv, 0, w), Xs, Hs,
-                        lnp1 + 3 * DM);
+    ffn_sublayer<ShQkv>(A, L, pk, acc, pre, seg_qkv(AK->pk[li + 1].qkv, 0, w), Xs, Hs, b1s);
   layer_norm(acc, lnp2, red, Xs);
 }
 
