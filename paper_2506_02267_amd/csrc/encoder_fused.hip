@@ -1006,19 +1006,23 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
 __device__ __forceinline__ void cache_store(const Args& A, int g, int p0, const bf16_t* Ks,
                                             const bf16_t* Vts, bf16_t* kc, bf16_t* vc) {
   const int tid = otid();
+  // (offsets in 32 bits: one candidate's cache holds at most DM x 1024 positions)
+  u32x4 kq[4], vq[4];   // all LDS reads first, so the stores go out back to back
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = tid + q * NT;
-    const int r = e >> 3, c = (e & 7) * 8;
-    *reinterpret_cast<u32x4*>(kc + int64_t(p0 + r) * DM + g * 64 + c) =
-        *reinterpret_cast<const u32x4*>(Ks + r * QLD + c);
+    kq[q] = *reinterpret_cast<const u32x4*>(Ks + (e >> 3) * QLD + (e & 7) * 8);
+    vq[q] = *reinterpret_cast<const u32x4*>(Vts + (e >> 4) * VLD + (e & 15) * 8);
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = tid + q * NT;
-    const int r = e >> 4, c = (e & 15) * 8;
-    *reinterpret_cast<u32x4*>(vc + int64_t(g * 64 + r) * A.tpad + p0 + c) =
-        *reinterpret_cast<const u32x4*>(Vts + r * VLD + c);
+    *reinterpret_cast<u32x4*>(kc + ((p0 + (e >> 3)) * DM + g * 64 + (e & 7) * 8)) = kq[q];
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = tid + q * NT;
+    *reinterpret_cast<u32x4*>(vc + ((g * 64 + (e >> 4)) * A.tpad + p0 + (e & 15) * 8)) = vq[q];
   }
 }
 
