@@ -36,6 +36,8 @@
 //  * Global loads complete in issue order, so loads whose data is needed soon are
 //    issued before the weight look-ahead of the next phase (biases, LayerNorm
 //    parameters, table rows), and stores of the K/V cache after it.
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 #include "token_source.h"
@@ -56,7 +58,7 @@ constexpr int KIN = 256;         // packed width of the token half of W_in (d ze
 constexpr int N_ACT = 8;         // action-type table rows (types are clamped to 0..7)
 constexpr int N_TIME = 64;       // time-bucket table rows (buckets are clamped to 0..63)
 constexpr int AT_COLS = 80;      // packed [E_act^T | 0 | E_time^T] columns: 0..7, 16..79
-constexpr int MAX_FFN = 4096;    // largest d_ffn (its first-layer biases are staged in LDS)
+constexpr int NKB_W = DM / 16 + 1;   // k-blocks per packed row of W_qkv, W_o, W_1: 16 + bias
 
 constexpr int XS_BYTES = BT * XLD * 2;                 // 67584
 constexpr int QS_BYTES = BT * QLD * 2;                 // 18432
@@ -66,12 +68,9 @@ constexpr int CS_BYTES = QS_BYTES + VS_BYTES;          // 35840: cached K / V^T 
 constexpr int LDS_BYTES = XS_BYTES + SC_BYTES + CS_BYTES;
 static_assert(LDS_BYTES <= 163840, "fused encoder exceeds the 160 KiB of LDS");
 // During the FFN the hidden chunk fills the scratch region and runs on into the
-// (then free) cache staging area, followed by the second LayerNorm's parameters;
-// the first-layer biases sit at the end of the staging area.
-constexpr int B1_OFF = CS_BYTES - MAX_FFN * 4;   // first-layer biases, from Kc
-static_assert(BT * HLD * 2 + 3 * DM * 4 <= SC_BYTES + B1_OFF, "FFN chunk buffers do not fit");
-static_assert(2 * BT * 4 * 4 <= QS_BYTES && (3 * DM + MAX_FFN) * 4 <= CS_BYTES,
-              "LayerNorm 1 and first-layer bias buffers do not fit");
+// (then free) cache staging area, followed by the second LayerNorm's parameters.
+static_assert(BT * HLD * 2 + 2 * DM * 4 <= SC_BYTES + CS_BYTES, "FFN chunk buffers do not fit");
+static_assert(2 * BT * 4 * 4 <= QS_BYTES && 2 * DM * 4 <= CS_BYTES, "LayerNorm 1 buffers do not fit");
 static_assert(BT * 8 + BT * 8 <= SC_BYTES, "encoding buffers do not fit");
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -104,6 +103,12 @@ __device__ __forceinline__ void st4(bf16_t* p, float a, float b, float c, float 
   *reinterpret_cast<uint2*>(p) = make_uint2(pack2(a, b), pack2(c, d));
 }
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+// MFMA operand with bf16 1.0 at k-rows 0 and 1 of every row / column (lanes 0..31
+// hold k-rows 0..7): multiplies a bias k-block fragment [b_hi, b_lo, 0 ...].
+__device__ __forceinline__ bf16x8 bias_ones() {
+  const unsigned v = (otid() % WAVE) < 32 ? 0x3F803F80u : 0u;
+  return __builtin_bit_cast(bf16x8, u32x4{v, 0u, 0u, 0u});
+}
 
 // Partner values across lane halves without LDS: the gfx950 permlane swaps of a
 // register with itself leave {v[l], v[l ^ 32]} (or {v[l], v[l ^ 16]}) in the pair.
@@ -128,11 +133,11 @@ __device__ __forceinline__ float xsum16(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-struct LayerPk {        // first fragment of each packed matrix
-  int qkv;              // [768 rows][16 kb]
-  int o;                // [256][16]
-  int w1;               // [ffn][16]
-  int w2;               // [256][ffn / 16]
+struct LayerPk {        // first fragment of each packed matrix (last k-block: bias)
+  int qkv;              // [768 rows][16 + 1 kb]
+  int o;                // [256][16 + 1]
+  int w1;               // [ffn][16 + 1]
+  int w2;               // [256][ffn / 16 + 1]
 };
 
 struct Args {
@@ -152,7 +157,7 @@ struct Args {
   int pk_at;                // packed [E_act^T | E_time^T], [256][AT_COLS / 16]
   int pk_pos;               // packed E_pos^T, [256][pos_nkb]
   int pos_nkb;
-  tav2_layer layers[MAX_LAYERS];   // biases and LayerNorm vectors
+  tav2_layer layers[MAX_LAYERS];   // LayerNorm vectors (biases are packed)
   LayerPk pk[MAX_LAYERS];
   int n_layers;
   int d;
@@ -189,9 +194,11 @@ typedef bf16x8 Pre[NSLOT];
 constexpr int default_depth(int nr, int nkb) {
   return nr == 0 ? 0 : (NSLOT / nr < nkb ? NSLOT / nr : nkb);
 }
-template <int NR_, int NKB_, int D_ = default_depth(NR_, NKB_)>
+template <int NR_, int NKB_, int D_ = default_depth(NR_, NKB_), bool BIAS_ = false>
 struct Shape {
   static constexpr int NR = NR_, NKB = NKB_, D = D_;
+  static constexpr bool BIAS = BIAS_;      // the last k-block is a bias k-block
+  static constexpr int NX = NKB - BIAS;    // k-blocks of activations
   static constexpr int U = D * NR;
   static_assert(U <= NSLOT && D <= NKB, "look-ahead");
 };
@@ -199,13 +206,19 @@ using NoPhase = Shape<0, 0>;
 using ShEmb = Shape<2, KIN / 16>;       // token half of W_in
 using ShTab = Shape<2, AT_COLS / 16>;   // [E_act | E_time]
 using ShPos = Shape<2, BT / 16>;        // E_pos rows of the block's positions
-using ShQkv = Shape<3, DM / 16>;        // Q / K / V of one head group
-using ShWo = Shape<2, 64 / 16>;         // W_o columns of one head group
-using ShF1 = Shape<2, DM / 16>;         // W_1 rows of one hidden chunk
+// Phases whose last k-block is the bias k-block of their matrix: weight fragment
+// = [b_hi, b_lo, 0 ...] per row (the two bf16 halves of the fp32 bias), times
+// the constant operand bias_ones() (1.0 at k-rows 0 and 1), so the MFMA adds the
+// bias to every token's accumulator.
+using ShQkv = Shape<3, NKB_W, default_depth(3, NKB_W), true>;   // Q / K / V of one head group
+using ShWo = Shape<2, 64 / 16>;                                 // W_o columns of one head group
+using ShWoL = Shape<2, 64 / 16 + 1, default_depth(2, 5), true>;  // ... of the last one
+using ShF1 = Shape<2, NKB_W, default_depth(2, NKB_W), true>;    // W_1 rows of one hidden chunk
 // W_2 columns of one hidden chunk: half of it ahead, so that the L2 traffic of
 // the two FFN phases is the same (each loads half of its own weights and half of
 // the other's)
 using ShF2 = Shape<2, FC / 16, FC / 32>;
+using ShF2L = Shape<2, FC / 16 + 1, FC / 32, true>;   // ... of the last hidden chunk
 static_assert(ShF1::D == DM / 32, "FFN look-ahead balance");
 using ShPool = Shape<2, DM / 16>;       // W_pool
 
@@ -237,7 +250,7 @@ __device__ __forceinline__ WSeg seg_resid(int P, int nkb, int kb0, int w) {
 __device__ __forceinline__ WSeg seg_ffn1(int P, int c, int w) {
   static_assert(FC == 4 * 64, "one pair of hidden tiles per wave");
   const int r = c * (FC / 32) + 2 * w;
-  return WSeg{P, DM / 16, 0, r, r + 1, 0, 0};
+  return WSeg{P, NKB_W, 0, r, r + 1, 0, 0};
 }
 // Q / K / V of head group g: column tiles 3(w >> 1) + 0..2 of [q0 q1 k0 k1 v0 v1]
 // are packed row tiles 8 part + 2g + dt
@@ -248,7 +261,7 @@ __device__ __forceinline__ WSeg seg_qkv(int P, int g, int w) {
     const int ct = 3 * (w >> 1) + t;
     r[t] = 8 * (ct >> 1) + 2 * g + (ct & 1);
   }
-  return WSeg{P, DM / 16, 0, r[0], r[1], r[2], 0};
+  return WSeg{P, NKB_W, 0, r[0], r[1], r[2], 0};
 }
 
 // Iteration of phase Cur after whose MFMAs slot i of the next phase's look-ahead
@@ -303,9 +316,12 @@ __device__ __forceinline__ void resid_phase(f32x16 (&acc)[2][4], Pre& pre, const
   for (int tt = 0; tt < 4; ++tt) xq[0][tt] = lfrag(arow + 32 * tt * ald);
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
-    if (j + 1 < NKB) {
+    if (j + 1 < Cur::NX) {
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) xq[j + 1][tt] = lfrag(arow + 32 * tt * ald + (j + 1) * 16);
+    } else if (j + 1 < NKB) {   // the bias k-block
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) xq[j + 1][tt] = bias_ones();
     }
 #pragma unroll
     for (int ft = 0; ft < 2; ++ft) {
@@ -385,53 +401,29 @@ __device__ __forceinline__ void pos_phase(f32x16 (&acc)[2][4], Pre& pre, const W
 }
 
 // ---------------------------------------------------------------- LayerNorm
-// The sublayer's bias, gain and offset (3 x DM floats) reach LDS through
-// registers: each thread loads its three values before the sublayer's last GEMM
-// phase and stores them after it, so the loads are older than that phase's
-// look-ahead loads of the next weights and waiting for them never waits for the
-// weight stream (vector memory loads complete in issue order).
+// The sublayer's gain and offset (2 x DM floats) reach LDS through registers:
+// each thread loads its two values before the sublayer's last GEMM phase and
+// stores them after it, so the loads are older than that phase's look-ahead
+// loads of the next weights and waiting for them never waits for the weight
+// stream (vector memory loads complete in issue order).  (The sublayer's output
+// bias is already in the accumulators: every packed matrix ends with a bias
+// k-block.)
 struct LnParams {
-  float bias, gain, off;
+  float gain, off;
 };
-// The FFN's first-layer biases (up to 4096) go to LDS the same way, with the
-// first LayerNorm's parameters.
-struct FfnBias {
-  float4 v[4];
-};
-static_assert(MAX_FFN == 4 * 4 * NT, "first-layer bias staging: 4 float4 per thread");
-__device__ __forceinline__ FfnBias ffn_bias_load(const float* b_1, int ffn) {
+static_assert(NT == DM, "one LayerNorm parameter pair per thread");
+__device__ __forceinline__ LnParams ln_params_load(const float* g, const float* b) {
   const int t = otid();
-  FfnBias q;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int e = 4 * (t + i * NT);
-    q.v[i] = e < ffn ? *reinterpret_cast<const float4*>(b_1 + e) : make_float4(0.f, 0.f, 0.f, 0.f);
-  }
-  return q;
-}
-__device__ __forceinline__ void ffn_bias_store(const FfnBias& q, float* P, int ffn) {
-  const int t = otid();
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int e = 4 * (t + i * NT);
-    if (e < ffn) *reinterpret_cast<float4*>(P + e) = q.v[i];
-  }
-}
-static_assert(NT == DM, "one LayerNorm parameter triple per thread");
-__device__ __forceinline__ LnParams ln_params_load(const float* bias, const float* g,
-                                                   const float* b) {
-  const int t = otid();
-  return LnParams{bias[t], g[t], b[t]};
+  return LnParams{g[t], b[t]};
 }
 __device__ __forceinline__ void ln_params_store(const LnParams& q, float* P) {
   const int t = otid();
-  P[t] = q.bias;
-  P[DM + t] = q.gain;
-  P[2 * DM + t] = q.off;
+  P[t] = q.gain;
+  P[DM + t] = q.off;
 }
 
-// x <- LN(acc + bias) with gain g and offset b over the 256 features of every
-// token, with P = [bias | g | b] in LDS; Xs <- bf16(x).  Each wave holds 64
+// x <- LN(acc) with gain g and offset b over the 256 features of every token,
+// with P = [g | b] in LDS; Xs <- bf16(x).  Each wave holds 64
 // features of every token: per-token partial sums meet in LDS (red: [BT][4] sums,
 // then [BT][4] sums of squares).  Ends with a barrier.
 __device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][4], const float* P, float* red,
@@ -441,18 +433,13 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][4], const float* P, 
 #pragma unroll
   for (int ft = 0; ft < 2; ++ft)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float4 bi = *reinterpret_cast<const float4*>(P + 64 * w + ft * 32 + 8 * j + 4 * hf);
+    for (int r = 0; r < 16; ++r)
 #pragma unroll
-      for (int tt = 0; tt < 4; ++tt) {   // (the biased values are formed again below)
-        const float v0 = acc[ft][tt][4 * j] + bi.x;
-        const float v1 = acc[ft][tt][4 * j + 1] + bi.y;
-        const float v2 = acc[ft][tt][4 * j + 2] + bi.z;
-        const float v3 = acc[ft][tt][4 * j + 3] + bi.w;
-        s[tt] += (v0 + v1) + (v2 + v3);
-        ss[tt] += (v0 * v0 + v1 * v1) + (v2 * v2 + v3 * v3);
+      for (int tt = 0; tt < 4; ++tt) {
+        const float v = acc[ft][tt][r];
+        s[tt] += v;
+        ss[tt] = fmaf(v, v, ss[tt]);
       }
-    }
 #pragma unroll
   for (int tt = 0; tt < 4; ++tt) {   // both lane halves end with the full sums
     s[tt] = xsum32(s[tt]);
@@ -478,15 +465,14 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][4], const float* P, 
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int f = 64 * w + ft * 32 + 8 * j + 4 * hf;
-      const float4 bi = *reinterpret_cast<const float4*>(P + f);
-      const float4 gg = *reinterpret_cast<const float4*>(P + DM + f);
-      const float4 bb = *reinterpret_cast<const float4*>(P + 2 * DM + f);
+      const float4 gg = *reinterpret_cast<const float4*>(P + f);
+      const float4 bb = *reinterpret_cast<const float4*>(P + DM + f);
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) {
-        const float v0 = fmaf(fmaf(acc[ft][tt][4 * j] + bi.x, rstd[tt], shift[tt]), gg.x, bb.x);
-        const float v1 = fmaf(fmaf(acc[ft][tt][4 * j + 1] + bi.y, rstd[tt], shift[tt]), gg.y, bb.y);
-        const float v2 = fmaf(fmaf(acc[ft][tt][4 * j + 2] + bi.z, rstd[tt], shift[tt]), gg.z, bb.z);
-        const float v3 = fmaf(fmaf(acc[ft][tt][4 * j + 3] + bi.w, rstd[tt], shift[tt]), gg.w, bb.w);
+        const float v0 = fmaf(fmaf(acc[ft][tt][4 * j], rstd[tt], shift[tt]), gg.x, bb.x);
+        const float v1 = fmaf(fmaf(acc[ft][tt][4 * j + 1], rstd[tt], shift[tt]), gg.y, bb.y);
+        const float v2 = fmaf(fmaf(acc[ft][tt][4 * j + 2], rstd[tt], shift[tt]), gg.z, bb.z);
+        const float v3 = fmaf(fmaf(acc[ft][tt][4 * j + 3], rstd[tt], shift[tt]), gg.w, bb.w);
         acc[ft][tt][4 * j] = v0;
         acc[ft][tt][4 * j + 1] = v1;
         acc[ft][tt][4 * j + 2] = v2;
@@ -860,27 +846,11 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
 // loop with fixed accumulator registers.
 template <int CS>
 __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
-                                          const float* b_qkv, int g, const bf16_t* Xs, bf16_t* Qs,
-                                          bf16_t* Ks, bf16_t* Vts) {
+                                          const bf16_t* Xs, bf16_t* Qs, bf16_t* Ks, bf16_t* Vts) {
   FZ_LANE_VARS
-  constexpr int NKB = DM / 16;
+  constexpr int NKB = ShQkv::NKB;
   constexpr int cs = CS;
   const int tp = w & 1;
-  // epilogue biases, loaded before this phase issues the next phase's weight
-  // loads (vector memory loads complete in order)
-  float4 bq[3][4];
-  float bv[3];
-#pragma unroll
-  for (int t = 0; t < 3; ++t) {
-    const int ct = 3 * cs + t;
-    const float* bias = b_qkv + (ct >> 1) * DM + g * 64 + (ct & 1) * 32;
-    if ((ct >> 1) < 2) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) bq[t][j] = *reinterpret_cast<const float4*>(bias + 8 * j + 4 * hf);
-    } else {
-      bv[t] = bias[l32];
-    }
-  }
   f32x16 qa[3][2];
 #pragma unroll
   for (int t = 0; t < 3; ++t) qa[t][0] = qa[t][1] = f32x16{};
@@ -891,9 +861,11 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
   xq[0][1] = lfrag(arow + 32 * XLD);
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
-    if (j + 1 < NKB) {
+    if (j + 1 < ShQkv::NX) {
       xq[j + 1][0] = lfrag(arow + (j + 1) * 16);
       xq[j + 1][1] = lfrag(arow + 32 * XLD + (j + 1) * 16);
+    } else if (j + 1 < NKB) {   // the bias k-block (also as the A operand of V)
+      xq[j + 1][0] = xq[j + 1][1] = bias_ones();
     }
     if constexpr (CS == 0) {   // q0 q1 k0: transposed
 #pragma unroll
@@ -926,18 +898,14 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
       if (part < 2) {
         bf16_t* dst = part == 0 ? Qs : Ks;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int dim = 8 * j + 4 * hf;
-          const float4 b4 = bq[t][j];
-          st4(dst + (tt * 32 + l32) * QLD + dt * 32 + dim, qa[t][u][4 * j] + b4.x,
-              qa[t][u][4 * j + 1] + b4.y, qa[t][u][4 * j + 2] + b4.z, qa[t][u][4 * j + 3] + b4.w);
-        }
+        for (int j = 0; j < 4; ++j)
+          st4(dst + (tt * 32 + l32) * QLD + dt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j],
+              qa[t][u][4 * j + 1], qa[t][u][4 * j + 2], qa[t][u][4 * j + 3]);
       } else {
-        const float b1 = bv[t];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j] + b1,
-              qa[t][u][4 * j + 1] + b1, qa[t][u][4 * j + 2] + b1, qa[t][u][4 * j + 3] + b1);
+          st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j],
+              qa[t][u][4 * j + 1], qa[t][u][4 * j + 2], qa[t][u][4 * j + 3]);
       }
     }
   }
@@ -945,29 +913,19 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
 
 // FFN first layer, chunk c: H^T = ReLU(W_1[chunk] Xs^T + b_1) into Hs; wave w
 // computes hidden tiles 2w, 2w + 1 of the chunk for all 4 token tiles, so each
-// weight fragment is loaded by one wave.  The accumulators start at the chunk's
-// biases b1c (in LDS); ReLU acts on the packed bf16 pairs (for bf16 bit patterns
-// the signed 16-bit max with zero is exactly ReLU, and rounding commutes with it).
+// weight fragment is loaded by one wave; the last k-block adds the biases.  ReLU
+// acts on the packed bf16 pairs (for bf16 bit patterns the signed 16-bit max with
+// zero is exactly ReLU, and rounding commutes with it).
 typedef short s16x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t relu2(uint32_t x) {
   return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, x), s16x2{0, 0}));
 }
+template <class Nxt>
 __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
-                                           const float* b1c, const bf16_t* Xs, bf16_t* Hs) {
+                                           const bf16_t* Xs, bf16_t* Hs) {
   FZ_LANE_VARS
   constexpr int NKB = ShF1::NKB;
   f32x16 ha[2][4];
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float4 b4 = *reinterpret_cast<const float4*>(b1c + (2 * w + t) * 32 + 8 * j + 4 * hf);
-      const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) ha[t][tt][4 * j + i] = bb[i];
-    }
   bf16x8 wq[NKB][2];
   bf16x8 xq[NKB][4];
   const bf16_t* arow = Xs + l32 * XLD + 8 * hf;
@@ -975,17 +933,21 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
   for (int tt = 0; tt < 4; ++tt) xq[0][tt] = lfrag(arow + 32 * tt * XLD);
 #pragma unroll
   for (int j = 0; j < NKB; ++j) {
-    if (j + 1 < NKB) {
+    if (j + 1 < ShF1::NX) {
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) xq[j + 1][tt] = lfrag(arow + 32 * tt * XLD + (j + 1) * 16);
+    } else if (j + 1 < NKB) {   // the bias k-block
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) xq[j + 1][tt] = bias_ones();
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const bf16x8 a = stream_frag<ShF1>(wq, pre, j, t);
 #pragma unroll
-      for (int tt = 0; tt < 4; ++tt) ha[t][tt] = mfma32(a, xq[j][tt], ha[t][tt]);
+      for (int tt = 0; tt < 4; ++tt)
+        ha[t][tt] = mfma32(a, xq[j][tt], j == 0 ? f32x16{} : ha[t][tt]);
     }
-    stream_fetch<ShF1, ShF2>(wq, pre, cur, nxt, j, lane);
+    stream_fetch<ShF1, Nxt>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
@@ -1037,16 +999,19 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
                                                 bf16_t* Kc, bf16_t* Vc, bf16_t* kc, bf16_t* vc,
                                                 int p0, bool keep, int g) {
   const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
-  const WSeg so = seg_resid(pk.o, DM / 16, 4 * g, w);
+  // (the last group's output projection also adds b_o: its bias k-block follows
+  // the group's 4 k-blocks)
+  using Wo = typename std::conditional<LAST, ShWoL, ShWo>::type;
+  const WSeg so = seg_resid(pk.o, NKB_W, 4 * g, w);
   if (w < 2)
-    qkv_phase<0>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
+    qkv_phase<0>(pre, seg_qkv(pk.qkv, g, w), so, Xs, Qs, Ks, Vts);
   else
-    qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, L.b_qkv, g, Xs, Qs, Ks, Vts);
+    qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, Xs, Qs, Ks, Vts);
   // the output projection's look-ahead, issued after the two Q / K / V variants
   // join (loads issued inside them would land in registers that differ between
   // the variants, and the copies at the join would wait for them); it arrives
   // during the attention
-  seg_prime<ShWo>(pre, so, otid() % WAVE);
+  seg_prime<Wo>(pre, so, otid() % WAVE);
   __syncthreads();
   if (A.dh == 64)
     attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
@@ -1059,12 +1024,10 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
     resid_phase<ShWo, ShQkv>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD);
     if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
   } else {   // the staging area is free now: it receives the LayerNorm parameters
-    const LnParams q = ln_params_load(L.b_o, L.ln1_g, L.ln1_b);   // and the FFN biases
-    const FfnBias fb = ffn_bias_load(L.b_1, A.ffn);
-    resid_phase<ShWo, ShF1>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
+    const LnParams q = ln_params_load(L.ln1_g, L.ln1_b);
+    resid_phase<ShWoL, ShF1>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
     if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
     ln_params_store(q, reinterpret_cast<float*>(Kc));
-    ffn_bias_store(fb, reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(Kc) + B1_OFF), A.ffn);
   }
   __syncthreads();   // Qs (O) and Ks / Vts are rewritten by the next group
 }
@@ -1082,39 +1045,39 @@ __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_lay
 }
 
 // FFN sublayer: per chunk of FC hidden units, H^T into LDS, then
-// acc += W_2[:, chunk] H^T.  The stream enters primed with chunk 0 and leaves
-// primed with `after`: the next layer's first Q / K / V phase, or (last layer)
-// the pooling projection (shape After).  The first-layer biases are in LDS at
-// b1s.  The last chunk is peeled out of the loop (see attention_sublayer).
+// acc += W_2[:, chunk] H^T (the last chunk also adds b_2).  The stream enters
+// primed with chunk 0 and leaves primed with `after`: the next layer's first
+// Q / K / V phase, or (last layer) the pooling projection (shape After).  The
+// last chunk is peeled out of the loop (see attention_sublayer).
 template <bool LAST, class After>
 __device__ __forceinline__ void ffn_chunk(const Args& A, const tav2_layer& L, const LayerPk& pk,
                                           f32x16 (&acc)[2][4], Pre& pre, const WSeg& after,
-                                          const bf16_t* Xs, bf16_t* Hs, const float* b1s, int c) {
+                                          const bf16_t* Xs, bf16_t* Hs, int c) {
+  using F2 = typename std::conditional<LAST, ShF2L, ShF2>::type;
   const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
-  const WSeg s2 = seg_resid(pk.w2, A.ffn / 16, c * (FC / 16), w);
+  const WSeg s2 = seg_resid(pk.w2, A.ffn / 16 + 1, c * (FC / 16), w);
   // last chunk: the LayerNorm parameters are loaded ahead of the first layer's
   // weight loads and go past the hidden chunk before the second layer
   LnParams q;
-  if constexpr (LAST) q = ln_params_load(L.b_2, L.ln2_g, L.ln2_b);
-  ffn1_phase(pre, seg_ffn1(pk.w1, c, w), s2, b1s + c * FC, Xs, Hs);
+  if constexpr (LAST) q = ln_params_load(L.ln2_g, L.ln2_b);
+  ffn1_phase<F2>(pre, seg_ffn1(pk.w1, c, w), s2, Xs, Hs);
   if constexpr (LAST)
     ln_params_store(q, reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(Hs) + BT * HLD * 2));
   __syncthreads();
   if constexpr (!LAST)
-    resid_phase<ShF2, ShF1>(acc, pre, s2, seg_ffn1(pk.w1, c + 1, w), Hs, HLD);
+    resid_phase<F2, ShF1>(acc, pre, s2, seg_ffn1(pk.w1, c + 1, w), Hs, HLD);
   else
-    resid_phase<ShF2, After>(acc, pre, s2, after, Hs, HLD);
+    resid_phase<F2, After>(acc, pre, s2, after, Hs, HLD);
   __syncthreads();   // Hs is rewritten by the next chunk
 }
 template <class After>
 __device__ __forceinline__ void ffn_sublayer(const Args& A, const tav2_layer& L,
                                              const LayerPk& pk, f32x16 (&acc)[2][4], Pre& pre,
-                                             const WSeg& after, bf16_t* Xs, bf16_t* Hs,
-                                             const float* b1s) {
+                                             const WSeg& after, bf16_t* Xs, bf16_t* Hs) {
   const int nch = A.ffn / FC;
   for (int c = 0; c + 1 < nch; ++c)
-    ffn_chunk<false, After>(A, L, pk, acc, pre, after, Xs, Hs, b1s, c);
-  ffn_chunk<true, After>(A, L, pk, acc, pre, after, Xs, Hs, b1s, nch - 1);
+    ffn_chunk<false, After>(A, L, pk, acc, pre, after, Xs, Hs, c);
+  ffn_chunk<true, After>(A, L, pk, acc, pre, after, Xs, Hs, nch - 1);
 }
 
 // One encoder layer of the block: attention, LayerNorm 1, FFN, LayerNorm 2.  The
@@ -1138,7 +1101,6 @@ __device__ __forceinline__ void encoder_layer(const Args& A, int li, f32x16 (&ac
   float* red = reinterpret_cast<float*>(Sc);                     // reductions
   float* lnp1 = reinterpret_cast<float*>(Kc);                    // LayerNorm 1 parameters
   float* lnp2 = reinterpret_cast<float*>(Sc + BT * HLD * 2);     // LayerNorm 2 parameters
-  const float* b1s = reinterpret_cast<const float*>(smem + XS_BYTES + SC_BYTES + B1_OFF);
   // layer records are read through the kernel-argument segment so the runtime
   // layer index stays a scalar load instead of a private copy of the array
   const tav2_layer L = AK->layers[li];
@@ -1148,9 +1110,9 @@ __device__ __forceinline__ void encoder_layer(const Args& A, int li, f32x16 (&ac
   attention_sublayer(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep);
   layer_norm(acc, lnp1, red, Xs);
   if constexpr (LASTL)
-    ffn_sublayer<ShPool>(A, L, pk, acc, pre, seg_resid(A.pk_pool, DM / 16, 0, w), Xs, Hs, b1s);
+    ffn_sublayer<ShPool>(A, L, pk, acc, pre, seg_resid(A.pk_pool, DM / 16, 0, w), Xs, Hs);
   else
-    ffn_sublayer<ShQkv>(A, L, pk, acc, pre, seg_qkv(AK->pk[li + 1].qkv, 0, w), Xs, Hs, b1s);
+    ffn_sublayer<ShQkv>(A, L, pk, acc, pre, seg_qkv(AK->pk[li + 1].qkv, 0, w), Xs, Hs);
   layer_norm(acc, lnp2, red, Xs);
 }
 
@@ -1263,8 +1225,10 @@ __global__ __launch_bounds__(DM) void cand_proj_kernel(const bf16_t* __restrict_
 // ---------------------------------------------------------------- weight packing
 // Rewrites a row-major [rows x K] bf16 matrix (row stride ld, columns >= kvalid
 // read as zero) into MFMA-fragment order: fragment (rt, kb) is 1 KB at
-// ((rt * K/16) + kb) * 512 elements, lane l holding row 32 rt + l % 32, columns
-// 16 kb + 8 (l / 32) .. +7.
+// ((rt * nkb) + kb) * 512 elements, lane l holding row 32 rt + l % 32, columns
+// 16 kb + 8 (l / 32) .. +7.  A bias job writes the bias k-block of a matrix
+// instead: columns 0 and 1 of row r hold the bf16 value nearest to bias[r] and
+// the bf16 value nearest to the remainder, the other columns zero.
 struct PackJob {
   const bf16_t* src;
   bf16_t* dst;       // first fragment of the destination matrix
@@ -1274,9 +1238,10 @@ struct PackJob {
   int ld;            // source row stride (elements)
   int kvalid;        // job columns >= kvalid are zero
   int trans;         // destination (row r, job column k) = src[k * ld + r] instead of src[r * ld + k]
+  const float* bias; // non-null: a bias job (one k-block)
   int64_t first;     // first item (16-byte piece) of this job
 };
-constexpr int MAX_JOBS = 4 + 4 * MAX_LAYERS;
+constexpr int MAX_JOBS = 4 + 8 * MAX_LAYERS;
 struct PackArgs {
   PackJob job[MAX_JOBS];
   int njobs;
@@ -1295,7 +1260,14 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(PackArgs P) {
   const int rt = int(frag / J.nkbj), kbj = int(frag % J.nkbj);
   const int row = rt * 32 + lane % 32, col = kbj * 16 + 8 * (lane / 32);   // job column
   uint4 v = make_uint4(0, 0, 0, 0);
-  if (!J.trans) {
+  if (J.bias) {
+    if (lane < 32) {
+      const float b = J.bias[row];
+      const __bf16 hi = static_cast<__bf16>(b);
+      const __bf16 lo = static_cast<__bf16>(b - static_cast<float>(hi));
+      v.x = uint32_t(__builtin_bit_cast(uint16_t, hi)) | (uint32_t(__builtin_bit_cast(uint16_t, lo)) << 16);
+    }
+  } else if (!J.trans) {
     if (col < J.kvalid) v = *reinterpret_cast<const uint4*>(J.src + int64_t(row) * J.ld + col);
   } else {
     bf16_t x[8];
@@ -1332,7 +1304,8 @@ int pos_cols(const tav2_weights& w) { return (w.max_pos + fz::BT - 1) / fz::BT *
 
 size_t packed_bytes(const tav2_weights& w) {
   const size_t dm = fz::DM, ff = size_t(w.d_ffn);
-  const size_t per_layer = 3 * dm * dm + dm * dm + ff * dm + dm * ff;
+  // W_qkv, W_o, W_1 with a bias k-block after their dm columns, W_2 after its ff
+  const size_t per_layer = (3 * dm + dm + ff) * (dm + 16) + dm * (ff + 16);
   const size_t tables = dm * (fz::AT_COLS + size_t(pos_cols(w)));
   return align_up((dm * fz::KIN + dm * dm + size_t(w.n_layers) * per_layer + tables) * 2, 256);
 }
@@ -1373,13 +1346,21 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
     J.ld = ld;
     J.kvalid = kvalid;
     J.trans = trans;
+    J.bias = nullptr;
     J.first = items;
     items += int64_t(rows) * nkbj * 2;   // 16-byte pieces: 2 per row per k-block
   };
-  auto add = [&](const void* srcm, int rows, int K, int ld, int kvalid) {
+  // matrix of rows x K (row-major source), followed by a bias k-block if bias
+  auto add = [&](const void* srcm, int rows, int K, int ld, int kvalid,
+                 const float* bias = nullptr) {
     const size_t mat = off;
-    add_cols(mat, rows, K / 16, 0, K / 16, srcm, ld, kvalid, 0);
-    off += size_t(rows) * K;
+    const int nkb = K / 16 + (bias ? 1 : 0);
+    add_cols(mat, rows, nkb, 0, K / 16, srcm, ld, kvalid, 0);
+    if (bias) {
+      add_cols(mat, rows, nkb, K / 16, 1, nullptr, 0, 0, 0);
+      P.job[P.njobs - 1].bias = bias;
+    }
+    off += size_t(rows) * nkb * 16;
     return int(mat / 512);   // 512 bf16 per fragment; every matrix is whole fragments
   };
   fz::Args a{};
@@ -1389,10 +1370,10 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
   a.pk_pool = add(w.W_pool, dm, dm, dm, dm);
   for (int i = 0; i < w.n_layers; ++i) {
     const tav2_layer& L = w.layers[i];
-    a.pk[i].qkv = add(L.W_qkv, 3 * dm, dm, dm, dm);
-    a.pk[i].o = add(L.W_o, dm, dm, dm, dm);
-    a.pk[i].w1 = add(L.W_1, ff, dm, dm, dm);
-    a.pk[i].w2 = add(L.W_2, dm, ff, ff, ff);
+    a.pk[i].qkv = add(L.W_qkv, 3 * dm, dm, dm, dm, L.b_qkv);
+    a.pk[i].o = add(L.W_o, dm, dm, dm, dm, L.b_o);
+    a.pk[i].w1 = add(L.W_1, ff, dm, dm, dm, L.b_1);
+    a.pk[i].w2 = add(L.W_2, dm, ff, ff, ff, L.b_2);
   }
   // side tables as [feature][row] matrices for the one-hot products of the input
   // encoding: E_act^T in columns 0..7, E_time^T in columns 16..79 (zero without

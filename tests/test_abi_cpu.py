@@ -89,16 +89,16 @@ def test_workspace_queries():
     tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
                    d=64, dtype=T.BF16, reserved=0)
     # fused bf16 encoder: every matrix in fragment order (W_in's token half padded to
-    # 256 columns; the side tables transposed: [E_act | E_time] in 80 columns, E_pos
-    # in max_pos rounded up to 128), the candidate half of the input projection
-    # (fp32 per candidate) and, past one 128-position block, a K / V cache of
-    # layers x 2 x T x d_model bf16
+    # 256 columns; each layer matrix followed by a 16-column bias block; the side
+    # tables transposed: [E_act | E_time] in 80 columns, E_pos in max_pos rounded up
+    # to 128), the candidate half of the input projection (fp32 per candidate) and,
+    # past one 128-position block, a K / V cache of layers x 2 x T x d_model bf16
     dm, ff, layers = 256, 512, 2
 
     def packed(max_pos):
         pos_cols = -(-max_pos // 128) * 128
-        return (dm * 256 + dm * dm + layers * (4 * dm * dm + 2 * ff * dm)
-                + dm * (80 + pos_cols)) * 2
+        per_layer = (3 * dm + dm + ff) * (dm + 16) + dm * (ff + 16)
+        return (dm * 256 + dm * dm + layers * per_layer + dm * (80 + pos_cols)) * 2
 
     cvec = 10 * dm * 4
     assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == packed(64) + cvec
