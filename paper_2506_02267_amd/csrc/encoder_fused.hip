@@ -710,11 +710,14 @@ __device__ __forceinline__ void cache_put(const CacheChunk& ch, bf16_t* Kc, bf16
 // Causal attention of the block's queries for head group g: first the block's
 // own keys (Ks / Vts), then the keys of earlier blocks from the cache, whose
 // first chunk is loaded while the block's own keys are processed (the softmax is
-// independent of the key order).
-template <int DH>
+// independent of the key order).  prime() issues the next weight phase's
+// look-ahead, after the own keys (issued earlier, its registers would be copied
+// around the wave-specific code, and the copies would wait for the loads).
+template <int DH, class Prime>
 __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf16_t* Ks,
                                              const bf16_t* Vts, const bf16_t* kc,
-                                             const bf16_t* vc, int tpad, bf16_t* Kc, bf16_t* Vc) {
+                                             const bf16_t* vc, int tpad, bf16_t* Kc, bf16_t* Vc,
+                                             const Prime& prime) {
   constexpr int NH = 64 / DH;
   const int lane = otid() % WAVE;
   const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
@@ -735,6 +738,7 @@ __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf
       attn_own<DH, 2>(sa, sb, Ks, Vts, hd * DH, lane);
     else
       attn_own<DH, 3>(sa, sb, Ks, Vts, hd * DH, lane);
+    if (hd == NH - 1) prime();
     for (int c0 = 0; c0 < p0; c0 += BT) {     // earlier blocks: every key visible
       if (c0 > 0) cache_load(ch, kc, vc, tpad, g, c0);
       cache_put(ch, Kc, Vc);
@@ -1007,16 +1011,13 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
     qkv_phase<0>(pre, seg_qkv(pk.qkv, g, w), so, Xs, Qs, Ks, Vts);
   else
     qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, Xs, Qs, Ks, Vts);
-  // the output projection's look-ahead, issued after the two Q / K / V variants
-  // join (loads issued inside them would land in registers that differ between
-  // the variants, and the copies at the join would wait for them); it arrives
-  // during the attention
-  seg_prime<Wo>(pre, so, otid() % WAVE);
   __syncthreads();
+  // the output projection's look-ahead is loaded during the attention
+  const auto prime = [&] { seg_prime<Wo>(pre, so, otid() % WAVE); };
   if (A.dh == 64)
-    attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
+    attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc, prime);
   else
-    attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc);
+    attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc, prime);
   __syncthreads();
   // the cache stores follow the phase's weight loads, so the next phase's first
   // wait on its weights does not also wait for the stores
