@@ -164,6 +164,117 @@ __device__ __forceinline__ void block_excl_scan(const uint64_t (&v)[NV], uint64_
   }
 }
 
+// Sampled threshold (the common case, exact result): a threshold t taken from a
+// strided sample of the keys (its r-th largest, cut to its top 16 bits, r a few
+// standard deviations above the expected number of sampled keys among the kk
+// largest) usually leaves between kk and TK_CAP keys >= t.  Those are compacted
+// into LDS as unique 48-bit values (key, 0xFFFF - row), whose kk-th largest is
+// found exactly by an 8-bit-per-pass radix select; every value at or above it is
+// one of the kk selected keys (ties between equal scores go to the lower row, as
+// in the exhaustive search).  Returns false (block-uniform) when the sample does
+// not give such a threshold, leaving the exhaustive search to the caller.
+constexpr int TK_CAP = 2048;
+template <int PT>
+__device__ bool topk_sampled(const uint32_t (&key)[PT], int kk, uint64_t* cand, uint32_t* hist,
+                             int* red, uint64_t* scan_w, uint64_t* sel, int* misc, int tid,
+                             int lane, int wid) {
+  constexpr int NC = PT / 4, CH = TK_THREADS * 4, NW = TK_THREADS / WAVE;
+  static_assert(NC >= 4, "four sample chunks per thread");
+  // sample: the first key of chunks 0, NC/4, NC/2, 3NC/4 of every thread (4 of PT)
+  const float expct = float(kk) * 4.f / float(PT);
+  const int r = int(expct + 4.f * sqrtf(expct) + 8.f);
+  if (r >= TK_THREADS * 2) return false;
+  uint32_t smp[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) smp[i] = key[4 * (i * NC / 4)];
+  uint32_t thr = 0;
+  for (int b = 31; b >= 16; --b) {
+    const uint32_t probe = thr | (1u << b);
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cnt += __popcll(__builtin_amdgcn_ballot_w64(smp[i] >= probe));
+    if (lane == 0) red[(b & 1) * NW + wid] = cnt;
+    __syncthreads();
+    int tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) tot += red[(b & 1) * NW + w];
+    if (tot >= r) thr = probe;
+  }
+  // keys >= thr: count, then compact
+  uint64_t c[1] = {0}, excl[1], total[1];
+#pragma unroll
+  for (int j = 0; j < PT; ++j) c[0] += key[j] >= thr ? 1u : 0u;
+  block_excl_scan<1>(c, excl, total, scan_w, lane, wid);
+  const int clo = int(total[0]);
+  if (clo < kk || clo > TK_CAP) return false;
+  int pos = int(excl[0]);
+#pragma unroll
+  for (int q = 0; q < NC; ++q)
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (key[4 * q + u] >= thr)
+        cand[pos++] = (uint64_t(key[4 * q + u]) << 16) | uint64_t(0xFFFFu - uint32_t(q * CH + tid * 4 + u));
+  // radix select of the kk-th largest 48-bit value, most significant byte first
+  uint64_t pre = 0;
+  int need = kk;
+  for (int sh = 40; sh >= 0; sh -= 8) {
+    if (tid < 256) hist[tid] = 0;
+    __syncthreads();   // (also publishes cand before the first pass)
+    for (int i = tid; i < clo; i += TK_THREADS) {
+      const uint64_t v = cand[i];
+      if ((v >> (sh + 8)) == pre) atomicAdd(&hist[(v >> sh) & 255u], 1u);
+    }
+    __syncthreads();
+    if (wid == 0) {   // bins in descending order: lane l holds 255 - 4l - q
+      uint32_t h[4], sum = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        h[q] = hist[255 - 4 * lane - q];
+        sum += h[q];
+      }
+      uint32_t incl = sum;
+#pragma unroll
+      for (int o = 1; o < WAVE; o <<= 1) {
+        const uint32_t t = __shfl_up(incl, o, WAVE);
+        if (lane >= o) incl += t;
+      }
+      const uint32_t before = incl - sum;   // values in higher bins
+      if (before < uint32_t(need) && uint32_t(need) <= incl) {
+        uint32_t cum = before;
+        int digit = 0, rest = 0;
+        bool hit = false;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (!hit && cum + h[q] >= uint32_t(need)) {
+            hit = true;
+            digit = 255 - 4 * lane - q;
+            rest = need - int(cum);
+          }
+          cum += h[q];
+        }
+        misc[0] = digit;
+        misc[1] = rest;
+      }
+    }
+    __syncthreads();
+    pre = (pre << 8) | uint64_t(misc[0]);
+    need = misc[1];
+    __syncthreads();   // misc and hist are rewritten by the next pass
+  }
+  // exactly kk values are >= pre; their order is set by the caller's rank sort
+  if (tid == 0) misc[2] = 0;
+  __syncthreads();
+  for (int i = tid; i < clo; i += TK_THREADS) {
+    const uint64_t v = cand[i];
+    if (v >= pre) {
+      const uint32_t kv = uint32_t(v >> 16), row = 0xFFFFu - uint32_t(v & 0xFFFFu);
+      sel[atomicAdd(&misc[2], 1)] = (uint64_t(kv) << 32) | uint64_t(0xFFFFFFFFu - row);
+    }
+  }
+  __syncthreads();
+  return true;
+}
+
 template <int PT>
 __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     const float* __restrict__ scores, int64_t ld, const int64_t* __restrict__ cand_off,
@@ -172,6 +283,9 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
   __shared__ int red[2][TK_THREADS / WAVE];
   __shared__ uint64_t scan_w[(TK_THREADS / WAVE) * 5];
   __shared__ uint64_t sel[TAV2_K_MAX];
+  __shared__ uint64_t cand[PT >= 16 ? TK_CAP : 1];
+  __shared__ uint32_t hist[256];
+  __shared__ int misc[4];
 
   const int r = blockIdx.y;
   const int64_t n = cand_off[r] + blockIdx.x;
@@ -209,7 +323,11 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     }
   }
 
-  // largest threshold t with count(key >= t) >= kk, one bit at a time
+  bool sampled = false;
+  if constexpr (PT >= 16)
+    sampled = topk_sampled<PT>(key, kk, cand, hist, &red[0][0], scan_w, sel, misc, tid, lane, wid);
+  if (!sampled) {
+  // exhaustive: largest threshold t with count(key >= t) >= kk, one bit at a time
   uint32_t thr = 0;
   for (int b = 31; b >= 0; --b) {
     const uint32_t probe = thr | (1u << b);
@@ -265,6 +383,7 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     }
   }
   __syncthreads();
+  }
 
   // survivors are distinct under (key, -row): rank = number of survivors before it
   for (int s = tid; s < kk; s += TK_THREADS) {
