@@ -1,7 +1,8 @@
 """GPU parity of tav2_nn_select (Eq. 3) against the oracle: indices and scores
 bit for bit, on the five workloads (full runs, all or sampled candidates) and
 on edge cases (ragged, empty and short requests, k = 1 and k = K_MAX, heavy
-ties, padded layout, every register-tile size of the top-k kernel)."""
+ties, padded layout, every register-tile size of the top-k kernel, ties inside
+the sampled-threshold path and inputs that make it fall back)."""
 import numpy as np
 import pytest
 import torch
@@ -90,6 +91,38 @@ def test_heavy_ties_and_k_max():
         idx, score = run_select(inp, k)
         ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
         assert_select_equal(idx, score, ref_i, ref_s)
+
+
+@pytest.mark.parametrize("k", [1, 256, 1024])
+def test_sampled_threshold_with_tied_rows(k):
+    # long rows (the top-k takes its threshold from a sample of the keys): every
+    # embedding row appears three times in a row, so ties fall inside the
+    # compacted candidate set and are resolved by row in the radix select
+    inp = custom_inputs([16384, 9000], [5, 4], d=64, levels=8, seed=11)
+    for r0, n in zip(inp.seq.offset, inp.seq.length):
+        e = inp.seq.emb[r0:r0 + n]
+        e[:] = np.repeat(e[0::3], 3, axis=0)[:n]
+    idx, score = run_select(inp, k)
+    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
+    assert_select_equal(idx, score, ref_i, ref_s)
+
+
+@pytest.mark.parametrize("case", ["all_equal", "sample_misses_top"])
+def test_sampled_threshold_falls_back(case):
+    # inputs for which the sample gives no usable threshold: all scores equal (far
+    # more than the candidate capacity at the threshold), or the largest scores
+    # only on rows the sample never looks at (rows = 2 mod 4)
+    inp = custom_inputs([16384], [4], d=32, levels=8, seed=5)
+    e = inp.seq.emb
+    if case == "all_equal":
+        e[:] = e[0]
+    else:
+        e[:] = -np.abs(e)
+        e[2::4] = np.abs(e[2::4]) + 1.0
+        inp.cand[:] = np.abs(inp.cand) + 0.125
+    idx, score = run_select(inp, 512)
+    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, 512)
+    assert_select_equal(idx, score, ref_i, ref_s)
 
 
 def test_zero_scores_are_positive_zero():
