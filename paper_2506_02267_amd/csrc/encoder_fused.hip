@@ -709,15 +709,15 @@ __device__ __forceinline__ void cache_put(const CacheChunk& ch, bf16_t* Kc, bf16
 
 // Causal attention of the block's queries for head group g: first the block's
 // own keys (Ks / Vts), then the keys of earlier blocks from the cache, whose
-// first chunk is loaded while the block's own keys are processed (the softmax is
-// independent of the key order).  prime() issues the next weight phase's
+// first chunk (in ch, loaded by the caller ahead of the group) is staged after the
+// block's own keys are processed (the softmax is independent of the key order).  prime() issues the next weight phase's
 // look-ahead, after the own keys (issued earlier, its registers would be copied
 // around the wave-specific code, and the copies would wait for the loads).
 template <int DH, class Prime>
 __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf16_t* Ks,
                                              const bf16_t* Vts, const bf16_t* kc,
                                              const bf16_t* vc, int tpad, bf16_t* Kc, bf16_t* Vc,
-                                             const Prime& prime) {
+                                             CacheChunk& ch, const Prime& prime) {
   constexpr int NH = 64 / DH;
   const int lane = otid() % WAVE;
   const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
@@ -727,8 +727,7 @@ __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf
     AttnState<DH> sa, sb;
     attn_init<DH>(sa, Qs, hd * DH, qa);
     attn_init<DH>(sb, Qs, hd * DH, qb);
-    CacheChunk ch;
-    if (p0 > 0) cache_load(ch, kc, vc, tpad, g, 0);
+    if (hd > 0 && p0 > 0) cache_load(ch, kc, vc, tpad, g, 0);   // head 0: loaded ahead
     // the block's own keys (one specialisation per wave: its pair counts)
     if (w == 0)
       attn_own<DH, 0>(sa, sb, Ks, Vts, hd * DH, lane);
@@ -748,6 +747,9 @@ __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf
     attn_finish<DH>(sa, Qs, hd * DH, qa);
     attn_finish<DH>(sb, Qs, hd * DH, qb);
   }
+  // the next group's first cached chunk, in flight during this group's output
+  // projection and the next group's Q / K / V
+  if (p0 > 0 && g + 1 < DM / 64) cache_load(ch, kc, vc, tpad, g + 1, 0);
 }
 
 __device__ __forceinline__ int64_t nl_of(const Args& A, int64_t n) { return n - A.c0; }
@@ -1001,7 +1003,7 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
                                                 const LayerPk& pk, f32x16 (&acc)[2][4], Pre& pre,
                                                 bf16_t* Xs, bf16_t* Qs, bf16_t* Ks, bf16_t* Vts,
                                                 bf16_t* Kc, bf16_t* Vc, bf16_t* kc, bf16_t* vc,
-                                                int p0, bool keep, int g) {
+                                                int p0, bool keep, int g, CacheChunk& ch) {
   const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
   // (the last group's output projection also adds b_o: its bias k-block follows
   // the group's 4 k-blocks)
@@ -1015,9 +1017,9 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
   // the output projection's look-ahead is loaded during the attention
   const auto prime = [&] { seg_prime<Wo>(pre, so, otid() % WAVE); };
   if (A.dh == 64)
-    attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc, prime);
+    attend_group<64>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc, ch, prime);
   else
-    attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc, prime);
+    attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc, ch, prime);
   __syncthreads();
   // the cache stores follow the phase's weight loads, so the next phase's first
   // wait on its weights does not also wait for the stores
@@ -1040,9 +1042,12 @@ __device__ __forceinline__ void attention_sublayer(const Args& A, const tav2_lay
                                                    bf16_t* Qs, bf16_t* Ks, bf16_t* Vts, bf16_t* Kc,
                                                    bf16_t* Vc, bf16_t* kc, bf16_t* vc, int p0,
                                                    bool keep) {
+  CacheChunk ch;   // first cached chunk of the group about to attend
+  if (p0 > 0) cache_load(ch, kc, vc, A.tpad, 0, 0);
   for (int g = 0; g + 1 < DM / 64; ++g)
-    attention_group<false>(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep, g);
-  attention_group<true>(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep, DM / 64 - 1);
+    attention_group<false>(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep, g, ch);
+  attention_group<true>(A, L, pk, acc, pre, Xs, Qs, Ks, Vts, Kc, Vc, kc, vc, p0, keep, DM / 64 - 1,
+                        ch);
 }
 
 // FFN sublayer: per chunk of FC hidden units, H^T into LDS, then
