@@ -824,9 +824,11 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
     const int w = __builtin_amdgcn_readfirstlane(otid() / WAVE);
     const WSeg s_at = seg_resid(A.pk_at, AT_COLS / 16, 0, w);
     const WSeg s_pos = seg_resid(A.pk_pos, A.pos_nkb, p0 / 16, w);
-    resid_phase<ShEmb, ShTab>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), s_at, Xs, XLD);
-    table_phase<ShPos>(acc, pre, s_at, s_pos, tinfo);
-    pos_phase<ShQkv>(acc, pre, s_pos, nxt);
+    // the position rows (many weight bytes per MFMA) right after the long token
+    // projection, whose iterations have time to bring their look-ahead in
+    resid_phase<ShEmb, ShPos>(acc, pre, seg_resid(A.pk_in, KIN / 16, 0, w), s_pos, Xs, XLD);
+    pos_phase<ShTab>(acc, pre, s_pos, s_at);
+    table_phase<ShQkv>(acc, pre, s_at, nxt, tinfo);
   }
   {
     FZ_LANE_VARS
