@@ -38,11 +38,13 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint2& lo, const uint2& hi) {
   return __builtin_bit_cast(bf16x8, v);
 }
 // Two floats -> packed bf16 pair (a in the low half), round to nearest even: the
-// gfx950 conversion instruction, one per pair.
+// gfx950 conversion instruction, one per pair.  (A vector conversion: two scalar
+// conversions are not always merged, e.g. when the pair feeds packed 16-bit
+// arithmetic, and then cost two conversions and a permute.)
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-  const bf16x2_t v = {static_cast<__bf16>(a), static_cast<__bf16>(b)};
-  return __builtin_bit_cast(uint32_t, v);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
 }
 
 // Order-preserving 32-bit key of an fp32 score: larger score <=> larger key,

@@ -112,15 +112,20 @@ __device__ __forceinline__ bf16x8 bias_ones() {
 
 // Partner values across lane halves without LDS: the gfx950 permlane swaps of a
 // register with itself leave {v[l], v[l ^ 32]} (or {v[l], v[l ^ 16]}) in the pair.
+// Maximum without NaN quieting (gfx950 v_maximum3_f32): fmaxf's IEEE semantics
+// make the compiler canonicalize every operand that is not the result of an
+// arithmetic instruction (MFMA results, lane swaps), one extra instruction each.
+// The operands here are finite or -inf.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 __device__ __forceinline__ float xmax32(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
                                                   false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float xmax16(float v) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
                                                   false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float xsum32(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
@@ -495,7 +500,7 @@ __device__ __forceinline__ void layer_norm(f32x16 (&acc)[2][4], const float* P, 
     const bool up = (l32 & (MASK)) != 0;                                      \
     const float keep = up ? v[k + (HALF)] : v[k];                             \
     const float send = up ? v[k] : v[k + (HALF)];                             \
-    v[k] = fmaxf(keep, __shfl_xor(send, (MASK), WAVE));                       \
+    v[k] = vmax(keep, __shfl_xor(send, (MASK), WAVE));                       \
   }
 
 __device__ __forceinline__ int pool_feature() {
@@ -516,7 +521,7 @@ __device__ __forceinline__ float pool_block(f32x16 (&acc)[2][4], float pm, int n
       float m = -__builtin_inff();
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt)
-        if (tt * 32 + l32 < nvalid) m = fmaxf(m, acc[ft][tt][r]);
+        if (tt * 32 + l32 < nvalid) m = vmax(m, acc[ft][tt][r]);
       v[ft * 16 + r] = m;
     }
   FZ_TMAX(16, 1)
@@ -524,7 +529,7 @@ __device__ __forceinline__ float pool_block(f32x16 (&acc)[2][4], float pm, int n
   FZ_TMAX(4, 4)
   FZ_TMAX(2, 8)
   FZ_TMAX(1, 16)
-  return fmaxf(pm, v[0]);
+  return vmax(pm, v[0]);
 }
 
 // ---------------------------------------------------------------- attention
@@ -564,18 +569,28 @@ __device__ __forceinline__ void attn_init(AttnState<DH>& st, const bf16_t* Qs, i
 // template parameters, so both tiles' work is one branch-free block the scheduler
 // can interleave.  S^T tile 2 kp + t holds keys 32 kp + 16 t + 4 gq + i; the P^T
 // fragment of pair kp takes them in that order (keys 4gq.., then 16 + 4gq..) and
-// V^T is read to match.  DIAG masks keys above the lane's query row (only the
-// last pair of a tile reaches past its first query).  exp2 is the hardware
-// instruction (results below 2^-126 flush to zero, far under the bf16
-// resolution of P).
-template <int DH, bool DIAG, int NP>
+// V^T is read to match.  exp2 is the hardware instruction (results below 2^-126
+// flush to zero, far under the bf16 resolution of P).
+//
+// Causal mask (DQ = the query tile, or -1 for a segment of earlier keys): only
+// the tile's last pair reaches past its first query.  Of its two 16-key halves,
+// the half holding keys 16 DQ .. +15 is a triangle (key 4 gq + i of it is
+// visible to the lane's query c16 iff 4 gq + i <= c16, the same four lane masks
+// for every tile); the other half is entirely visible (odd DQ) or entirely
+// masked (even DQ: no products, P = 0).
+template <int DQ, int NP>
+constexpr bool dead_half(int kp, int t) {   // all keys of S^T tile 2 kp + t masked
+  return DQ >= 0 && (DQ & 1) == 0 && kp == NP - 1 && t == 1;
+}
+template <int DH, int DQ, int NP>
 __device__ __forceinline__ void seg_scores(f32x4v (&s)[8], const AttnState<DH>& st,
-                                           const bf16_t* Kl, int kld, int col0, int qt, int lane) {
+                                           const bf16_t* Kl, int kld, int col0, int lane) {
   const int gq = lane / 16, c16 = lane % 16;
 #pragma unroll
   for (int kp = 0; kp < NP; ++kp)
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
+      if (dead_half<DQ, NP>(kp, t)) continue;
       f32x4v acc = f32x4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < DH / 32; ++kb)
@@ -583,33 +598,36 @@ __device__ __forceinline__ void seg_scores(f32x4v (&s)[8], const AttnState<DH>& 
                      st.qf[kb], acc);
       s[2 * kp + t] = acc;
     }
-  if (DIAG) {
-    const int qrow = 16 * qt + c16;
-    constexpr int kp = NP - 1;
+  if constexpr (DQ >= 0) {
+    constexpr int tri = 2 * (NP - 1) + (DQ & 1);
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (32 * kp + 16 * t + 4 * gq + i > qrow) s[2 * kp + t][i] = -__builtin_inff();
+    for (int i = 0; i < 4; ++i)
+      if (4 * gq + i > c16) s[tri][i] = -__builtin_inff();
   }
 }
-template <int DH, int NP>
+// FIRST: the tile's first segment (l and O still zero: no rescale).
+template <int DH, int DQ, int NP, bool FIRST>
 __device__ __forceinline__ float seg_rescale(AttnState<DH>& st, const f32x4v (&s)[8]) {
   constexpr float sc = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
   float mx = -__builtin_inff();
 #pragma unroll
   for (int q = 0; q < 2 * NP; ++q)
-    mx = fmaxf(mx, fmaxf(fmaxf(s[q][0], s[q][1]), fmaxf(s[q][2], s[q][3])));
+    if (!dead_half<DQ, NP>(q / 2, q % 2))
+      mx = vmax(mx, vmax(vmax(s[q][0], s[q][1]), vmax(s[q][2], s[q][3])));
   mx = xmax32(xmax16(mx));
-  const float mnew = fmaxf(st.m, mx * sc);   // finite: every segment has a visible key
-  const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
-  st.m = mnew;
-  st.l *= alpha;
+  if constexpr (FIRST) {
+    st.m = mx * sc;                 // finite: every segment has a visible key
+  } else {
+    const float mnew = vmax(st.m, mx * sc);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
+    st.m = mnew;
+    st.l *= alpha;
 #pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] *= alpha;
-  return mnew;
+    for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] *= alpha;
+  }
+  return st.m;
 }
-template <int DH, int NP>
+template <int DH, int DQ, int NP>
 __device__ __forceinline__ void seg_pv(AttnState<DH>& st, const f32x4v (&s)[8], float mnew,
                                        const bf16_t* Vl, int vld, int col0, int lane) {
   const int gq = lane / 16, c16 = lane % 16;
@@ -619,13 +637,19 @@ __device__ __forceinline__ void seg_pv(AttnState<DH>& st, const f32x4v (&s)[8], 
   for (int kp = 0; kp < NP; ++kp) {
     bf16x8 pb;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < 2; ++t) {
+      if (dead_half<DQ, NP>(kp, t)) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pb[4 * t + i] = static_cast<__bf16>(0.f);
+        continue;
+      }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float pv = __builtin_amdgcn_exp2f(fmaf(s[2 * kp + t][i], sc, -mnew));
         psum += pv;
         pb[4 * t + i] = static_cast<__bf16>(pv);
       }
+    }
 #pragma unroll
     for (int dt = 0; dt < DH / 16; ++dt) {
       const bf16_t* vr = Vl + (col0 + 16 * dt + c16) * vld + 32 * kp + 4 * gq;
@@ -636,25 +660,25 @@ __device__ __forceinline__ void seg_pv(AttnState<DH>& st, const f32x4v (&s)[8], 
   }
   st.l += psum;
 }
-template <int DH, bool DIAG, int NPA, int NPB>
+template <int DH, int DQA, int DQB, int NPA, int NPB, bool FIRST>
 __device__ __forceinline__ void attn_segment2(AttnState<DH>& sa, AttnState<DH>& sb,
                                               const bf16_t* Kl, int kld, const bf16_t* Vl,
-                                              int vld, int col0, int qa, int qb, int lane) {
+                                              int vld, int col0, int lane) {
   f32x4v s_a[8], s_b[8];
-  seg_scores<DH, DIAG, NPA>(s_a, sa, Kl, kld, col0, qa, lane);
-  seg_scores<DH, DIAG, NPB>(s_b, sb, Kl, kld, col0, qb, lane);
-  const float ma = seg_rescale<DH, NPA>(sa, s_a);
-  const float mb = seg_rescale<DH, NPB>(sb, s_b);
-  seg_pv<DH, NPA>(sa, s_a, ma, Vl, vld, col0, lane);
-  seg_pv<DH, NPB>(sb, s_b, mb, Vl, vld, col0, lane);
+  seg_scores<DH, DQA, NPA>(s_a, sa, Kl, kld, col0, lane);
+  seg_scores<DH, DQB, NPB>(s_b, sb, Kl, kld, col0, lane);
+  const float ma = seg_rescale<DH, DQA, NPA, FIRST>(sa, s_a);
+  const float mb = seg_rescale<DH, DQB, NPB, FIRST>(sb, s_b);
+  seg_pv<DH, DQA, NPA>(sa, s_a, ma, Vl, vld, col0, lane);
+  seg_pv<DH, DQB, NPB>(sb, s_b, mb, Vl, vld, col0, lane);
 }
 // The block's own keys for wave W: tiles W and 7 - W see W / 2 + 1 and
 // (7 - W) / 2 + 1 pairs.
 template <int DH, int W>
 __device__ __forceinline__ void attn_own(AttnState<DH>& sa, AttnState<DH>& sb, const bf16_t* Ks,
                                          const bf16_t* Vts, int col0, int lane) {
-  attn_segment2<DH, true, W / 2 + 1, (7 - W) / 2 + 1>(sa, sb, Ks, QLD, Vts, VLD, col0, W, 7 - W,
-                                                      lane);
+  attn_segment2<DH, W, 7 - W, W / 2 + 1, (7 - W) / 2 + 1, true>(sa, sb, Ks, QLD, Vts, VLD, col0,
+                                                                lane);
 }
 
 // O = O^T / l into the tile's rows of Qs (the tile's Q is already in registers).
@@ -741,7 +765,7 @@ __device__ __forceinline__ void attend_group(int g, int p0, bf16_t* Qs, const bf
     for (int c0 = 0; c0 < p0; c0 += BT) {     // earlier blocks: every key visible
       if (c0 > 0) cache_load(ch, kc, vc, tpad, g, c0);
       cache_put(ch, Kc, Vc);
-      attn_segment2<DH, false, 4, 4>(sa, sb, Kc, QLD, Vc, VLD, hd * DH, qa, qb, lane);
+      attn_segment2<DH, -1, -1, 4, 4, false>(sa, sb, Kc, QLD, Vc, VLD, hd * DH, lane);
       __syncthreads();
     }
     attn_finish<DH>(sa, Qs, hd * DH, qa);
