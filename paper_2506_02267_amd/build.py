@@ -35,9 +35,16 @@ def compile_flags():
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
+# Per-source extra flags.  The fused encoder's MFMA results are read by VALU code
+# (softmax, epilogues, LayerNorm): results kept in VGPRs save one accumulator
+# move per element.
+EXTRA_FLAGS = {"encoder_fused.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc()] + compile_flags() + ["-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = ([hipcc()] + compile_flags() + EXTRA_FLAGS.get(src, [])
+           + ["-c", os.path.join(CSRC, src), "-o", obj])
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -568,8 +568,9 @@ __device__ __forceinline__ void attn_init(AttnState<DH>& st, const bf16_t* Qs, i
 // of l and O per segment, then P and O^T += V^T P^T per pair.  The pair counts are
 // template parameters, so both tiles' work is one branch-free block the scheduler
 // can interleave.  S^T tile 2 kp + t holds keys 32 kp + 16 t + 4 gq + i; the P^T
-// fragment of pair kp takes them in that order (keys 4gq.., then 16 + 4gq..) and
-// V^T is read to match.  exp2 is the hardware instruction (results below 2^-126
+// fragment of pair kp takes them in that order (keys 4gq.., then 16 + 4gq..), and
+// V^T rows store each pair's keys in the same order (vpos), so a lane's V^T
+// fragment is one 16-byte read.  exp2 is the hardware instruction (results below 2^-126
 // flush to zero, far under the bf16 resolution of P).
 //
 // Causal mask (DQ = the query tile, or -1 for a segment of earlier keys): only
@@ -627,50 +628,84 @@ __device__ __forceinline__ float seg_rescale(AttnState<DH>& st, const f32x4v (&s
   }
   return st.m;
 }
-template <int DH, int DQ, int NP>
-__device__ __forceinline__ void seg_pv(AttnState<DH>& st, const f32x4v (&s)[8], float mnew,
-                                       const bf16_t* Vl, int vld, int col0, int lane) {
+// V^T fragment (16 dims x the 32 keys of pair kp) for head dims col0 + 16 dt: one
+// 16-byte read, since V^T rows keep each pair's keys in P^T fragment order.
+template <int DH>
+__device__ __forceinline__ void v_frags(bf16x8 (&vf)[DH / 16], const bf16_t* Vl, int vld, int col0,
+                                        int kp, int lane) {
   const int gq = lane / 16, c16 = lane % 16;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt)
+    vf[dt] = lfrag(Vl + (col0 + 16 * dt + c16) * vld + 32 * kp + 8 * gq);
+}
+// P^T fragment of pair kp (bf16 probabilities of S^T tiles 2 kp, 2 kp + 1) and its
+// contribution to the tile's row sum.
+template <int DH, int DQ, int NP>
+__device__ __forceinline__ bf16x8 seg_probs(const f32x4v (&s)[8], int kp, float mnew,
+                                            float& psum) {
   constexpr float sc = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
-  float psum = 0.f;
+  bf16x8 pb;
 #pragma unroll
-  for (int kp = 0; kp < NP; ++kp) {
-    bf16x8 pb;
+  for (int t = 0; t < 2; ++t) {
+    if (dead_half<DQ, NP>(kp, t)) {
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      if (dead_half<DQ, NP>(kp, t)) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pb[4 * t + i] = static_cast<__bf16>(0.f);
-        continue;
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float pv = __builtin_amdgcn_exp2f(fmaf(s[2 * kp + t][i], sc, -mnew));
-        psum += pv;
-        pb[4 * t + i] = static_cast<__bf16>(pv);
-      }
+      for (int i = 0; i < 4; ++i) pb[4 * t + i] = static_cast<__bf16>(0.f);
+      continue;
     }
 #pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt) {
-      const bf16_t* vr = Vl + (col0 + 16 * dt + c16) * vld + 32 * kp + 4 * gq;
-      const bf16x8 vf = as_bf16x8(*reinterpret_cast<const uint2*>(vr),
-                                  *reinterpret_cast<const uint2*>(vr + 16));
-      st.o[dt] = mfma16(vf, pb, st.o[dt]);
+    for (int i = 0; i < 4; ++i) {
+      const float pv = __builtin_amdgcn_exp2f(fmaf(s[2 * kp + t][i], sc, -mnew));
+      psum += pv;
+      pb[4 * t + i] = static_cast<__bf16>(pv);
     }
   }
-  st.l += psum;
+  return pb;
+}
+// O^T += V^T P^T for both tiles, pair by pair: each V^T fragment is read once for
+// the two tiles, the next pair's while this pair's probabilities are computed.
+// vf enters holding pair 0 (read after the S products: read before them, its
+// registers make the compiler serialize the K reads).
+template <int DH, int DQA, int DQB, int NPA, int NPB>
+__device__ __forceinline__ void seg_pv2(AttnState<DH>& sa, AttnState<DH>& sb,
+                                        const f32x4v (&s_a)[8], const f32x4v (&s_b)[8], float ma,
+                                        float mb, bf16x8 (&vf)[DH / 16], const bf16_t* Vl,
+                                        int vld, int col0, int lane) {
+  constexpr int NP = NPA > NPB ? NPA : NPB;
+  float psa = 0.f, psb = 0.f;
+#pragma unroll
+  for (int kp = 0; kp < NP; ++kp) {
+    bf16x8 vn[DH / 16];
+    if (kp + 1 < NP) v_frags<DH>(vn, Vl, vld, col0, kp + 1, lane);
+    if (kp < NPA) {
+      const bf16x8 pb = seg_probs<DH, DQA, NPA>(s_a, kp, ma, psa);
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) sa.o[dt] = mfma16(vf[dt], pb, sa.o[dt]);
+    }
+    if (kp < NPB) {
+      const bf16x8 pb = seg_probs<DH, DQB, NPB>(s_b, kp, mb, psb);
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) sb.o[dt] = mfma16(vf[dt], pb, sb.o[dt]);
+    }
+    if (kp + 1 < NP) {
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) vf[dt] = vn[dt];
+    }
+  }
+  sa.l += psa;
+  sb.l += psb;
 }
 template <int DH, int DQA, int DQB, int NPA, int NPB, bool FIRST>
 __device__ __forceinline__ void attn_segment2(AttnState<DH>& sa, AttnState<DH>& sb,
                                               const bf16_t* Kl, int kld, const bf16_t* Vl,
                                               int vld, int col0, int lane) {
   f32x4v s_a[8], s_b[8];
+  bf16x8 vf[DH / 16];
   seg_scores<DH, DQA, NPA>(s_a, sa, Kl, kld, col0, lane);
   seg_scores<DH, DQB, NPB>(s_b, sb, Kl, kld, col0, lane);
+  v_frags<DH>(vf, Vl, vld, col0, 0, lane);
   const float ma = seg_rescale<DH, DQA, NPA, FIRST>(sa, s_a);
   const float mb = seg_rescale<DH, DQB, NPB, FIRST>(sb, s_b);
-  seg_pv<DH, DQA, NPA>(sa, s_a, ma, Vl, vld, col0, lane);
-  seg_pv<DH, DQB, NPB>(sb, s_b, mb, Vl, vld, col0, lane);
+  seg_pv2<DH, DQA, DQB, NPA, NPB>(sa, sb, s_a, s_b, ma, mb, vf, Vl, vld, col0, lane);
 }
 // The block's own keys for wave W: tiles W and 7 - W see W / 2 + 1 and
 // (7 - W) / 2 + 1 pairs.
@@ -871,6 +906,13 @@ __device__ __forceinline__ void encode_block_input(const Args& A, int64_t n, int
 }
 
 // ---------------------------------------------------------------- sublayers
+// Position of key k (0..31, a multiple of 4 here) inside its 32-key pair in a V^T
+// row: the order of the P^T fragment of 16x16x32 products, where lane group gq
+// holds keys 4 gq .. +3 and 16 + 4 gq .. +3 as k-rows 8 gq .. +7.
+__device__ __forceinline__ int vpos(int k) {
+  return 8 * ((k >> 2) & 3) + 4 * (k >> 4) + (k & 3);
+}
+
 // Q / K / V of head group g: wave w computes token tiles 2(w & 1), 2(w & 1) + 1 of
 // column tiles 3 CS .. +2 of [q0 q1 k0 k1 v0 v1] (CS = w >> 1); Q and K
 // transposed ([dim][token]), V untransposed.  Leaves the look-ahead empty.  The
@@ -936,7 +978,7 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
       } else {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j],
+          st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + vpos(8 * j + 4 * hf), qa[t][u][4 * j],
               qa[t][u][4 * j + 1], qa[t][u][4 * j + 2], qa[t][u][4 * j + 3]);
       }
     }
