@@ -6,12 +6,15 @@
 // inputs use fp32 FMA).  Each request's rows are read by every candidate tile of
 // that request straight from the one stored copy (no per-candidate broadcast).
 //
-// Top-k: one workgroup per candidate holds the candidate's score row in
-// registers as order-preserving 32-bit keys, finds the k-th largest key with a
-// 32-step bitwise search (each step one block-wide count), keeps every key
-// above it plus the lowest-indexed rows equal to it (an ordered compaction by
-// block-wide prefix sum), and places the k survivors by counting, for each,
-// how many survivors precede it in the total order.
+// Top-k, one workgroup per candidate, scores as order-preserving 32-bit keys.
+// Rows of up to 4096 keys: the row is held in registers, the k-th largest key
+// found by a 32-step bitwise search (each step one block-wide count), every key
+// above it kept plus the lowest-indexed rows equal to it (an ordered compaction
+// by block-wide prefix sum).  Longer rows are streamed once against a threshold
+// taken from a sample, the keys above it compacted into LDS and the k-th largest
+// found there by a radix select (an exact streaming search when the sample
+// gives no usable threshold).  Either way the k survivors are placed by counting,
+// for each, how many survivors precede it in the total order.
 #include "common.h"
 #include "internal.h"
 
@@ -132,7 +135,8 @@ __global__ __launch_bounds__(256) void score_f32_kernel(
 constexpr int TK_THREADS = 512;
 
 // Exclusive prefix (in thread order) and block total of NV 64-bit values per
-// thread; sw holds NV per wave.  Ends with a barrier.
+// thread; sw holds NV per wave.  sw is read after the one barrier inside: the
+// caller synchronizes again before sw is written by a later scan.
 template <int NV>
 __device__ __forceinline__ void block_excl_scan(const uint64_t (&v)[NV], uint64_t (&excl)[NV],
                                                 uint64_t (&total)[NV], uint64_t* sw, int lane,
@@ -164,117 +168,6 @@ __device__ __forceinline__ void block_excl_scan(const uint64_t (&v)[NV], uint64_
   }
 }
 
-// Sampled threshold (the common case, exact result): a threshold t taken from a
-// strided sample of the keys (its r-th largest, cut to its top 16 bits, r a few
-// standard deviations above the expected number of sampled keys among the kk
-// largest) usually leaves between kk and TK_CAP keys >= t.  Those are compacted
-// into LDS as unique 48-bit values (key, 0xFFFF - row), whose kk-th largest is
-// found exactly by an 8-bit-per-pass radix select; every value at or above it is
-// one of the kk selected keys (ties between equal scores go to the lower row, as
-// in the exhaustive search).  Returns false (block-uniform) when the sample does
-// not give such a threshold, leaving the exhaustive search to the caller.
-constexpr int TK_CAP = 2048;
-template <int PT>
-__device__ bool topk_sampled(const uint32_t (&key)[PT], int kk, uint64_t* cand, uint32_t* hist,
-                             int* red, uint64_t* scan_w, uint64_t* sel, int* misc, int tid,
-                             int lane, int wid) {
-  constexpr int NC = PT / 4, CH = TK_THREADS * 4, NW = TK_THREADS / WAVE;
-  static_assert(NC >= 4, "four sample chunks per thread");
-  // sample: the first key of chunks 0, NC/4, NC/2, 3NC/4 of every thread (4 of PT)
-  const float expct = float(kk) * 4.f / float(PT);
-  const int r = int(expct + 4.f * sqrtf(expct) + 8.f);
-  if (r >= TK_THREADS * 2) return false;
-  uint32_t smp[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) smp[i] = key[4 * (i * NC / 4)];
-  uint32_t thr = 0;
-  for (int b = 31; b >= 16; --b) {
-    const uint32_t probe = thr | (1u << b);
-    int cnt = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) cnt += __popcll(__builtin_amdgcn_ballot_w64(smp[i] >= probe));
-    if (lane == 0) red[(b & 1) * NW + wid] = cnt;
-    __syncthreads();
-    int tot = 0;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) tot += red[(b & 1) * NW + w];
-    if (tot >= r) thr = probe;
-  }
-  // keys >= thr: count, then compact
-  uint64_t c[1] = {0}, excl[1], total[1];
-#pragma unroll
-  for (int j = 0; j < PT; ++j) c[0] += key[j] >= thr ? 1u : 0u;
-  block_excl_scan<1>(c, excl, total, scan_w, lane, wid);
-  const int clo = int(total[0]);
-  if (clo < kk || clo > TK_CAP) return false;
-  int pos = int(excl[0]);
-#pragma unroll
-  for (int q = 0; q < NC; ++q)
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (key[4 * q + u] >= thr)
-        cand[pos++] = (uint64_t(key[4 * q + u]) << 16) | uint64_t(0xFFFFu - uint32_t(q * CH + tid * 4 + u));
-  // radix select of the kk-th largest 48-bit value, most significant byte first
-  uint64_t pre = 0;
-  int need = kk;
-  for (int sh = 40; sh >= 0; sh -= 8) {
-    if (tid < 256) hist[tid] = 0;
-    __syncthreads();   // (also publishes cand before the first pass)
-    for (int i = tid; i < clo; i += TK_THREADS) {
-      const uint64_t v = cand[i];
-      if ((v >> (sh + 8)) == pre) atomicAdd(&hist[(v >> sh) & 255u], 1u);
-    }
-    __syncthreads();
-    if (wid == 0) {   // bins in descending order: lane l holds 255 - 4l - q
-      uint32_t h[4], sum = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        h[q] = hist[255 - 4 * lane - q];
-        sum += h[q];
-      }
-      uint32_t incl = sum;
-#pragma unroll
-      for (int o = 1; o < WAVE; o <<= 1) {
-        const uint32_t t = __shfl_up(incl, o, WAVE);
-        if (lane >= o) incl += t;
-      }
-      const uint32_t before = incl - sum;   // values in higher bins
-      if (before < uint32_t(need) && uint32_t(need) <= incl) {
-        uint32_t cum = before;
-        int digit = 0, rest = 0;
-        bool hit = false;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (!hit && cum + h[q] >= uint32_t(need)) {
-            hit = true;
-            digit = 255 - 4 * lane - q;
-            rest = need - int(cum);
-          }
-          cum += h[q];
-        }
-        misc[0] = digit;
-        misc[1] = rest;
-      }
-    }
-    __syncthreads();
-    pre = (pre << 8) | uint64_t(misc[0]);
-    need = misc[1];
-    __syncthreads();   // misc and hist are rewritten by the next pass
-  }
-  // exactly kk values are >= pre; their order is set by the caller's rank sort
-  if (tid == 0) misc[2] = 0;
-  __syncthreads();
-  for (int i = tid; i < clo; i += TK_THREADS) {
-    const uint64_t v = cand[i];
-    if (v >= pre) {
-      const uint32_t kv = uint32_t(v >> 16), row = 0xFFFFu - uint32_t(v & 0xFFFFu);
-      sel[atomicAdd(&misc[2], 1)] = (uint64_t(kv) << 32) | uint64_t(0xFFFFFFFFu - row);
-    }
-  }
-  __syncthreads();
-  return true;
-}
-
 template <int PT>
 __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     const float* __restrict__ scores, int64_t ld, const int64_t* __restrict__ cand_off,
@@ -283,9 +176,6 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
   __shared__ int red[2][TK_THREADS / WAVE];
   __shared__ uint64_t scan_w[(TK_THREADS / WAVE) * 5];
   __shared__ uint64_t sel[TAV2_K_MAX];
-  __shared__ uint64_t cand[PT >= 16 ? TK_CAP : 1];
-  __shared__ uint32_t hist[256];
-  __shared__ int misc[4];
 
   const int r = blockIdx.y;
   const int64_t n = cand_off[r] + blockIdx.x;
@@ -323,10 +213,7 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     }
   }
 
-  bool sampled = false;
-  if constexpr (PT >= 16)
-    sampled = topk_sampled<PT>(key, kk, cand, hist, &red[0][0], scan_w, sel, misc, tid, lane, wid);
-  if (!sampled) {
+  {
   // exhaustive: largest threshold t with count(key >= t) >= kk, one bit at a time
   uint32_t thr = 0;
   for (int b = 31; b >= 0; --b) {
@@ -402,6 +289,291 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
   }
 }
 
+// ---------------------------------------------------------------- top-k, long rows
+// Rows of more than 4096 keys: instead of holding the row in registers (which
+// limits a compute unit to two rows at a time), the row is streamed once.
+//  1. Threshold t from a sample: blocks of 64 consecutive rows at a fixed spacing
+//     (at most 2048 sampled rows, one load per thread); t is the r-th largest
+//     sampled key cut to its top 16 bits, r a few standard deviations above the
+//     expected number of sampled keys among the kk largest.
+//  2. Stream the row once, appending every key >= t to LDS as the unique 48-bit
+//     value (key, 0xFFFF - row) (positions from one LDS counter per wave and
+//     chunk: the order does not matter, the final rank sort sets it).
+//  3. Radix select of the kk-th largest appended value (8 bits per pass); the kk
+//     values at or above it are the result (ties between equal scores go to the
+//     lower row through the 48-bit value).
+// When the sample gives no usable t (fewer than kk or more than TK_CAP keys
+// >= t), a streaming exhaustive search takes over: the largest t with at least
+// kk keys >= t, one bit per pass over the row, then every key above t and the
+// lowest rows equal to it (an ordered compaction, chunk by chunk).
+constexpr int TS_THREADS = 512;
+constexpr int TS_NW = TS_THREADS / WAVE;
+constexpr int TK_CAP = 2048;            // appended keys at most (else the exhaustive search)
+constexpr int TS_CH = TS_THREADS * 4;   // rows per streamed chunk (4 per thread)
+constexpr int TS_SBLK = 64;             // sampled rows come in blocks of 64
+
+// Keys of rows r0 .. r0 + 3 (r0 a multiple of 4); rows past L get key 0, which
+// lies below every score.  One buffer load over the row (its stride, a multiple
+// of 64 that is >= L, in bytes as the range: reads past it return zeros).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const float* srow, int64_t ld) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(srow), (short)0, int(ld * 4),
+                                           0x00020000);
+}
+__device__ __forceinline__ void load_keys4(__amdgpu_buffer_rsrc_t rs, int r0, int L,
+                                           uint32_t (&kv)[4]) {
+  const float4 v = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, r0 * 4, 0, 0));
+  kv[0] = r0 < L ? score_key(v.x) : 0u;
+  kv[1] = r0 + 1 < L ? score_key(v.y) : 0u;
+  kv[2] = r0 + 2 < L ? score_key(v.z) : 0u;
+  kv[3] = r0 + 3 < L ? score_key(v.w) : 0u;
+}
+// Block-wide sum of a wave-uniform count (one value per wave); red[parity] must
+// not be in use by the previous call (alternate the parity).
+__device__ __forceinline__ int block_sum_waves(int cnt, int* red, int lane, int wid) {
+  if (lane == 0) red[wid] = cnt;
+  __syncthreads();
+  int tot = 0;
+#pragma unroll
+  for (int w = 0; w < TS_NW; ++w) tot += red[w];
+  return tot;
+}
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi(uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0));
+}
+
+__global__ __launch_bounds__(TS_THREADS) void topk_stream_kernel(
+    const float* __restrict__ scores, int64_t ld, const int64_t* __restrict__ cand_off,
+    const int32_t* __restrict__ seq_len, int max_len, int k, int32_t* __restrict__ out_idx,
+    float* __restrict__ out_score) {
+  __shared__ int red[2][TS_NW];
+  __shared__ uint64_t scan_w[TS_NW];
+  __shared__ uint64_t sel[TAV2_K_MAX];
+  __shared__ uint64_t cand[TK_CAP];
+  __shared__ uint32_t hist[256];
+  __shared__ int misc[4];   // radix digit, rest, selected count, appended count
+
+  const int r = blockIdx.y;
+  const int64_t n = cand_off[r] + blockIdx.x;
+  if (n >= cand_off[r + 1]) return;
+  const int L = min(seq_len[r], max_len);
+  const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
+  const int kk = k < L ? k : L;
+  int32_t* oi = out_idx + n * k;
+  float* os = out_score + n * k;
+  for (int p = kk + tid; p < k; p += TS_THREADS) {
+    oi[p] = -1;
+    os[p] = -__builtin_inff();
+  }
+  if (kk == 0) return;
+  const __amdgpu_buffer_rsrc_t rs = row_rsrc(scores + n * ld, ld);
+  const int nch = (L + TS_CH - 1) / TS_CH;
+  int par = 0;   // parity of the next block_sum_waves buffer
+
+  // 1. threshold from the sample (rows of a short row all survive: key >= 1)
+  bool ok = true;
+  uint32_t thr = 1;
+  if (L > TK_CAP) {
+    const int sp = TS_SBLK * ((L + TK_CAP - 1) / TK_CAP);   // block spacing: <= 32 blocks
+    const int j0 = 4 * tid;                                 // sample slots j0 .. j0 + 3
+    uint32_t smp[4];
+    load_keys4(rs, sp * (j0 / TS_SBLK) + j0 % TS_SBLK, L, smp);
+    const int nb = (L + sp - 1) / sp;
+    const int ns = (nb - 1) * TS_SBLK + min(TS_SBLK, L - (nb - 1) * sp);   // sampled rows < L
+    const float expct = float(kk) * float(ns) / float(L);
+    const int rr = int(expct + 4.f * sqrtf(expct) + 8.f);
+    if (rr > ns) {
+      ok = false;
+    } else {
+      thr = 0;
+      for (int b = 31; b >= 16; --b) {
+        const uint32_t probe = thr | (1u << b);
+        int cnt = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) cnt += __popcll(__builtin_amdgcn_ballot_w64(smp[u] >= probe));
+        if (block_sum_waves(cnt, red[par], lane, wid) >= rr) thr = probe;
+        par ^= 1;
+      }
+      if (thr == 0) thr = 1;
+    }
+  }
+
+  // 2. stream the row, appending the keys >= thr
+  if (ok) {
+    if (tid == 0) misc[3] = 0;
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+      const int r0 = c * TS_CH + 4 * tid;
+      uint32_t kv[4];
+      load_keys4(rs, r0, L, kv);
+      uint64_t bm[4];
+      int tot = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        bm[u] = __builtin_amdgcn_ballot_w64(kv[u] >= thr);
+        tot += __popcll(bm[u]);
+      }
+      if (tot == 0) continue;   // wave-uniform
+      int base = 0;             // one counter update per wave and chunk
+      if (lane == 0) base = atomicAdd(&misc[3], tot);
+      base = __shfl(base, 0, WAVE);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int pos = base + lanes_below(bm[u]);
+        if (kv[u] >= thr && pos < TK_CAP)
+          cand[pos] = (uint64_t(kv[u]) << 16) | uint64_t(0xFFFFu - uint32_t(r0 + u));
+        base += __popcll(bm[u]);
+      }
+    }
+    __syncthreads();
+    const int clo = misc[3];
+    if (clo < kk || clo > TK_CAP) ok = false;
+    if (ok) {
+      // 3. radix select of the kk-th largest 48-bit value, most significant byte first
+      uint64_t pre = 0;
+      int need = kk;
+      for (int sh = 40; sh >= 0; sh -= 8) {
+        if (tid < 256) hist[tid] = 0;
+        __syncthreads();
+        for (int i = tid; i < clo; i += TS_THREADS) {
+          const uint64_t v = cand[i];
+          if ((v >> (sh + 8)) == pre) atomicAdd(&hist[(v >> sh) & 255u], 1u);
+        }
+        __syncthreads();
+        if (wid == 0) {   // bins in descending order: lane l holds 255 - 4l - q
+          uint32_t h[4], sum = 0;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            h[q] = hist[255 - 4 * lane - q];
+            sum += h[q];
+          }
+          uint32_t incl = sum;
+#pragma unroll
+          for (int o = 1; o < WAVE; o <<= 1) {
+            const uint32_t t = __shfl_up(incl, o, WAVE);
+            if (lane >= o) incl += t;
+          }
+          const uint32_t before = incl - sum;
+          if (before < uint32_t(need) && uint32_t(need) <= incl) {
+            uint32_t cum = before;
+            int digit = 0, rest = 0;
+            bool hit = false;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              if (!hit && cum + h[q] >= uint32_t(need)) {
+                hit = true;
+                digit = 255 - 4 * lane - q;
+                rest = need - int(cum);
+              }
+              cum += h[q];
+            }
+            misc[0] = digit;
+            misc[1] = rest;
+          }
+        }
+        __syncthreads();
+        pre = (pre << 8) | uint64_t(misc[0]);
+        need = misc[1];
+        __syncthreads();   // misc and hist are rewritten by the next pass
+      }
+      // exactly kk values are >= pre
+      if (tid == 0) misc[2] = 0;
+      __syncthreads();
+      for (int i = tid; i < clo; i += TS_THREADS) {
+        const uint64_t v = cand[i];
+        if (v >= pre) {
+          const uint32_t kv = uint32_t(v >> 16), row = 0xFFFFu - uint32_t(v & 0xFFFFu);
+          sel[atomicAdd(&misc[2], 1)] = (uint64_t(kv) << 32) | uint64_t(0xFFFFFFFFu - row);
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  if (!ok) {
+    // exhaustive: largest t with count(key >= t) >= kk, one bit (one pass) at a time
+    uint32_t t = 0;
+    for (int b = 31; b >= 0; --b) {
+      const uint32_t probe = t | (1u << b);
+      int cnt = 0;
+      for (int c = 0; c < nch; ++c) {
+        uint32_t kv[4];
+        load_keys4(rs, c * TS_CH + 4 * tid, L, kv);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) cnt += __popcll(__builtin_amdgcn_ballot_w64(kv[u] >= probe));
+      }
+      if (block_sum_waves(cnt, red[par], lane, wid) >= kk) t = probe;
+      par ^= 1;
+    }
+    // every key above t (any order), then the need_eq lowest rows equal to t
+    int gt = 0;
+    for (int c = 0; c < nch; ++c) {
+      uint32_t kv[4];
+      load_keys4(rs, c * TS_CH + 4 * tid, L, kv);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) gt += __popcll(__builtin_amdgcn_ballot_w64(kv[u] > t));
+    }
+    const int count_gt = block_sum_waves(gt, red[par], lane, wid);
+    par ^= 1;
+    const int need_eq = kk - count_gt;
+    if (tid == 0) misc[2] = 0;
+    __syncthreads();
+    int eq_before = 0;   // equal keys in earlier chunks (block-uniform)
+    for (int c = 0; c < nch; ++c) {
+      const int r0 = c * TS_CH + 4 * tid;
+      uint32_t kv[4];
+      load_keys4(rs, r0, L, kv);
+      uint64_t bm[4];
+      int tot = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        bm[u] = __builtin_amdgcn_ballot_w64(kv[u] > t);
+        tot += __popcll(bm[u]);
+      }
+      if (tot > 0) {   // wave-uniform
+        int base = 0;
+        if (lane == 0) base = atomicAdd(&misc[2], tot);
+        base = __shfl(base, 0, WAVE);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (kv[u] > t)
+            sel[base + lanes_below(bm[u])] =
+                (uint64_t(kv[u]) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(r0 + u));
+          base += __popcll(bm[u]);
+        }
+      }
+      // equal keys in row order: rows of the chunk are ordered by (thread, u)
+      uint64_t e[1] = {0}, excl[1], total[1];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) e[0] += kv[u] == t ? 1u : 0u;
+      block_excl_scan<1>(e, excl, total, scan_w, lane, wid);
+      int pos = eq_before + int(excl[0]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (kv[u] == t) {
+          if (pos < need_eq)
+            sel[count_gt + pos] = (uint64_t(kv[u]) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(r0 + u));
+          ++pos;
+        }
+      eq_before += int(total[0]);
+      __syncthreads();   // scan_w is rewritten by the next chunk's scan
+    }
+  }
+
+  // survivors are distinct under (key, -row): rank = number of survivors before it
+  for (int s = tid; s < kk; s += TS_THREADS) {
+    const uint64_t me = sel[s];
+    int rank = 0;
+    int t = 0;
+    for (; t + 8 <= kk; t += 8) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) rank += sel[t + u] > me ? 1 : 0;
+    }
+    for (; t < kk; ++t) rank += sel[t] > me ? 1 : 0;
+    oi[rank] = int32_t(0xFFFFFFFFu - uint32_t(me));
+    os[rank] = key_score(uint32_t(me >> 32));
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores, int64_t ld,
                          hipStream_t st) {
@@ -444,9 +616,9 @@ hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* sc
   topk_kernel<PT><<<grid, TK_THREADS, 0, st>>>(scores, ld, c.offset, seq.len, seq.max_len, k, out_idx, out_score)
   if (per <= 4) TAV2_TOPK(4);
   else if (per <= 8) TAV2_TOPK(8);
-  else if (per <= 16) TAV2_TOPK(16);
-  else if (per <= 32) TAV2_TOPK(32);
-  else TAV2_TOPK(64);
+  else
+    topk_stream_kernel<<<grid, TS_THREADS, 0, st>>>(scores, ld, c.offset, seq.len, seq.max_len, k,
+                                                     out_idx, out_score);
 #undef TAV2_TOPK
   return hipGetLastError();
 }

@@ -1,8 +1,9 @@
 """GPU parity of tav2_nn_select (Eq. 3) against the oracle: indices and scores
 bit for bit, on the five workloads (full runs, all or sampled candidates) and
 on edge cases (ragged, empty and short requests, k = 1 and k = K_MAX, heavy
-ties, padded layout, every register-tile size of the top-k kernel, ties inside
-the sampled-threshold path and inputs that make it fall back)."""
+ties, padded layout, every register-tile size of the short-row top-k and the
+long-row (streaming) top-k with short rows in its batch, ties inside its
+sampled-threshold path and inputs that make it fall back)."""
 import numpy as np
 import pytest
 import torch
@@ -69,6 +70,17 @@ def test_ragged_short_and_empty_requests(dtype):
         assert_select_equal(idx, score, ref_i, ref_s)
 
 
+def test_short_rows_in_a_long_batch():
+    # the batch's longest request selects the streaming top-k kernel; its shorter
+    # requests take that kernel's other branches (every row kept at <= 2048 rows,
+    # sampled threshold just above)
+    inp = custom_inputs([5000, 100, 3000, 0, 2048, 2049], [3, 4, 5, 2, 3, 3], seed=7)
+    for k in (1, 64, 301, 1024):
+        idx, score = run_select(inp, k)
+        ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
+        assert_select_equal(idx, score, ref_i, ref_s)
+
+
 def test_request_without_candidates():
     inp = custom_inputs([100, 200, 300], [4, 0, 3])
     idx, score = run_select(inp, 16)
@@ -111,14 +123,18 @@ def test_sampled_threshold_with_tied_rows(k):
 def test_sampled_threshold_falls_back(case):
     # inputs for which the sample gives no usable threshold: all scores equal (far
     # more than the candidate capacity at the threshold), or the largest scores
-    # only on rows the sample never looks at (rows = 2 mod 4)
+    # only on rows the sample never looks at (the sample of a 16384-row request is
+    # the 64-row blocks starting at multiples of 512: big scores on rows = 2 mod 4
+    # outside those blocks)
     inp = custom_inputs([16384], [4], d=32, levels=8, seed=5)
     e = inp.seq.emb
     if case == "all_equal":
         e[:] = e[0]
     else:
+        rows = np.arange(e.shape[0])
+        big = (rows % 4 == 2) & (rows % 512 >= 64)
         e[:] = -np.abs(e)
-        e[2::4] = np.abs(e[2::4]) + 1.0
+        e[big] = np.abs(e[big]) + 1.0
         inp.cand[:] = np.abs(inp.cand) + 0.125
     idx, score = run_select(inp, 512)
     ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, 512)
