@@ -306,11 +306,19 @@ __device__ __forceinline__ void stream_fetch(bf16x8 (&wq)[Cur::NKB][Cur::NR], Pr
   }
 }
 
+// Work a residual phase carries along: step(j) after the MFMAs of k-block j,
+// finish() after the last k-block.
+struct NoSide {
+  __device__ __forceinline__ void step(int) {}
+  __device__ __forceinline__ void finish() {}
+};
+
 // acc[ft][tt] += C^T: features 64 w + 32 ft (packed rows of cur), tokens 32 tt
 // (rows of ACT in LDS, columns 16 j), over Cur::NKB k-blocks.
-template <class Cur, class Nxt>
+template <class Cur, class Nxt, class Side = NoSide>
 __device__ __forceinline__ void resid_phase(f32x16 (&acc)[2][4], Pre& pre, const WSeg& cur,
-                                            const WSeg& nxt, const bf16_t* ACT, int ald) {
+                                            const WSeg& nxt, const bf16_t* ACT, int ald,
+                                            Side&& side = Side{}) {
   static_assert(Cur::NR == 2, "residual phases have two row tiles per wave");
   FZ_LANE_VARS
   constexpr int NKB = Cur::NKB;
@@ -334,9 +342,11 @@ __device__ __forceinline__ void resid_phase(f32x16 (&acc)[2][4], Pre& pre, const
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) acc[ft][tt] = mfma32(a, xq[j][tt], acc[ft][tt]);
     }
+    side.step(j);
     stream_fetch<Cur, Nxt>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
+  side.finish();
 }
 
 // ---------------------------------------------------------------- table rows
@@ -1038,28 +1048,54 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
 }
 
 // This block's K and V^T of head group g into the candidate's cache (read by the
-// candidate's later blocks).
-__device__ __forceinline__ void cache_store(const Args& A, int g, int p0, const bf16_t* Ks,
-                                            const bf16_t* Vts, bf16_t* kc, bf16_t* vc) {
+// candidate's later blocks), carried along by the output projection: piece q
+// (one 16-byte chunk of K and one of V^T per thread) is read from LDS at k-block
+// q and stored at k-block q + 1.  Buffer stores whose range is empty when the
+// block keeps nothing, so the phase has no branch.
+struct CacheStore {
+  __amdgpu_buffer_rsrc_t rk, rv;
+  const bf16_t* ks;   // this thread's piece 0 in Ks / Vts
+  const bf16_t* vs;
+  int ko, vo;         // its byte offsets in the cache slices
+  int vstep;          // bytes between V^T pieces (16 rows of the cache)
+  u32x4 k, v;         // the piece in flight
+  __device__ __forceinline__ void read(int q) {
+    k = *reinterpret_cast<const u32x4*>(ks + q * 32 * QLD);
+    v = *reinterpret_cast<const u32x4*>(vs + q * 16 * VLD);
+  }
+  __device__ __forceinline__ void write(int q) {
+    __builtin_amdgcn_raw_buffer_store_b128(k, rk, ko, q * 32 * DM * 2, 0);
+    __builtin_amdgcn_raw_buffer_store_b128(v, rv, vo, q * vstep, 0);
+  }
+  __device__ __forceinline__ void step(int j) {
+    if (j >= 1 && j <= 4) write(j - 1);
+    if (j <= 3) read(j);
+  }
+  __device__ __forceinline__ void finish() {}
+};
+template <int NKB>
+struct CacheStoreTail : CacheStore {   // a phase of 4 k-blocks stores the last piece after it
+  __device__ __forceinline__ void finish() {
+    if constexpr (NKB == 4) write(3);
+  }
+};
+template <int NKB>
+__device__ __forceinline__ CacheStoreTail<NKB> cache_store(const Args& A, int g, int p0,
+                                                           const bf16_t* Ks, const bf16_t* Vts,
+                                                           bf16_t* kc, bf16_t* vc, bool keep) {
+  static_assert(NKB == 4 || NKB == 5, "four pieces over the output projection's k-blocks");
   const int tid = otid();
   // (offsets in 32 bits: one candidate's cache holds at most DM x 1024 positions)
-  u32x4 kq[4], vq[4];   // all LDS reads first, so the stores go out back to back
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int e = tid + q * NT;
-    kq[q] = *reinterpret_cast<const u32x4*>(Ks + (e >> 3) * QLD + (e & 7) * 8);
-    vq[q] = *reinterpret_cast<const u32x4*>(Vts + (e >> 4) * VLD + (e & 15) * 8);
-  }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int e = tid + q * NT;
-    *reinterpret_cast<u32x4*>(kc + ((p0 + (e >> 3)) * DM + g * 64 + (e & 7) * 8)) = kq[q];
-  }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int e = tid + q * NT;
-    *reinterpret_cast<u32x4*>(vc + ((g * 64 + (e >> 4)) * A.tpad + p0 + (e & 15) * 8)) = vq[q];
-  }
+  const int bytes = keep ? A.tpad * DM * 2 : 0;
+  CacheStoreTail<NKB> c;
+  c.rk = __builtin_amdgcn_make_buffer_rsrc(kc, (short)0, bytes, 0x00020000);
+  c.rv = __builtin_amdgcn_make_buffer_rsrc(vc, (short)0, bytes, 0x00020000);
+  c.ks = Ks + (tid >> 3) * QLD + (tid & 7) * 8;
+  c.vs = Vts + (tid >> 4) * VLD + (tid & 15) * 8;
+  c.ko = ((p0 + (tid >> 3)) * DM + g * 64 + (tid & 7) * 8) * 2;
+  c.vo = ((g * 64 + (tid >> 4)) * A.tpad + p0 + (tid & 15) * 8) * 2;
+  c.vstep = 16 * A.tpad * 2;
+  return c;
 }
 
 // Attention sublayer of one layer for the block: per 64-dim head group, Q / K /
@@ -1089,15 +1125,16 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
   else
     attend_group<32>(g, p0, Qs, Ks, Vts, kc, vc, A.tpad, Kc, Vc, ch, prime);
   __syncthreads();
-  // the cache stores follow the phase's weight loads, so the next phase's first
-  // wait on its weights does not also wait for the stores
+  // the output projection carries the cache stores (after its first k-block's
+  // weight loads, so the next phase's first wait on its weights does not also wait
+  // for a store)
   if constexpr (!LAST) {
-    resid_phase<ShWo, ShQkv>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD);
-    if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
+    resid_phase<ShWo, ShQkv>(acc, pre, so, seg_qkv(pk.qkv, g + 1, w), Qs, QLD,
+                             cache_store<ShWo::NKB>(A, g, p0, Ks, Vts, kc, vc, keep));
   } else {   // the staging area is free now: it receives the LayerNorm parameters
     const LnParams q = ln_params_load(L.ln1_g, L.ln1_b);
-    resid_phase<ShWoL, ShF1>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD);
-    if (keep) cache_store(A, g, p0, Ks, Vts, kc, vc);
+    resid_phase<ShWoL, ShF1>(acc, pre, so, seg_ffn1(pk.w1, 0, w), Qs, QLD,
+                             cache_store<ShWoL::NKB>(A, g, p0, Ks, Vts, kc, vc, keep));
     ln_params_store(q, reinterpret_cast<float*>(Kc));
   }
   __syncthreads();   // Qs (O) and Ks / Vts are rewritten by the next group
