@@ -1297,40 +1297,42 @@ __global__ __launch_bounds__(NT) void encoder_fused_kernel(Args A) {
 
 // ---------------------------------------------------------------- candidate half
 // cvec[i] = c W_in[:, d:]^T + b_in for candidates c0 + i (the candidate's part of
-// the Eq. 4 input projection, the same for every position of the candidate);
-// CB candidates per workgroup (enough workgroups to cover the chip), thread f
-// computes output feature f.
-constexpr int CB = 4;
-__global__ __launch_bounds__(DM) void cand_proj_kernel(const bf16_t* __restrict__ cand,
-                                                       const bf16_t* __restrict__ W_in,
-                                                       const float* __restrict__ b_in, int d,
-                                                       int64_t c0, int64_t nc,
-                                                       float* __restrict__ cvec) {
-  __shared__ float cs[CB][KIN];
-  const int64_t base = int64_t(blockIdx.x) * CB;
-  const int nb = nc - base < CB ? int(nc - base) : CB;
-  for (int e = threadIdx.x; e < CB * d; e += DM) {
-    const int r = e / d, c = e % d;
-    cs[r][c] = r < nb ? bf2f(cand[(c0 + base + r) * d + c]) : 0.f;
+// the Eq. 4 input projection, the same for every position of the candidate): one
+// 32 x 32 MFMA tile (32 candidates x 32 features) per single-wave workgroup, every
+// k-block's operands loaded up front (A: candidate rows, B: W_in rows, both 16
+// bytes per lane straight from global memory).
+constexpr int CP_KB = KIN / 16;   // k-blocks at most (d <= KIN)
+__global__ __launch_bounds__(WAVE) void cand_proj_kernel(const bf16_t* __restrict__ cand,
+                                                         const bf16_t* __restrict__ W_in,
+                                                         const float* __restrict__ b_in, int d,
+                                                         int64_t c0, int64_t nc,
+                                                         float* __restrict__ cvec) {
+  const int lane = threadIdx.x;
+  const int hf = lane / 32, l32 = lane % 32;
+  const int64_t nb = int64_t(blockIdx.x) * 32;    // first candidate of the tile
+  const int f0 = blockIdx.y * 32;                 // first feature
+  int64_t ci = nb + l32;
+  ci = ci < nc ? ci : nc - 1;                     // rows past the chunk: clamped, not stored
+  const bf16_t* arow = cand + (c0 + ci) * d + 8 * hf;
+  const bf16_t* brow = W_in + int64_t(f0 + l32) * 2 * d + d + 8 * hf;
+  const int nkb = (d + 15) / 16;
+  bf16x8 a[CP_KB], b[CP_KB];
+#pragma unroll
+  for (int kb = 0; kb < CP_KB; ++kb) {
+    const bool ok = kb < nkb && 16 * kb + 8 * hf < d;   // d is a multiple of 8
+    a[kb] = ok ? as_bf16x8(*reinterpret_cast<const uint4*>(arow + 16 * kb)) : bf16x8{};
+    b[kb] = ok ? as_bf16x8(*reinterpret_cast<const uint4*>(brow + 16 * kb)) : bf16x8{};
   }
-  __syncthreads();
-  const int f = threadIdx.x;
-  float acc[CB];
+  f32x16 acc = f32x16{};
 #pragma unroll
-  for (int r = 0; r < CB; ++r) acc[r] = b_in[f];
-  const bf16_t* wr = W_in + int64_t(f) * 2 * d + d;
-#pragma unroll 4
-  for (int j = 0; j < d; j += 8) {
-    const uint4 wv = *reinterpret_cast<const uint4*>(wr + j);
-    const bf16_t* wp = reinterpret_cast<const bf16_t*>(&wv);
+  for (int kb = 0; kb < CP_KB; ++kb)
+    if (kb < nkb) acc = mfma32(a[kb], b[kb], acc);
+  const float bias = b_in[f0 + l32];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float wf = bf2f(wp[u]);
-#pragma unroll
-      for (int r = 0; r < CB; ++r) acc[r] = fmaf(wf, cs[r][j + u], acc[r]);
-    }
+  for (int r = 0; r < 16; ++r) {
+    const int64_t n = nb + 8 * (r / 4) + 4 * hf + (r % 4);
+    if (n < nc) cvec[n * DM + f0 + l32] = acc[r] + bias;
   }
-  for (int r = 0; r < nb; ++r) cvec[(base + r) * DM + f] = acc[r];
 }
 
 // ---------------------------------------------------------------- weight packing
@@ -1531,8 +1533,8 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
     a.c0 = c0;
     {
       ProfScope prof("cand_proj", st);
-      fz::cand_proj_kernel<<<unsigned(cdiv(nc, fz::CB)), fz::DM, 0, st>>>(
-          a.cand, a.W_in, a.b_in, d, c0, nc, cvec);
+      fz::cand_proj_kernel<<<dim3(unsigned(cdiv(nc, 32)), unsigned(fz::DM / 32)), WAVE, 0,
+                             st>>>(a.cand, a.W_in, a.b_in, d, c0, nc, cvec);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
