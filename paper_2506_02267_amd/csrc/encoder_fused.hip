@@ -1352,22 +1352,19 @@ struct PackJob {
   int kvalid;        // job columns >= kvalid are zero
   int trans;         // destination (row r, job column k) = src[k * ld + r] instead of src[r * ld + k]
   const float* bias; // non-null: a bias job (one k-block)
-  int64_t first;     // first item (16-byte piece) of this job
 };
 constexpr int MAX_JOBS = 4 + 8 * MAX_LAYERS;
 struct PackArgs {
   PackJob job[MAX_JOBS];
   int njobs;
-  int64_t items;
 };
 
+// Grid: (workgroups of the largest job) x (jobs); blockIdx.y names the job, so its
+// fields are scalar loads, and the workgroups past a smaller job's end return.
 __global__ __launch_bounds__(256) void pack_weights_kernel(PackArgs P) {
-  const int64_t it = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (it >= P.items) return;
-  int j = 0;
-  while (j + 1 < P.njobs && it >= P.job[j + 1].first) ++j;
-  const PackJob& J = P.job[j];
-  const int64_t e = it - J.first;               // piece within the job
+  const PackJob& J = P.job[blockIdx.y];
+  const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;   // piece within the job
+  if (e >= int64_t(J.rows) * J.nkbj * 2) return;
   const int lane = int(e % 64);
   const int64_t frag = e / 64;
   const int rt = int(frag / J.nkbj), kbj = int(frag % J.nkbj);
@@ -1443,7 +1440,7 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
   // ---- pack every matrix into fragment order (head of the workspace)
   bf16_t* pk = static_cast<bf16_t*>(ws);
   fz::PackArgs P{};
-  int64_t items = 0;
+  int64_t maxwg = 0;   // workgroups of the largest job
   size_t off = 0;
   // matrix m of rows x (16 nkb) columns at fragment `off`; add_cols fills k-blocks
   // [kb0, kb0 + nkbj) from a row-major (or transposed) source
@@ -1460,8 +1457,8 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
     J.kvalid = kvalid;
     J.trans = trans;
     J.bias = nullptr;
-    J.first = items;
-    items += int64_t(rows) * nkbj * 2;   // 16-byte pieces: 2 per row per k-block
+    // 16-byte pieces: 2 per row per k-block, one per thread
+    maxwg = std::max(maxwg, (int64_t(rows) * nkbj * 2 + 255) / 256);
   };
   // matrix of rows x K (row-major source), followed by a bias k-block if bias
   auto add = [&](const void* srcm, int rows, int K, int ld, int kvalid,
@@ -1500,10 +1497,9 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
   a.pos_nkb = pos_cols(w) / 16;
   add_cols(off, dm, pos_cols(w) / 16, 0, pos_cols(w) / 16, w.E_pos, dm, w.max_pos, 1);
   off += size_t(dm) * pos_cols(w);
-  P.items = items;
   {
     ProfScope prof("pack_weights", st);
-    fz::pack_weights_kernel<<<unsigned(cdiv(items, 256)), 256, 0, st>>>(P);
+    fz::pack_weights_kernel<<<dim3(unsigned(maxwg), unsigned(P.njobs)), 256, 0, st>>>(P);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
