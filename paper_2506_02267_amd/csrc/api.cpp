@@ -167,7 +167,7 @@ tav2_status tav2_nn_select(const tav2_seq* seq, const tav2_cands* cands, int32_t
   float* scores = static_cast<float*>(ws);
   const int64_t ld = score_ld(seq->max_len);
   hipError_t e = launch_scores(*seq, *cands, scores, ld, s);
-  if (e == hipSuccess) e = launch_topk(*seq, *cands, scores, ld, k, out_idx, out_score, s);
+  if (e == hipSuccess) e = launch_topk(*seq, *cands, scores, ld, k, out_idx, out_score, nullptr, s);
   return hip_status(e);
 }
 
@@ -248,8 +248,8 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt, const ta
   void* enc_ws = base + sel_b + req_b;
   const int64_t ld = score_ld(seq->max_len);
   hipError_t e = launch_scores(*seq, *cands, scores, ld, s);
-  if (e == hipSuccess) e = launch_topk(*seq, *cands, scores, ld, k, out_idx, out_score, s);
-  if (e == hipSuccess) e = launch_cand_request(*cands, seq->num_requests, cand_req, s);
+  if (e == hipSuccess)
+    e = launch_topk(*seq, *cands, scores, ld, k, out_idx, out_score, cand_req, s);
   if (e != hipSuccess) return TAV2_ERR_HIP;
   TokenSource src{};
   src.explicit_tokens = false;

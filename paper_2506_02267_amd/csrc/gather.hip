@@ -9,13 +9,6 @@
 
 namespace tav2 {
 
-__global__ __launch_bounds__(256) void cand_request_kernel(const int64_t* __restrict__ off,
-                                                           int32_t* __restrict__ cand_req) {
-  const int r = blockIdx.y;
-  const int64_t n = off[r] + int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (n < off[r + 1]) cand_req[n] = r;
-}
-
 __global__ __launch_bounds__(256) void gather_kernel(
     const uint8_t* __restrict__ seq_emb, const uint8_t* __restrict__ seq_act,
     const uint8_t* __restrict__ seq_time, const int64_t* __restrict__ seq_off,
@@ -58,14 +51,6 @@ __global__ __launch_bounds__(256) void gather_kernel(
     if (tok_time) tok_time[n * T + p] = t;
   }
   if (threadIdx.x == 0) valid_len[n] = t_ll + lrt;
-}
-
-hipError_t launch_cand_request(const tav2_cands& c, int R, int32_t* cand_req, hipStream_t st) {
-  if (R == 0 || c.total == 0) return hipSuccess;
-  dim3 grid(unsigned(cdiv(c.max_count, 256)), unsigned(R));
-  ProfScope prof("cand_request", st);
-  cand_request_kernel<<<grid, 256, 0, st>>>(c.offset, cand_req);
-  return hipGetLastError();
 }
 
 hipError_t launch_gather(const tav2_seq& seq, const tav2_seq* rt, const tav2_cands& c,

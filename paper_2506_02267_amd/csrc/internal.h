@@ -30,8 +30,10 @@ class ProfScope {
 int64_t score_ld(int32_t max_len);
 hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores, int64_t ld,
                          hipStream_t st);
+// cand_req (nullable): also receives each candidate's request index.
 hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* scores, int64_t ld,
-                       int k, int32_t* out_idx, float* out_score, hipStream_t st);
+                       int k, int32_t* out_idx, float* out_score, int32_t* cand_req,
+                       hipStream_t st);
 
 // ---- gather.hip
 // Where encoder tokens come from: either explicit token tensors, or the
@@ -61,7 +63,6 @@ struct TokenSource {
   bool explicit_tokens;
 };
 
-hipError_t launch_cand_request(const tav2_cands& c, int R, int32_t* cand_req, hipStream_t st);
 hipError_t launch_gather(const tav2_seq& seq, const tav2_seq* rt, const tav2_cands& c,
                          const int32_t* idx, int k, int T, void* tok_emb, uint8_t* tok_act,
                          uint8_t* tok_time, int32_t* valid_len, hipStream_t st);
