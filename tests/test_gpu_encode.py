@@ -45,6 +45,15 @@ def test_small_bf16_all_candidates():
     check_workload(w)
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_small_bf16_narrow_embedding(d):
+    # token / candidate embeddings narrower than d_model: the input projection's
+    # token half is zero-padded to 256 columns, its candidate half is a shorter
+    # contraction
+    w = synth.scaled(synth.SINGLE, R=2, L=1500, N=20, k=64, d=d)
+    check_workload(w)
+
+
 def test_small_bf16_eight_heads_ragged_tail():
     # T = 40 + 0 (not a multiple of 32), 8 heads of 32
     w = synth.scaled(synth.STRESS, R=3, L=900, N=10, k=40, tie_frac=0.01)
