@@ -226,9 +226,10 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt,
  * After the caller has synchronised, tav2_profile_report() writes one line
  * "<site> <launches> <total_ms>" per site into buf (NUL-terminated, truncated
  * to buf_bytes), forgets the recorded launches and returns the untruncated
- * text length.  Site names: score_bf16, score_f32, topk, cand_request, gather,
- * gemm_cand, gemm_embed, gemm_qkv, attention, gemm_oproj_ln1, gemm_ffn1,
- * gemm_ffn2_ln2, fill, gemm_pool, pool_finalize, encode_f32.
+ * text length.  Site names: score_bf16, score_f32, topk, gather, pack_weights,
+ * cand_proj, encoder_fused (the fused bf16 encoder), gemm_cand, gemm_embed,
+ * gemm_qkv, attention, gemm_oproj_ln1, gemm_ffn1, gemm_ffn2_ln2, fill, gemm_pool,
+ * pool_finalize (the layer-wise bf16 encoder), encode_f32.
  */
 int32_t tav2_profile_enable(int32_t on, const char* only_site);
 int64_t tav2_profile_report(char* buf, size_t buf_bytes);
