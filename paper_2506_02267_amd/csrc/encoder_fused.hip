@@ -257,16 +257,11 @@ __device__ __forceinline__ WSeg seg_ffn1(int P, int c, int w) {
   const int r = c * (FC / 32) + 2 * w;
   return WSeg{P, NKB_W, 0, r, r + 1, 0, 0};
 }
-// Q / K / V of head group g: column tiles 3(w >> 1) + 0..2 of [q0 q1 k0 k1 v0 v1]
-// are packed row tiles 8 part + 2g + dt
+// Q / K / V of head group g for wave w: q_d, k_d, v_d (d = w >> 1) are the packed
+// row tiles 8 part + 2g + d of [W_q | W_k | W_v] (part 0, 1, 2)
 __device__ __forceinline__ WSeg seg_qkv(int P, int g, int w) {
-  int r[3];
-#pragma unroll
-  for (int t = 0; t < 3; ++t) {
-    const int ct = 3 * (w >> 1) + t;
-    r[t] = 8 * (ct >> 1) + 2 * g + (ct & 1);
-  }
-  return WSeg{P, NKB_W, 0, r[0], r[1], r[2], 0};
+  const int d = w >> 1;
+  return WSeg{P, NKB_W, 0, 2 * g + d, 8 + 2 * g + d, 16 + 2 * g + d, 0};
 }
 
 // Iteration of phase Cur after whose MFMAs slot i of the next phase's look-ahead
@@ -924,17 +919,14 @@ __device__ __forceinline__ int vpos(int k) {
 }
 
 // Q / K / V of head group g: wave w computes token tiles 2(w & 1), 2(w & 1) + 1 of
-// column tiles 3 CS .. +2 of [q0 q1 k0 k1 v0 v1] (CS = w >> 1); Q and K
-// transposed ([dim][token]), V untransposed.  Leaves the look-ahead empty.  The
-// column split is a template parameter so that each wave runs a branch-free
-// loop with fixed accumulator registers.
-template <int CS>
+// the column tiles q_d, k_d, v_d (d = w >> 1, 32 dims each) — one tile of each,
+// so every wave's epilogue writes the same amount; Q and K transposed
+// ([dim][token]), V untransposed.  Leaves the look-ahead empty.
 __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg& nxt,
                                           const bf16_t* Xs, bf16_t* Qs, bf16_t* Ks, bf16_t* Vts) {
   FZ_LANE_VARS
   constexpr int NKB = ShQkv::NKB;
-  constexpr int cs = CS;
-  const int tp = w & 1;
+  const int tp = w & 1, dt = w >> 1;
   f32x16 qa[3][2];
 #pragma unroll
   for (int t = 0; t < 3; ++t) qa[t][0] = qa[t][1] = f32x16{};
@@ -951,47 +943,35 @@ __device__ __forceinline__ void qkv_phase(Pre& pre, const WSeg& cur, const WSeg&
     } else if (j + 1 < NKB) {   // the bias k-block (also as the A operand of V)
       xq[j + 1][0] = xq[j + 1][1] = bias_ones();
     }
-    if constexpr (CS == 0) {   // q0 q1 k0: transposed
 #pragma unroll
-      for (int t = 0; t < 3; ++t) {
-        const bf16x8 a = stream_frag<ShQkv>(wq, pre, j, t);
-        qa[t][0] = mfma32(a, xq[j][0], qa[t][0]);
-        qa[t][1] = mfma32(a, xq[j][1], qa[t][1]);
-      }
-    } else {         // k1 transposed; v0 v1 untransposed
-      const bf16x8 a0 = stream_frag<ShQkv>(wq, pre, j, 0);
-      qa[0][0] = mfma32(a0, xq[j][0], qa[0][0]);
-      qa[0][1] = mfma32(a0, xq[j][1], qa[0][1]);
-#pragma unroll
-      for (int t = 1; t < 3; ++t) {
-        const bf16x8 a = stream_frag<ShQkv>(wq, pre, j, t);
-        qa[t][0] = mfma32(xq[j][0], a, qa[t][0]);
-        qa[t][1] = mfma32(xq[j][1], a, qa[t][1]);
-      }
+    for (int t = 0; t < 2; ++t) {   // q_d, k_d: transposed
+      const bf16x8 a = stream_frag<ShQkv>(wq, pre, j, t);
+      qa[t][0] = mfma32(a, xq[j][0], qa[t][0]);
+      qa[t][1] = mfma32(a, xq[j][1], qa[t][1]);
+    }
+    {                               // v_d: untransposed
+      const bf16x8 a = stream_frag<ShQkv>(wq, pre, j, 2);
+      qa[2][0] = mfma32(xq[j][0], a, qa[2][0]);
+      qa[2][1] = mfma32(xq[j][1], a, qa[2][1]);
     }
     stream_fetch<ShQkv, NoPhase>(wq, pre, cur, nxt, j, lane);
     sched_fence();
   }
 #pragma unroll
-  for (int t = 0; t < 3; ++t) {
-    const int ct = 3 * cs + t;
-    const int part = ct >> 1, dt = ct & 1;
+  for (int u = 0; u < 2; ++u) {
+    const int tt = 2 * tp + u;
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int tt = 2 * tp + u;
-      if (part < 2) {
-        bf16_t* dst = part == 0 ? Qs : Ks;
+    for (int t = 0; t < 2; ++t) {
+      bf16_t* dst = t == 0 ? Qs : Ks;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          st4(dst + (tt * 32 + l32) * QLD + dt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j],
-              qa[t][u][4 * j + 1], qa[t][u][4 * j + 2], qa[t][u][4 * j + 3]);
-      } else {
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + vpos(8 * j + 4 * hf), qa[t][u][4 * j],
-              qa[t][u][4 * j + 1], qa[t][u][4 * j + 2], qa[t][u][4 * j + 3]);
-      }
+      for (int j = 0; j < 4; ++j)
+        st4(dst + (tt * 32 + l32) * QLD + dt * 32 + 8 * j + 4 * hf, qa[t][u][4 * j],
+            qa[t][u][4 * j + 1], qa[t][u][4 * j + 2], qa[t][u][4 * j + 3]);
     }
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      st4(Vts + (dt * 32 + l32) * VLD + tt * 32 + vpos(8 * j + 4 * hf), qa[2][u][4 * j],
+          qa[2][u][4 * j + 1], qa[2][u][4 * j + 2], qa[2][u][4 * j + 3]);
   }
 }
 
@@ -1113,10 +1093,7 @@ __device__ __forceinline__ void attention_group(const Args& A, const tav2_layer&
   // the group's 4 k-blocks)
   using Wo = typename std::conditional<LAST, ShWoL, ShWo>::type;
   const WSeg so = seg_resid(pk.o, NKB_W, 4 * g, w);
-  if (w < 2)
-    qkv_phase<0>(pre, seg_qkv(pk.qkv, g, w), so, Xs, Qs, Ks, Vts);
-  else
-    qkv_phase<1>(pre, seg_qkv(pk.qkv, g, w), so, Xs, Qs, Ks, Vts);
+  qkv_phase(pre, seg_qkv(pk.qkv, g, w), so, Xs, Qs, Ks, Vts);
   __syncthreads();
   // the output projection's look-ahead is loaded during the attention
   const auto prime = [&] { seg_prime<Wo>(pre, so, otid() % WAVE); };
