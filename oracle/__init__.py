@@ -17,9 +17,11 @@ selection invariants, the encoder against torch's own post-LN
 TransformerEncoderLayer in float64, the single-token closed form, causal prefix
 invariance, head-permutation invariance and the Eq. 4 special case.
 """
-from .nn_select import exact_scores, nn_select, nn_select_batch, token_positions, gather_tokens
+from .nn_select import (exact_scores, nn_select, nn_select_batch, token_positions, gather_tokens,
+                        normalised_scores, nn_select_i8)
 from .encoder import feature_encode, encoder_layer, pool, encode, encode_states, select_encode
 
 __all__ = ["exact_scores", "nn_select", "nn_select_batch", "token_positions", "gather_tokens",
+           "normalised_scores", "nn_select_i8",
            "feature_encode", "encoder_layer", "pool", "encode", "encode_states",
            "select_encode"]

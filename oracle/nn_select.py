@@ -61,6 +61,51 @@ def rank_order(s: np.ndarray) -> np.ndarray:
     return np.argsort(-s, axis=1, kind="stable")
 
 
+def normalised_scores(Q: np.ndarray, C: np.ndarray) -> np.ndarray:
+    """Scores over the int8 sequence storage with dequantisation and L2
+    normalisation (Sec. 3.4.2, fused sequence dequantisation; codes of Sec. 3.1).
+
+    Row i dequantises to e_i = (0.65 / 127) q_i and is normalised to unit length
+    before the dot product of Eq. 3, so s[n, i] = <e_i / |e_i|, c_n>; the scale
+    cancels and s[n, i] = <q_i, c_n> / |q_i|.  An all-zero row scores 0.
+    Precision (the paper gives none for this step): the dot product and the sum
+    of squares exactly, then one float32 square root and one float32 division,
+    each rounded to nearest.  Returns float32 [n, L].
+    """
+    Q = np.asarray(Q)
+    n, L = C.shape[0], Q.shape[0]
+    if n == 0 or L == 0:
+        return np.zeros((n, L), dtype=np.float32)
+    dot = exact_scores(Q.astype(np.float64), C)
+    dot32 = dot.astype(np.float32)
+    if not np.array_equal(dot32.astype(np.float64), dot):
+        raise ValueError("dot products not exact in float32: the rounding order would matter")
+    sq = np.sum(Q.astype(np.int64) ** 2, axis=1)
+    if sq.max() >= 2 ** 24:
+        raise ValueError("sum of squares not exact in float32")
+    norm = np.sqrt(sq.astype(np.float32))                  # one rounding
+    safe = np.where(sq > 0, norm, np.float32(1.0)).astype(np.float32)
+    s = (dot32 / safe[None, :]).astype(np.float32)         # one rounding
+    return np.where(sq[None, :] > 0, s, np.float32(0.0)).astype(np.float32)
+
+
+def _select(s: np.ndarray, k: int) -> Tuple[np.ndarray, np.ndarray]:
+    """The first k rows of each score row in the total order, padded."""
+    if k < 1:
+        raise ValueError("k must be >= 1")
+    n, L = s.shape
+    idx = np.full((n, k), -1, dtype=np.int32)
+    score = np.full((n, k), -np.inf, dtype=np.float32)
+    if n == 0 or L == 0:
+        return idx, score
+    order = rank_order(s)[:, :min(k, L)]
+    m = order.shape[1]
+    idx[:, :m] = order
+    top = np.take_along_axis(s, order, axis=1) + 0.0   # -0.0 -> +0.0
+    score[:, :m] = top.astype(np.float32)
+    return idx, score
+
+
 def nn_select(E: np.ndarray, C: np.ndarray, k: int) -> Tuple[np.ndarray, np.ndarray]:
     """Top-k rows of one request's sequence for each of its candidates.
 
@@ -70,18 +115,15 @@ def nn_select(E: np.ndarray, C: np.ndarray, k: int) -> Tuple[np.ndarray, np.ndar
     """
     if k < 1:
         raise ValueError("k must be >= 1")
-    n, L = C.shape[0], E.shape[0]
-    idx = np.full((n, k), -1, dtype=np.int32)
-    score = np.full((n, k), -np.inf, dtype=np.float32)
-    if n == 0 or L == 0:
-        return idx, score
-    s = exact_scores(E, C)
-    order = rank_order(s)[:, :min(k, L)]
-    m = order.shape[1]
-    idx[:, :m] = order
-    top = np.take_along_axis(s, order, axis=1) + 0.0   # -0.0 -> +0.0
-    score[:, :m] = top.astype(np.float32)
-    return idx, score
+    return _select(exact_scores(E, C), k)
+
+
+def nn_select_i8(Q: np.ndarray, C: np.ndarray, k: int) -> Tuple[np.ndarray, np.ndarray]:
+    """nn_select over int8 codes, ranked by normalised_scores (float32 values,
+    compared exactly)."""
+    if k < 1:
+        raise ValueError("k must be >= 1")
+    return _select(normalised_scores(Q, C).astype(np.float64), k)
 
 
 def nn_select_batch(seq, cand: np.ndarray, cand_offset: np.ndarray, k: int,
@@ -106,7 +148,7 @@ def nn_select_batch(seq, cand: np.ndarray, cand_offset: np.ndarray, k: int,
         if ids.size == 0:
             continue
         E = seq.emb[seq.rows(r)]
-        i, s = nn_select(E, cand[ids], k)
+        i, s = (nn_select_i8 if E.dtype == np.int8 else nn_select)(E, cand[ids], k)
         idx[ids], score[ids] = i, s
     return idx, score
 

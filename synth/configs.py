@@ -18,7 +18,8 @@ from typing import Optional, Tuple
 class Workload:
     cid: int                      # 1..5, also the data seed
     name: str
-    dtype: str                    # "f32" or "bf16": storage and MFMA operand type
+    dtype: str                    # "f32" or "bf16": storage and MFMA operand type; "i8":
+                                  # int8 sequence codes, bf16 candidates (NN search only)
     R: int                        # requests (users) in one batch
     L: Optional[int]              # lifelong length per request (fixed), or None
     L_range: Optional[Tuple[int, int]]  # inclusive [lo, hi] when ragged
@@ -65,7 +66,13 @@ STRESS = Workload(5, "stress_bf16", "bf16", R=16, L=16384, L_range=None, d=256, 
                   tie_frac=0.01)
 
 WORKLOADS = {w.cid: w for w in (TINY, SINGLE, RAGGED, MIXED, STRESS)}
-BY_NAME = {w.name: w for w in WORKLOADS.values()}
+# NN search over the paper's int8 sequence storage (32-d codes, Sec. 3.1) with
+# dequantisation and L2 normalisation fused into the score kernel (Sec. 3.4.2);
+# one request of the single workload's size.  The encoder fields are unused.
+SELECT_I8 = Workload(6, "select_i8", "i8", R=1, L=16384, L_range=None, d=32, N=1000, k=256,
+                     d_model=256, n_heads=4, d_ffn=1024, n_layers=2, has_time=True,
+                     tie_frac=0.01)
+BY_NAME = {w.name: w for w in list(WORKLOADS.values()) + [SELECT_I8]}
 
 
 def scaled(w: Workload, **changes) -> Workload:

@@ -46,6 +46,15 @@ def grid_values(rng: np.random.Generator, shape) -> np.ndarray:
     return (rng.integers(-8, 9, size=shape).astype(np.float32) / np.float32(8.0))
 
 
+def int8_codes(rng: np.random.Generator, shape) -> np.ndarray:
+    """Codes of the int8 embedding storage (Sec. 3.1, Eq. 1's quantised sequence
+    features): rows drawn as random unit vectors, scaled by 127 / 0.65, rounded half
+    to even and clamped to [-127, 127].  Returns int8."""
+    e = rng.standard_normal(shape)
+    e /= np.maximum(np.linalg.norm(e, axis=-1, keepdims=True), 1e-30)
+    return np.clip(np.rint(e * (127.0 / 0.65)), -127, 127).astype(np.int8)
+
+
 @dataclass
 class SeqBatch:
     """A de-duplicated request-level sequence batch: rows of all requests stored once.
@@ -130,18 +139,18 @@ class Weights:
         return len(self.layers)
 
 
-def _draw_seq(rng, lengths, d, has_time, tie_frac) -> SeqBatch:
+def _draw_seq(rng, lengths, d, has_time, tie_frac, codes=False) -> SeqBatch:
     R = len(lengths)
     offset = np.zeros(R, dtype=np.int64)
     if R > 1:
         offset[1:] = np.cumsum(np.asarray(lengths, dtype=np.int64))[:-1]
     rows = int(np.sum(lengths))
-    emb = np.empty((rows, d), dtype=np.float32)
+    emb = np.empty((rows, d), dtype=np.int8 if codes else np.float32)
     act = np.empty(rows, dtype=np.uint8)
     time = np.empty(rows, dtype=np.uint8) if has_time else None
     for r, L in enumerate(lengths):
         o = int(offset[r])
-        e = grid_values(rng, (L, d))
+        e = int8_codes(rng, (L, d)) if codes else grid_values(rng, (L, d))
         if tie_frac > 0.0 and L > 1:
             n_dup = max(1, int(L * tie_frac))
             dst = rng.choice(L, size=n_dup, replace=False)
@@ -163,7 +172,7 @@ def make_inputs(w: Workload, seed: Optional[int] = None) -> Inputs:
         lengths = [int(x) for x in rng.integers(lo, hi + 1, size=w.R)]
     else:
         lengths = [w.L] * w.R
-    seq = _draw_seq(rng, lengths, w.d, w.has_time, w.tie_frac)
+    seq = _draw_seq(rng, lengths, w.d, w.has_time, w.tie_frac, codes=(w.dtype == "i8"))
     cand = grid_values(rng, (w.R * w.N, w.d))
     cand_offset = np.arange(w.R + 1, dtype=np.int64) * w.N
     rt = None

@@ -195,3 +195,72 @@ def test_empty_request_and_no_candidates():
     assert np.all(idx == -1) and np.all(np.isneginf(score))
     idx, score = oracle.nn_select(np.ones((5, 8), np.float32), np.zeros((0, 8), np.float32), 4)
     assert idx.shape == (0, 4)
+
+
+# ---------------------------------------------------------------- int8 storage
+# Scores over int8 codes with dequantisation and L2 normalisation (Sec. 3.4.2,
+# fused sequence dequantisation; the codes of Sec. 3.1).
+
+def test_normalised_closed_forms():
+    """Hand-computed values: <q, c> / |q| with |q| a perfect square root."""
+    Q = np.zeros((5, 16), dtype=np.int8)
+    Q[0, :2] = [3, 4]                 # |q| = 5
+    Q[1, :4] = [1, 1, 1, 1]           # |q| = 2
+    Q[2, 0] = -127                    # |q| = 127
+    Q[4, :2] = [-4, 3]                # |q| = 5; row 3 stays zero
+    C = np.zeros((1, 16), dtype=np.float32)
+    C[0, :4] = [1.0, 1.0, 0.5, 0.5]
+    s = oracle.normalised_scores(Q, C)
+    assert s.dtype == np.float32
+    assert s[0, 0] == np.float32(7.0) / np.float32(5.0)      # 1.4 rounded once
+    assert s[0, 1] == np.float32(1.5)                          # (1 + 1 + .5 + .5) / 2
+    assert s[0, 2] == np.float32(-1.0)
+    assert s[0, 3] == 0.0                                      # all-zero row
+    assert s[0, 4] == np.float32(-0.2)                         # (-4 + 3) / 5
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_normalised_scores_match_the_dequantised_definition(seed):
+    """Against Sec. 3.4.2 written out in float64: dequantise with the 0.65 / 127
+    scale, divide each row by its length, dot with the candidate.  Two roundings
+    to float32 bound the difference by about 2 ulp of the score."""
+    rng = np.random.default_rng(seed)
+    Q = synth.int8_codes(rng, (300, 32))
+    C = synth.generate.grid_values(rng, (7, 32))
+    s = oracle.normalised_scores(Q, C).astype(np.float64)
+    E = Q.astype(np.float64) * (0.65 / 127.0)
+    Eh = E / np.linalg.norm(E, axis=1, keepdims=True)
+    ref = C.astype(np.float64) @ Eh.T
+    assert np.all(np.abs(s - ref) <= 2.5 * 2.0 ** -24 * np.abs(ref) + 1e-12)
+    # the normalisation is what ranks: the raw dot product ranks differently
+    raw = oracle.exact_scores(Q.astype(np.float64), C)
+    assert not np.array_equal(np.argsort(-raw, axis=1), np.argsort(-ref, axis=1))
+
+
+@pytest.mark.parametrize("seed", [3, 4])
+def test_i8_select_is_brute_force_order_of_normalised_scores(seed):
+    rng = np.random.default_rng(seed)
+    Q = synth.int8_codes(rng, (40, 16))
+    Q[[5, 17]] = Q[9]                      # ties: equal rows rank by index
+    Q[11] = 0
+    C = synth.generate.grid_values(rng, (6, 16))
+    s = oracle.normalised_scores(Q, C)
+    for k in (1, 7, 40, 45):
+        idx, sc = oracle.nn_select_i8(Q, C, k)
+        for n in range(C.shape[0]):
+            want = sorted(range(40), key=lambda i: (-float(s[n, i]), i))[:k]
+            got = [int(i) for i in idx[n] if i >= 0]
+            assert got == want
+            assert np.array_equal(sc[n, :len(want)], s[n, want] + np.float32(0.0))
+            assert np.all(sc[n, len(want):] == -np.inf)
+
+
+def test_i8_batch_uses_each_requests_rows():
+    w = synth.scaled(synth.SELECT_I8, R=3, L=None, L_range=(5, 60), N=4, k=8)
+    inp = synth.make_inputs(w, seed=11)
+    assert inp.seq.emb.dtype == np.int8
+    idx, sc = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, w.k)
+    for r in range(w.R):
+        a, b = int(inp.cand_offset[r]), int(inp.cand_offset[r + 1])
+        i1, s1 = oracle.nn_select_i8(inp.seq.emb[inp.seq.rows(r)], inp.cand[a:b], w.k)
+        assert np.array_equal(idx[a:b], i1) and np.array_equal(sc[a:b], s1)
