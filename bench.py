@@ -25,6 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "candidates scored/sec at L=16k (NN-select+encode); % MFMA / HBM roofline"
+METRIC_SELECT = "candidates NN-selected/sec at L=16k over int8 codes (fused dequant + L2 norm)"
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3       # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
@@ -60,6 +61,8 @@ def site_work(w, total, valid_tokens, max_len, launches_per_step):
                             + 2.0 * M * dm * dm)
     per["score_bf16"] = ("flop", 2.0 * total * max_len * d)
     per["score_f32"] = ("flop", 2.0 * total * max_len * d)
+    # int8 storage: the score rows written dominate (d = 32 codes per row)
+    per["score_i8"] = ("byte", 4.0 * total * max_len + max_len * d * w.R + 2.0 * total * d)
     per["topk"] = ("byte", 4.0 * total * max_len)
     out = {}
     for site, (kind, amount) in per.items():
@@ -99,6 +102,22 @@ def measured_traffic(site, workload):
     return float(fields["hbm_bytes_per_launch"])
 
 
+def cpu_baseline_select(inp, k):
+    """The oracle's NN search, untuned, over every candidate of the workload."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
+    t_sel = time.perf_counter() - t0
+    return {"value": inp.total / t_sel, "unit": "candidates/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"NN search of all {inp.total} candidates ({t_sel:.2f} s), numpy"}
+
+
 def cpu_baseline(inp, W, k, budget_s):
     """The oracle, untuned, on a bounded sample of the same workload."""
     import oracle
@@ -136,7 +155,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="single_bf16",
-                    help="tiny_f32 | single_bf16 | ragged_bf16 | mixed_bf16 | stress_bf16")
+                    help="tiny_f32 | single_bf16 | ragged_bf16 | mixed_bf16 | stress_bf16 | "
+                         "select_i8 (the NN search alone over int8 codes)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle encoder work in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -156,12 +176,22 @@ def main():
 
     w = synth.BY_NAME[args.workload]
     inp = synth.make_inputs(w)
-    W = synth.make_weights(w)
-    dt = T.BF16 if w.dtype == "bf16" else T.F32
+    select_only = w.dtype == "i8"
+    W = None if select_only else synth.make_weights(w)
+    dt = {"bf16": T.BF16, "i8": T.I8}.get(w.dtype, T.F32)
     seq = T.DeviceSeq.from_host(inp.seq, dt)
     rt = T.DeviceSeq.from_host(inp.rt, dt) if inp.rt is not None else None
     cands = T.DeviceCands.from_host(inp.cand, inp.cand_offset, dt)
-    call = T.SelectEncode(seq, rt, cands, w.k, T.DeviceWeights(W))
+    if select_only:
+        # one step = tav2_nn_select over the whole batch (outputs and workspace reused)
+        out_idx = torch.empty((inp.total, w.k), dtype=torch.int32, device="cuda")
+        out_score = torch.empty((inp.total, w.k), dtype=torch.float32, device="cuda")
+        ws = T.Workspace(torch.device("cuda"))
+
+        def call():
+            T.nn_select(seq, cands, w.k, out_idx, out_score, ws)
+    else:
+        call = T.SelectEncode(seq, rt, cands, w.k, T.DeviceWeights(W))
     stream = torch.cuda.current_stream()
     total = inp.total
     lengths = inp.seq.length.astype(np.int64)
@@ -215,7 +245,7 @@ def main():
     avg_s = dom_ms / max(cnt, 1) / 1000.0
     kind, amount = work.get(dominant, ("flop", 0.0))
     if kind == "flop":
-        peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+        peak = PEAK_BF16_TFLOPS if w.dtype in ("bf16", "i8") else PEAK_F32_TFLOPS
         achieved = amount / avg_s / 1e12 if avg_s > 0 else 0.0
         roof = {"bound": "mfma" if w.dtype == "bf16" else "alu", "achieved": round(achieved, 2),
                 "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
@@ -244,16 +274,22 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(inp, W, w.k, args.cpu_budget)
+        cpu = (cpu_baseline_select(inp, w.k) if select_only
+               else cpu_baseline(inp, W, w.k, args.cpu_budget))
 
     config = {"workload": w.name, "requests": w.R, "L": w.L if w.L else list(w.L_range),
-              "d": w.d, "candidates": total, "k": w.k, "rt_len": w.rt_len, "T": w.T,
-              "d_model": w.d_model, "heads": w.n_heads, "d_ffn": w.d_ffn, "layers": w.n_layers}
-    line = {"metric": METRIC, "value": round(value, 1), "unit": "candidates/s", "n_gpus": 1,
+              "d": w.d, "candidates": total, "k": w.k}
+    if not select_only:
+        config.update({"rt_len": w.rt_len, "T": w.T, "d_model": w.d_model, "heads": w.n_heads,
+                       "d_ffn": w.d_ffn, "layers": w.n_layers})
+    line = {"metric": METRIC_SELECT if select_only else METRIC, "value": round(value, 1),
+            "unit": "candidates/s", "n_gpus": 1,
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-            "dtype": "bf16" if w.dtype == "bf16" else "f32",
-            "data": "synthetic (seeded 1/8-grid embeddings, N(0,0.02) weights)",
+            "dtype": "bf16" if w.dtype in ("bf16", "i8") else "f32",
+            "data": ("synthetic (seeded int8 codes of random unit rows, 1/8-grid candidates)"
+                     if select_only else
+                     "synthetic (seeded 1/8-grid embeddings, N(0,0.02) weights)"),
             "config": config, "roofline": roof, "cpu_baseline": cpu}
     print(json.dumps(line), flush=True)
 

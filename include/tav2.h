@@ -60,6 +60,8 @@ typedef int32_t tav2_status;
 
 #define TAV2_F32  0   /* float32 storage and arithmetic */
 #define TAV2_BF16 1   /* bfloat16 storage, fp32 accumulation */
+#define TAV2_I8   2   /* int8 codes of the quantised sequence storage (Sec. 3.1): a
+                         sequence dtype for tav2_nn_select only, with bf16 candidates */
 
 #define TAV2_K_MAX     1024  /* largest k of the NN search */
 #define TAV2_T_MAX     1024  /* largest encoder sequence (k + real-time tail) */
@@ -80,13 +82,14 @@ typedef struct tav2_seq {
   const int32_t* len;          /* device [R]: rows of each request, 0 <= len[r] <= max_len */
   int32_t num_requests;        /* R >= 0 */
   int32_t d;                   /* embedding width, multiple of 16, 16..512 */
-  int32_t dtype;               /* TAV2_F32 or TAV2_BF16 */
+  int32_t dtype;               /* TAV2_F32, TAV2_BF16, or TAV2_I8 (tav2_nn_select only) */
   int32_t max_len;             /* host-side bound: len[r] <= max_len for every r */
 } tav2_seq;
 
 /* The candidate items of the same R requests, stored contiguously by request. */
 typedef struct tav2_cands {
-  const void*    emb;          /* device [total, d], same dtype and d as the sequence */
+  const void*    emb;          /* device [total, d], same dtype and d as the sequence
+                                  (bf16 when the sequence is TAV2_I8) */
   const int64_t* offset;       /* device [R + 1]: candidates of request r are
                                   [offset[r], offset[r+1]); offset[0] = 0, offset[R] = total */
   int64_t total;               /* host: number of candidates (>= 0) */
@@ -157,6 +160,13 @@ int32_t tav2_abi_version(void);
  *             k > len[r] (positions >= len[r]).
  *   out_score device [total, k] float32: the scores (fp32 accumulation; exact
  *             whenever the fp32 sum is exact), -inf in padded positions.
+ * A TAV2_I8 sequence holds int8 codes q (Sec. 3.1); each row is dequantised and
+ * L2-normalised before the dot product (Sec. 3.4.2, fused sequence
+ * dequantisation), all inside the score kernel: the dequantisation scale cancels
+ * and s[n, i] = <q_i, cand[n]> / |q_i| (0 for an all-zero row), from the fp32 dot
+ * product and the exact sum of squares with one correctly rounded square root
+ * and one correctly rounded division.  tav2_gather, tav2_encode and
+ * tav2_select_encode return TAV2_ERR_UNSUPPORTED for TAV2_I8.
  *   ws        device workspace of at least tav2_nn_select_workspace() bytes,
  *             256-byte aligned.
  * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE (k < 1 or k > TAV2_K_MAX, d, counts),
@@ -226,7 +236,7 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt,
  * After the caller has synchronised, tav2_profile_report() writes one line
  * "<site> <launches> <total_ms>" per site into buf (NUL-terminated, truncated
  * to buf_bytes), forgets the recorded launches and returns the untruncated
- * text length.  Site names: score_bf16, score_f32, topk, gather, pack_weights,
+ * text length.  Site names: score_bf16, score_i8, score_f32, topk, gather, pack_weights,
  * cand_proj, encoder_fused (the fused bf16 encoder), gemm_cand, gemm_embed,
  * gemm_qkv, attention, gemm_oproj_ln1, gemm_ffn1, gemm_ffn2_ln2, fill, gemm_pool,
  * pool_finalize (the layer-wise bf16 encoder), encode_f32.

@@ -38,7 +38,10 @@ def compile_flags():
 # Per-source extra flags.  The fused encoder's MFMA results are read by VALU code
 # (softmax, epilogues, LayerNorm): results kept in VGPRs save one accumulator
 # move per element.
-EXTRA_FLAGS = {"encoder_fused.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# The int8 score kernel's division and square root must round correctly (the
+# compiler's default for HIP, stated explicitly).
+EXTRA_FLAGS = {"encoder_fused.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+               "select.hip": ["-fhip-fp32-correctly-rounded-divide-sqrt"]}
 
 
 def _compile(src: str) -> str:

@@ -25,7 +25,7 @@ tav2_status check_dtype(int32_t dt) {
 // A sequence batch.  `for_select` adds the limits of the NN search kernels.
 tav2_status check_seq(const tav2_seq* s, bool for_select) {
   if (!s) return TAV2_ERR_NULL;
-  tav2_status st = check_dtype(s->dtype);
+  tav2_status st = s->dtype == TAV2_I8 ? TAV2_OK : check_dtype(s->dtype);
   if (st) return st;
   if (s->num_requests < 0 || s->max_len < 0) return TAV2_ERR_SHAPE;
   if (s->d < 16 || s->d > 512 || s->d % 16) return TAV2_ERR_SHAPE;
@@ -159,7 +159,8 @@ tav2_status tav2_nn_select(const tav2_seq* seq, const tav2_cands* cands, int32_t
                            void* stream) {
   tav2_status st;
   if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
-  if (seq->dtype != TAV2_F32 && seq->dtype != TAV2_BF16) return TAV2_ERR_DTYPE;
+  if (seq->dtype != TAV2_F32 && seq->dtype != TAV2_BF16 && seq->dtype != TAV2_I8)
+    return TAV2_ERR_DTYPE;
   if (cands->total == 0) return TAV2_OK;
   if (!out_idx || !out_score) return TAV2_ERR_NULL;
   if ((st = check_ws(ws, ws_bytes, select_ws_bytes(seq, cands)))) return st;
@@ -176,6 +177,7 @@ tav2_status tav2_gather(const tav2_seq* seq, const tav2_seq* rt, const tav2_cand
                         uint8_t* tok_time, int32_t* valid_len, void* stream) {
   tav2_status st;
   if ((st = check_seq(seq, false)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
+  if (seq->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;
   if ((st = check_rt(rt, seq))) return st;
   if (cands->total == 0) return TAV2_OK;
   if (!idx || !tok_emb || !tok_act || !valid_len) return TAV2_ERR_NULL;
@@ -231,6 +233,7 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt, const ta
                                void* stream) {
   tav2_status st;
   if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
+  if (seq->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;
   if ((st = check_rt(rt, seq))) return st;
   const int T = k + rt_len_max(rt);
   if ((st = check_weights(w, seq->d, seq->dtype, T, seq->time_bucket != nullptr))) return st;

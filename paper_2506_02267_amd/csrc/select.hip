@@ -3,7 +3,8 @@
 // total order (score desc, row asc).
 //
 // Scores: bf16 operands on the 32x32x16 MFMA with fp32 accumulation (float32
-// inputs use fp32 FMA).  Each request's rows are read by every candidate tile of
+// inputs use fp32 FMA; int8 sequence codes are dequantised and L2-normalised in
+// the score kernel).  Each request's rows are read by every candidate tile of
 // that request straight from the one stored copy (no per-candidate broadcast).
 //
 // Top-k, one workgroup per candidate, scores as order-preserving 32-bit keys.
@@ -98,6 +99,104 @@ __global__ __launch_bounds__(256) void score_bf16_kernel(
       for (int reg = 0; reg < 16; ++reg) {
         const int64_t n = n0 + a * 32 + 8 * (reg / 4) + 4 * h + (reg % 4);
         if (n < c_end) scores[n * ld + i] = acc[a][b][reg];
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- scores, int8
+// The int8 sequence storage (codes q, Sec. 3.1) with dequantisation and L2
+// normalisation fused into the score kernel (Sec. 3.4.2): s = <q_i, c> / |q_i|
+// (the dequantisation scale cancels in the normalisation).  Same tiling as the
+// bf16 kernel; each lane converts its 8 codes per k-block to bf16 (exact: |q| <=
+// 127) for the MFMA and adds their squares (exact in fp32: the row's sum of
+// squares is an integer below 2^24), the two lanes holding a row's halves
+// combine them, and the epilogue divides by the square root (both rounded to
+// nearest: the build keeps division and square root correctly rounded).
+__device__ __forceinline__ bf16x8 codes_to_bf16(uint2 raw, float& sq) {
+  bf16x8 v;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t word = j < 4 ? raw.x : raw.y;
+    const float x = float(int8_t((word >> (8 * (j & 3))) & 0xFF));
+    sq = fmaf(x, x, sq);
+    v[j] = static_cast<__bf16>(x);
+  }
+  return v;
+}
+
+__global__ __launch_bounds__(256) void score_i8_kernel(
+    const int8_t* __restrict__ emb, const int64_t* __restrict__ seq_off,
+    const int32_t* __restrict__ seq_len, const bf16_t* __restrict__ cand,
+    const int64_t* __restrict__ cand_off, int d, int max_len, float* __restrict__ scores,
+    int64_t ld) {
+  extern __shared__ __attribute__((aligned(16))) bf16_t ctile[];   // [SC_CANDS][d + SC_PAD]
+  const int r = blockIdx.z;
+  const int64_t c_begin = cand_off[r], c_end = cand_off[r + 1];
+  const int64_t n0 = c_begin + int64_t(blockIdx.y) * SC_CANDS;
+  if (n0 >= c_end) return;
+  const int L = min(seq_len[r], max_len);
+  if (int(blockIdx.x) * SC_ROWS >= L) return;
+  const int cld = d + SC_PAD;
+  for (int e = threadIdx.x; e < SC_CANDS * (d / 8); e += 256) {
+    const int row = e / (d / 8), c = e % (d / 8);
+    int64_t n = n0 + row;
+    n = n < c_end ? n : c_end - 1;
+    *reinterpret_cast<uint4*>(ctile + row * cld + c * 8) =
+        *reinterpret_cast<const uint4*>(cand + n * d + c * 8);
+  }
+  __syncthreads();
+  const int row0 = blockIdx.x * SC_ROWS + (threadIdx.x / WAVE) * 64;
+  if (row0 >= L) return;
+  const int lane = threadIdx.x % WAVE;
+  const int h = lane / 32, l32 = lane % 32;
+  const int8_t* seq = emb + seq_off[r] * int64_t(d);
+  const int8_t* brow[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    int i = row0 + t * 32 + l32;
+    i = i < L ? i : L - 1;   // clamped; not stored
+    brow[t] = seq + int64_t(i) * d + 8 * h;
+  }
+  const bf16_t* arow = ctile + l32 * cld + 8 * h;
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+  float sq[2] = {0.f, 0.f};
+  uint2 raw[2], nxt[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) raw[t] = *reinterpret_cast<const uint2*>(brow[t]);
+  for (int k0 = 0; k0 < d; k0 += 16) {
+    const int kn = k0 + 16 < d ? k0 + 16 : k0;   // next k-block (the last one reloads itself)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) nxt[t] = *reinterpret_cast<const uint2*>(brow[t] + kn);
+    bf16x8 bv[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) bv[t] = codes_to_bf16(raw[t], sq[t]);
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+      const bf16x8 av = as_bf16x8(*reinterpret_cast<const uint4*>(arow + a * 32 * cld + k0));
+#pragma unroll
+      for (int b = 0; b < 2; ++b) acc[a][b] = mfma32(av, bv[b], acc[a][b]);
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t) raw[t] = nxt[t];
+  }
+
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const float ss = sq[b] + __shfl_xor(sq[b], 32, WAVE);   // the row's other half
+    const float nrm = sqrtf(ss);
+    const int i = row0 + b * 32 + l32;
+    if (i >= L) continue;
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg) {
+        const int64_t n = n0 + a * 32 + 8 * (reg / 4) + 4 * h + (reg % 4);
+        if (n < c_end) scores[n * ld + i] = ss > 0.f ? acc[a][b][reg] / nrm : 0.f;
       }
     }
   }
@@ -597,6 +696,24 @@ hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores
     }
     score_bf16_kernel<<<grid, 256, lds, st>>>(
         static_cast<const bf16_t*>(seq.emb), seq.offset, seq.len,
+        static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
+  } else if (seq.dtype == TAV2_I8) {
+    dim3 grid(unsigned(cdiv(seq.max_len, SC_ROWS)), unsigned(cdiv(c.max_count, SC_CANDS)),
+              unsigned(seq.num_requests));
+    ProfScope prof("score_i8", st);
+    const size_t lds = size_t(SC_CANDS) * size_t(seq.d + SC_PAD) * 2;
+    static size_t lds_set[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64 || lds_set[dev] < lds) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(score_i8_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+      if (e != hipSuccess) return e;
+      if (dev >= 0 && dev < 64) lds_set[dev] = lds;
+    }
+    score_i8_kernel<<<grid, 256, lds, st>>>(
+        static_cast<const int8_t*>(seq.emb), seq.offset, seq.len,
         static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
   } else {
     dim3 grid(unsigned(cdiv(seq.max_len, 256)), unsigned(c.max_count), unsigned(seq.num_requests));

@@ -17,7 +17,7 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtav2.so")
 
-F32, BF16 = 0, 1
+F32, BF16, I8 = 0, 1, 2
 K_MAX, T_MAX = 1024, 1024
 STATUS = {0: "ok", -1: "null", -2: "shape", -3: "dtype", -4: "unsupported", -5: "workspace",
           -6: "hip"}
@@ -116,7 +116,13 @@ def _stream_handle(stream: Optional[torch.cuda.Stream]):
 
 
 def torch_dtype(dtype: int):
-    return torch.bfloat16 if dtype == BF16 else torch.float32
+    """Storage type of a sequence of this dtype (int8 codes for I8)."""
+    return {BF16: torch.bfloat16, I8: torch.int8}.get(dtype, torch.float32)
+
+
+def cand_dtype(dtype: int):
+    """Storage type of the candidates that go with a sequence of this dtype."""
+    return torch.bfloat16 if dtype in (BF16, I8) else torch.float32
 
 
 def _dev(a, dtype, device) -> torch.Tensor:
@@ -166,7 +172,7 @@ class DeviceCands:
     def from_host(cls, cand, cand_offset, dtype: int, device="cuda"):
         off = np.asarray(cand_offset, dtype=np.int64)
         counts = np.diff(off)
-        return cls(emb=_dev(cand, torch_dtype(dtype), device), offset=_dev(off, torch.int64, device),
+        return cls(emb=_dev(cand, cand_dtype(dtype), device), offset=_dev(off, torch.int64, device),
                    max_count=int(counts.max()) if counts.size else 0)
 
     @property

@@ -11,7 +11,7 @@ F32_TOL = 1e-4    # max-abs error bound for fp32 encoder outputs
 
 
 def dtype_code(w):
-    return T.BF16 if w.dtype == "bf16" else T.F32
+    return {"bf16": T.BF16, "i8": T.I8}.get(w.dtype, T.F32)
 
 
 def upload(inp, device="cuda"):

@@ -228,3 +228,20 @@ def test_status_strings():
     for code in range(-6, 1):
         assert lib.tav2_status_string(code).decode()
     assert lib.tav2_abi_version() >= 1
+
+
+def test_int8_sequence_is_for_the_nn_search_only():
+    """TAV2_I8 passes the NN search's argument checks (the error comes from the
+    empty output pointer, i.e. after the dtype was accepted); gather and
+    select_encode refuse it as unsupported."""
+    lib = T.load_library()
+    s, c = fake_seq(dtype=T.I8, d=32), fake_cands()
+    assert call_select(s, c, 8, idx=None) == -1
+    assert lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 8) == 10 * 128 * 4
+    st = lib.tav2_gather(ctypes.byref(s), None, ctypes.byref(c), FAKE, 8, FAKE, FAKE, FAKE, FAKE,
+                         None)
+    assert st == -4
+    w = fake_weights(d=32)
+    st = lib.tav2_select_encode(ctypes.byref(s), None, ctypes.byref(c), 8, ctypes.byref(w), FAKE,
+                                FAKE, FAKE, FAKE, 1 << 40, None)
+    assert st == -4
