@@ -107,9 +107,8 @@ __global__ __launch_bounds__(256) void score_bf16_kernel(
 // ---------------------------------------------------------------- scores, int8
 // The int8 sequence storage (codes q, Sec. 3.1) with dequantisation and L2
 // normalisation fused into the score kernel (Sec. 3.4.2): s = <q_i, c> / |q_i|
-// (the dequantisation scale cancels in the normalisation).  Same tiling as the
-// bf16 kernel; each lane converts its 8 codes per k-block to bf16 (exact: |q| <=
-// 127) for the MFMA and adds their squares (exact in fp32: the row's sum of
+// (the dequantisation scale cancels in the normalisation).  Each lane converts
+// its 8 codes per k-block to bf16 (exact: |q| <= 127) for the MFMA and adds their squares (exact in fp32: the row's sum of
 // squares is an integer below 2^24), the two lanes holding a row's halves
 // combine them, and the epilogue divides by the square root (both rounded to
 // nearest: the build keeps division and square root correctly rounded).
@@ -125,20 +124,30 @@ __device__ __forceinline__ bf16x8 codes_to_bf16(uint2 raw, float& sq) {
   return v;
 }
 
+// Block: 4 waves, 32 candidates x 256 rows (a narrow candidate tile: the codes are
+// short, so the block count, not operand reuse, sets the speed).  The normalised
+// scores are staged in LDS and leave as one 1 KB store per candidate row.
+constexpr int SI_CANDS = 32;
+constexpr int SI_ROWS = 256;
+constexpr int SI_SLD = SI_ROWS + 8;   // staged score row stride (floats)
+
 __global__ __launch_bounds__(256) void score_i8_kernel(
     const int8_t* __restrict__ emb, const int64_t* __restrict__ seq_off,
     const int32_t* __restrict__ seq_len, const bf16_t* __restrict__ cand,
     const int64_t* __restrict__ cand_off, int d, int max_len, float* __restrict__ scores,
     int64_t ld) {
-  extern __shared__ __attribute__((aligned(16))) bf16_t ctile[];   // [SC_CANDS][d + SC_PAD]
+  extern __shared__ __attribute__((aligned(16))) uint8_t si_smem[];
+  float* stile = reinterpret_cast<float*>(si_smem);                           // [32][SI_SLD]
+  bf16_t* ctile = reinterpret_cast<bf16_t*>(si_smem + SI_CANDS * SI_SLD * 4);  // [32][d + pad]
   const int r = blockIdx.z;
   const int64_t c_begin = cand_off[r], c_end = cand_off[r + 1];
-  const int64_t n0 = c_begin + int64_t(blockIdx.y) * SC_CANDS;
+  const int64_t n0 = c_begin + int64_t(blockIdx.y) * SI_CANDS;
   if (n0 >= c_end) return;
   const int L = min(seq_len[r], max_len);
-  if (int(blockIdx.x) * SC_ROWS >= L) return;
+  const int ib = blockIdx.x * SI_ROWS;
+  if (ib >= L) return;
   const int cld = d + SC_PAD;
-  for (int e = threadIdx.x; e < SC_CANDS * (d / 8); e += 256) {
+  for (int e = threadIdx.x; e < SI_CANDS * (d / 8); e += 256) {
     const int row = e / (d / 8), c = e % (d / 8);
     int64_t n = n0 + row;
     n = n < c_end ? n : c_end - 1;
@@ -146,24 +155,18 @@ __global__ __launch_bounds__(256) void score_i8_kernel(
         *reinterpret_cast<const uint4*>(cand + n * d + c * 8);
   }
   __syncthreads();
-  const int row0 = blockIdx.x * SC_ROWS + (threadIdx.x / WAVE) * 64;
-  if (row0 >= L) return;
-  const int lane = threadIdx.x % WAVE;
+  const int w = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
   const int h = lane / 32, l32 = lane % 32;
   const int8_t* seq = emb + seq_off[r] * int64_t(d);
   const int8_t* brow[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    int i = row0 + t * 32 + l32;
-    i = i < L ? i : L - 1;   // clamped; not stored
+    int i = ib + 64 * w + t * 32 + l32;
+    i = i < L ? i : L - 1;   // clamped; never stored
     brow[t] = seq + int64_t(i) * d + 8 * h;
   }
   const bf16_t* arow = ctile + l32 * cld + 8 * h;
-  f32x16 acc[4][2];
-#pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = f32x16{};
+  f32x16 acc[2] = {f32x16{}, f32x16{}};
   float sq[2] = {0.f, 0.f};
   uint2 raw[2], nxt[2];
 #pragma unroll
@@ -172,32 +175,38 @@ __global__ __launch_bounds__(256) void score_i8_kernel(
     const int kn = k0 + 16 < d ? k0 + 16 : k0;   // next k-block (the last one reloads itself)
 #pragma unroll
     for (int t = 0; t < 2; ++t) nxt[t] = *reinterpret_cast<const uint2*>(brow[t] + kn);
-    bf16x8 bv[2];
+    const bf16x8 av = as_bf16x8(*reinterpret_cast<const uint4*>(arow + k0));
 #pragma unroll
-    for (int t = 0; t < 2; ++t) bv[t] = codes_to_bf16(raw[t], sq[t]);
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-      const bf16x8 av = as_bf16x8(*reinterpret_cast<const uint4*>(arow + a * 32 * cld + k0));
-#pragma unroll
-      for (int b = 0; b < 2; ++b) acc[a][b] = mfma32(av, bv[b], acc[a][b]);
-    }
+    for (int t = 0; t < 2; ++t) acc[t] = mfma32(av, codes_to_bf16(raw[t], sq[t]), acc[t]);
 #pragma unroll
     for (int t = 0; t < 2; ++t) raw[t] = nxt[t];
   }
-
+  // D register 4j + i of tile t: candidate 8j + 4h + i, row 64w + 32t + l32
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const float ss = sq[b] + __shfl_xor(sq[b], 32, WAVE);   // the row's other half
+  for (int t = 0; t < 2; ++t) {
+    const float ss = sq[t] + __shfl_xor(sq[t], 32, WAVE);   // the row's other half
     const float nrm = sqrtf(ss);
-    const int i = row0 + b * 32 + l32;
-    if (i >= L) continue;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
+    for (int reg = 0; reg < 16; ++reg)
+      stile[(8 * (reg / 4) + 4 * h + (reg % 4)) * SI_SLD + 64 * w + 32 * t + l32] =
+          ss > 0.f ? acc[t][reg] / nrm : 0.f;
+  }
+  __syncthreads();
+  const int nv = min(SI_ROWS, L - ib);   // valid rows of this block
+  const int ii = 4 * lane;
 #pragma unroll
-      for (int reg = 0; reg < 16; ++reg) {
-        const int64_t n = n0 + a * 32 + 8 * (reg / 4) + 4 * h + (reg % 4);
-        if (n < c_end) scores[n * ld + i] = ss > 0.f ? acc[a][b][reg] / nrm : 0.f;
-      }
+  for (int q = 0; q < SI_CANDS / 4; ++q) {
+    const int c = (SI_CANDS / 4) * w + q;
+    const int64_t n = n0 + c;
+    if (n >= c_end || ii >= nv) continue;
+    const float4 v = *reinterpret_cast<const float4*>(stile + c * SI_SLD + ii);
+    float* dst = scores + n * ld + ib + ii;
+    if (ii + 4 <= nv) {
+      *reinterpret_cast<float4*>(dst) = v;
+    } else {
+      dst[0] = v.x;
+      if (ii + 1 < nv) dst[1] = v.y;
+      if (ii + 2 < nv) dst[2] = v.z;
     }
   }
 }
@@ -698,10 +707,10 @@ hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores
         static_cast<const bf16_t*>(seq.emb), seq.offset, seq.len,
         static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
   } else if (seq.dtype == TAV2_I8) {
-    dim3 grid(unsigned(cdiv(seq.max_len, SC_ROWS)), unsigned(cdiv(c.max_count, SC_CANDS)),
+    dim3 grid(unsigned(cdiv(seq.max_len, SI_ROWS)), unsigned(cdiv(c.max_count, SI_CANDS)),
               unsigned(seq.num_requests));
     ProfScope prof("score_i8", st);
-    const size_t lds = size_t(SC_CANDS) * size_t(seq.d + SC_PAD) * 2;
+    const size_t lds = size_t(SI_CANDS) * SI_SLD * 4 + size_t(SI_CANDS) * size_t(seq.d + SC_PAD) * 2;
     static size_t lds_set[64] = {};
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
