@@ -107,3 +107,28 @@ def test_pool_on_wrong_token_is_caught(monkeypatch):
 
     monkeypatch.setattr(enc, "pool", first_token)
     _fails(te.test_pool_properties_and_valid_length_groups)
+
+
+def _score_mutant(kind):
+    """normalised_scores with one plausible mistake."""
+    def scores(Q, C):
+        Q = np.asarray(Q)
+        dot = sel.exact_scores(Q.astype(np.float64), C)
+        sq = np.sum(Q.astype(np.int64) ** 2, axis=1).astype(np.float64)
+        if kind == "no_normalisation":
+            s = dot
+        elif kind == "no_square_root":
+            s = dot / np.where(sq > 0, sq, 1.0)[None, :]
+        else:   # "candidate_normalised": the wrong operand's length
+            s = dot / np.linalg.norm(np.asarray(C, dtype=np.float64), axis=1, keepdims=True)
+        return s.astype(np.float32)
+    return scores
+
+
+@pytest.mark.parametrize("kind", ["no_normalisation", "no_square_root", "candidate_normalised"])
+def test_int8_score_mistakes_are_caught(monkeypatch, kind):
+    bad = _score_mutant(kind)
+    monkeypatch.setattr(sel, "normalised_scores", bad)
+    monkeypatch.setattr(oracle, "normalised_scores", bad)
+    _fails(ts.test_normalised_closed_forms)
+    _fails(ts.test_normalised_scores_match_the_dequantised_definition, 0)
