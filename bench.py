@@ -160,6 +160,9 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle encoder work in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of one step captured as a HIP graph (the roofline "
+                         "figure still comes from an eager pass)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 256 MiB device to device three times "
                          "(a plain copy of known size for scaling memory counters)")
@@ -229,6 +232,19 @@ def main():
     dom = T.profile_report()
     T.profile_enable(False)
     ms = ev0.elapsed_time(ev1)
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            call()
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            graph.replay()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1)
     ms_per_step = ms / args.steps
     value = total * args.steps / (ms / 1000.0)
 
@@ -279,6 +295,8 @@ def main():
 
     config = {"workload": w.name, "requests": w.R, "L": w.L if w.L else list(w.L_range),
               "d": w.d, "candidates": total, "k": w.k}
+    if args.graph:
+        config["launch"] = "hip_graph"
     if not select_only:
         config.update({"rt_len": w.rt_len, "T": w.T, "d_model": w.d_model, "heads": w.n_heads,
                        "d_ffn": w.d_ffn, "layers": w.n_layers})
