@@ -35,6 +35,12 @@ def test_full_size_all_candidates():
     check(synth.SELECT_I8, zero_every=1021)
 
 
+def test_several_long_requests_large_k():
+    """Four 16k-row requests with 2000 candidates each and k = 512."""
+    w = synth.scaled(synth.SELECT_I8, R=4, N=2000, k=512)
+    check(w, seed=25, zero_every=2003)
+
+
 @pytest.mark.parametrize("d,R,Lr,N,k,seed", [
     (32, 3, (1, 700), 130, 64, 21),       # 2 candidate tiles, ragged tails, short rows
     (256, 2, (300, 2100), 40, 256, 22),   # wide codes, k above some row counts
