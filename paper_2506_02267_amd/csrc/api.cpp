@@ -198,6 +198,7 @@ tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2
                         float* out, void* ws, size_t ws_bytes, void* stream) {
   if (!tok || !w) return TAV2_ERR_NULL;
   tav2_status st;
+  if (tok->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;   // codes are for the NN search
   if ((st = check_dtype(tok->dtype))) return st;
   if (tok->total < 0 || tok->d < 16 || tok->d > 512 || tok->d % 16) return TAV2_ERR_SHAPE;
   if (tok->total > (int64_t(1) << 31) - 1) return TAV2_ERR_UNSUPPORTED;

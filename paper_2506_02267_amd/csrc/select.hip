@@ -16,6 +16,8 @@
 // found there by a radix select (an exact streaming search when the sample
 // gives no usable threshold).  Either way the k survivors are placed by counting,
 // for each, how many survivors precede it in the total order.
+#include <atomic>
+
 #include "common.h"
 #include "internal.h"
 
@@ -685,6 +687,21 @@ __global__ __launch_bounds__(TS_THREADS) void topk_stream_kernel(
 }
 
 // ---------------------------------------------------------------- launchers
+// Allow a kernel its largest dynamic LDS (`lds`: the size at the largest d) on the
+// current device, once per device (done[dev]).  Every caller sets the same value,
+// so calls from several host threads at most repeat the attribute call.
+static hipError_t allow_dynamic_lds(const void* kernel, size_t lds, std::atomic<bool>* done) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const bool cached = dev >= 0 && dev < 64;
+  if (cached && done[dev].load(std::memory_order_acquire)) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (e != hipSuccess) return e;
+  if (cached) done[dev].store(true, std::memory_order_release);
+  return hipSuccess;
+}
+
 hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores, int64_t ld,
                          hipStream_t st) {
   if (seq.num_requests == 0 || c.total == 0 || seq.max_len == 0) return hipSuccess;
@@ -693,16 +710,10 @@ hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores
               unsigned(seq.num_requests));
     ProfScope prof("score_bf16", st);
     const size_t lds = size_t(SC_CANDS) * size_t(seq.d + SC_PAD) * 2;   // d <= 512: <= 133 KB
-    static size_t lds_set[64] = {};   // per device: largest dynamic LDS allowed so far
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
+    static std::atomic<bool> lds_done[64] = {};
+    const hipError_t e = allow_dynamic_lds(reinterpret_cast<const void*>(score_bf16_kernel),
+                                           size_t(SC_CANDS) * (512 + SC_PAD) * 2, lds_done);
     if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= 64 || lds_set[dev] < lds) {
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(score_bf16_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-      if (e != hipSuccess) return e;
-      if (dev >= 0 && dev < 64) lds_set[dev] = lds;
-    }
     score_bf16_kernel<<<grid, 256, lds, st>>>(
         static_cast<const bf16_t*>(seq.emb), seq.offset, seq.len,
         static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);
@@ -711,16 +722,11 @@ hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores
               unsigned(seq.num_requests));
     ProfScope prof("score_i8", st);
     const size_t lds = size_t(SI_CANDS) * SI_SLD * 4 + size_t(SI_CANDS) * size_t(seq.d + SC_PAD) * 2;
-    static size_t lds_set[64] = {};
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
+    static std::atomic<bool> lds_done[64] = {};
+    const hipError_t e = allow_dynamic_lds(
+        reinterpret_cast<const void*>(score_i8_kernel),
+        size_t(SI_CANDS) * SI_SLD * 4 + size_t(SI_CANDS) * (512 + SC_PAD) * 2, lds_done);
     if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= 64 || lds_set[dev] < lds) {
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(score_i8_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-      if (e != hipSuccess) return e;
-      if (dev >= 0 && dev < 64) lds_set[dev] = lds;
-    }
     score_i8_kernel<<<grid, 256, lds, st>>>(
         static_cast<const int8_t*>(seq.emb), seq.offset, seq.len,
         static_cast<const bf16_t*>(c.emb), c.offset, seq.d, seq.max_len, scores, ld);

@@ -232,7 +232,7 @@ def test_status_strings():
 
 def test_int8_sequence_is_for_the_nn_search_only():
     """TAV2_I8 passes the NN search's argument checks (the error comes from the
-    empty output pointer, i.e. after the dtype was accepted); gather and
+    empty output pointer, i.e. after the dtype was accepted); gather, encode and
     select_encode refuse it as unsupported."""
     lib = T.load_library()
     s, c = fake_seq(dtype=T.I8, d=32), fake_cands()
@@ -242,6 +242,10 @@ def test_int8_sequence_is_for_the_nn_search_only():
                          None)
     assert st == -4
     w = fake_weights(d=32)
+    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
+                   d=32, dtype=T.I8, reserved=0)
+    assert lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), FAKE, FAKE, 1 << 40,
+                           None) == -4
     st = lib.tav2_select_encode(ctypes.byref(s), None, ctypes.byref(c), 8, ctypes.byref(w), FAKE,
                                 FAKE, FAKE, FAKE, 1 << 40, None)
     assert st == -4
