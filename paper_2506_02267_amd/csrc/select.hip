@@ -128,7 +128,8 @@ __device__ __forceinline__ bf16x8 codes_to_bf16(uint2 raw, float& sq) {
 
 // Block: 4 waves, 32 candidates x 256 rows (a narrow candidate tile: the codes are
 // short, so the block count, not operand reuse, sets the speed).  The normalised
-// scores are staged in LDS and leave as one 1 KB store per candidate row.
+// scores are staged in LDS and leave as one 1 KB non-temporal store per candidate
+// row.
 constexpr int SI_CANDS = 32;
 constexpr int SI_ROWS = 256;
 constexpr int SI_SLD = SI_ROWS + 8;   // staged score row stride (floats)
@@ -204,7 +205,8 @@ __global__ __launch_bounds__(256) void score_i8_kernel(
     const float4 v = *reinterpret_cast<const float4*>(stile + c * SI_SLD + ii);
     float* dst = scores + n * ld + ib + ii;
     if (ii + 4 <= nv) {
-      *reinterpret_cast<float4*>(dst) = v;
+      // streaming store: the scores are read once, by the top-k
+      __builtin_nontemporal_store(f32x4{v.x, v.y, v.z, v.w}, reinterpret_cast<f32x4*>(dst));
     } else {
       dst[0] = v.x;
       if (ii + 1 < nv) dst[1] = v.y;
