@@ -31,45 +31,57 @@ PEAK_F32_TFLOPS = 157.3       # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 
 
-def site_work(w, total, valid_tokens, max_len, launches_per_step):
+def site_work(w, total, valid_tokens, pairs, launches_per_step, rows_total, k):
     """Algorithmic work of one launch of each kernel site.
 
-    Returns {site: (kind, amount)} with kind 'flop' or 'byte'.  Only the work the
-    method defines is counted: valid tokens only, causal attention over
-    T (T + 1) / 2 query-key pairs, scores 2 L d per candidate, the top-k's read
-    of the score rows.
+    Returns {site: (kind, amount, materialised)}: kind 'flop' or 'byte', amount the
+    work the method defines, materialised the bytes of intermediate results the
+    implementation writes or reads back (None where there are none).  Counted:
+    valid tokens only, causal attention over T (T + 1) / 2 query-key pairs, scores
+    2 L_r d per candidate of request r (pairs = the sum of L_r over candidates); an NN search over int8 codes moves the codes, the
+    candidates and its outputs.
     """
     dm, ff, d, H = w.d_model, w.d_ffn, w.d, w.n_heads
     dh = dm // H
     per = {}
     M = valid_tokens
-    per["gemm_ffn1"] = ("flop", 2.0 * M * ff * dm)
-    per["gemm_ffn2_ln2"] = ("flop", 2.0 * M * ff * dm)
-    per["gemm_qkv"] = ("flop", 2.0 * M * 3 * dm * dm)
-    per["gemm_oproj_ln1"] = ("flop", 2.0 * M * dm * dm)
-    per["gemm_embed"] = ("flop", 2.0 * M * d * dm)
-    per["gemm_pool"] = ("flop", 2.0 * M * dm * dm)
-    per["gemm_cand"] = ("flop", 2.0 * total * d * dm)
+    per["gemm_ffn1"] = ("flop", 2.0 * M * ff * dm, None)
+    per["gemm_ffn2_ln2"] = ("flop", 2.0 * M * ff * dm, None)
+    per["gemm_qkv"] = ("flop", 2.0 * M * 3 * dm * dm, None)
+    per["gemm_oproj_ln1"] = ("flop", 2.0 * M * dm * dm, None)
+    per["gemm_embed"] = ("flop", 2.0 * M * d * dm, None)
+    per["gemm_pool"] = ("flop", 2.0 * M * dm * dm, None)
+    per["gemm_cand"] = ("flop", 2.0 * total * d * dm, None)
     T = w.T
-    per["attention"] = ("flop", 4.0 * H * dh * total * T * (T + 1) / 2.0)
+    per["attention"] = ("flop", 4.0 * H * dh * total * T * (T + 1) / 2.0, None)
     # the fused encoder: input projection (token half per token, candidate half per
     # candidate), all layers (causal attention over valid positions) and the head
-    Tv = valid_tokens / max(total, 1)
-    per["encoder_fused"] = ("flop", 2.0 * valid_tokens * d * dm + 2.0 * total * d * dm
-                            + w.n_layers * (2.0 * M * (3 * dm * dm + dm * dm + 2 * ff * dm)
-                                            + 4.0 * H * dh * total * Tv * (Tv + 1) / 2.0)
-                            + 2.0 * M * dm * dm)
-    per["score_bf16"] = ("flop", 2.0 * total * max_len * d)
-    per["score_f32"] = ("flop", 2.0 * total * max_len * d)
-    # int8 storage: the score rows written dominate (d = 32 codes per row)
-    per["score_i8"] = ("byte", 4.0 * total * max_len + max_len * d * w.R + 2.0 * total * d)
-    per["topk"] = ("byte", 4.0 * total * max_len)
+    per["encoder_fused"] = ("flop", encoder_flop(w, total, valid_tokens), None)
+    per["encode_f32"] = ("flop", encoder_flop(w, total, valid_tokens), None)
+    scores_bytes = 4.0 * pairs
+    per["score_bf16"] = ("flop", 2.0 * pairs * d, scores_bytes)
+    per["score_f32"] = ("flop", 2.0 * pairs * d, scores_bytes)
+    # int8 storage: the codes and the candidates are what the method reads
+    per["score_i8"] = ("byte", 1.0 * rows_total * d + 2.0 * total * d, scores_bytes)
+    per["topk"] = ("byte", 8.0 * total * k, scores_bytes)
     out = {}
-    for site, (kind, amount) in per.items():
+    for site, (kind, amount, mat) in per.items():
         n = launches_per_step.get(site)
         if n:
-            out[site] = (kind, amount / n)
+            out[site] = (kind, amount / n, None if mat is None else mat / n)
     return out
+
+
+def encoder_flop(w, total, valid_tokens):
+    """Algorithmic FLOP of the encoder over all candidates (valid tokens only)."""
+    dm, ff, d, H = w.d_model, w.d_ffn, w.d, w.n_heads
+    dh = dm // H
+    M = valid_tokens
+    Tv = valid_tokens / max(total, 1)
+    return (2.0 * M * d * dm + 2.0 * total * d * dm
+            + w.n_layers * (2.0 * M * (3 * dm * dm + dm * dm + 2 * ff * dm)
+                            + 4.0 * H * dh * total * Tv * (Tv + 1) / 2.0)
+            + 2.0 * M * dm * dm)
 
 
 TRAFFIC_FILES = {"encoder_fused": "encoder_fused_{workload}_traffic.md"}
@@ -102,50 +114,76 @@ def measured_traffic(site, workload):
     return float(fields["hbm_bytes_per_launch"])
 
 
-def cpu_baseline_select(inp, k):
-    """The oracle's NN search, untuned, over every candidate of the workload."""
-    import oracle
+def _threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
     except Exception:
-        threads = os.cpu_count() or 1
-    t0 = time.perf_counter()
-    oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
-    t_sel = time.perf_counter() - t0
-    return {"value": inp.total / t_sel, "unit": "candidates/s", "cores": int(threads),
+        return os.cpu_count() or 1
+
+
+def _oracle_select_sample(inp, k, budget_s):
+    """The oracle's NN search over candidate chunks (every request in turn, 32
+    candidates at a time) until budget_s has passed.  Returns (ids, idx, seconds)."""
+    import oracle
+    chunks = []
+    for r in range(inp.seq.R):
+        a, b = int(inp.cand_offset[r]), int(inp.cand_offset[r + 1])
+        chunks.extend(np.arange(s, min(b, s + 32)) for s in range(a, b, 32))
+    # round robin over requests so a short budget still sees every request's length
+    order = []
+    per_req = {}
+    for c in chunks:
+        per_req.setdefault(int(np.searchsorted(inp.cand_offset, c[0], side="right")) - 1,
+                           []).append(c)
+    while any(per_req.values()):
+        for r in sorted(per_req):
+            if per_req[r]:
+                order.append(per_req[r].pop(0))
+    done, t = [], 0.0
+    idx = np.full((inp.total, k), -1, dtype=np.int32)
+    for c in order:
+        t0 = time.perf_counter()
+        i, _ = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k, only=c)
+        t += time.perf_counter() - t0
+        idx[c] = i[c]
+        done.append(c)
+        if t >= budget_s:
+            break
+    ids = np.concatenate(done)
+    return ids, idx, t
+
+
+def cpu_baseline_select(inp, k, budget_s):
+    """The oracle's NN search, untuned, on a bounded sample of the workload."""
+    ids, _, t_sel = _oracle_select_sample(inp, k, budget_s)
+    return {"value": ids.size / t_sel, "unit": "candidates/s", "cores": _threads(),
             "kind": "oracle",
-            "sample": f"NN search of all {inp.total} candidates ({t_sel:.2f} s), numpy"}
+            "sample": f"NN search of {ids.size} of {inp.total} candidates ({t_sel:.2f} s), numpy"}
 
 
 def cpu_baseline(inp, W, k, budget_s):
-    """The oracle, untuned, on a bounded sample of the same workload."""
+    """The oracle, untuned, on a bounded sample of the same workload: its NN search
+    over candidate chunks for about budget_s / 2, then the gather and encoder of the
+    selected candidates for about budget_s / 2, each scaled per candidate."""
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
-    total = inp.total
-    T = inp.w.T
-    t0 = time.perf_counter()
-    idx, _ = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
-    t_sel = time.perf_counter() - t0
+    ids, idx, t_sel = _oracle_select_sample(inp, k, budget_s / 2)
     creq = inp.cand_request()
+    T = inp.w.T
     n, t_enc, chunk = 0, 0.0, 8
-    while n < total and (t_enc < budget_s or n == 0):
-        ids = np.arange(n, min(total, n + chunk))
+    while n < ids.size and (t_enc < budget_s / 2 or n == 0):
+        part = ids[n:n + chunk]
         t1 = time.perf_counter()
-        tok_emb, tok_act, tok_time, valid = oracle.gather_tokens(inp.seq, inp.rt, creq[ids],
-                                                                 idx[ids], T)
-        oracle.encode(tok_emb, tok_act, tok_time, valid, inp.cand[ids], W)
+        tok_emb, tok_act, tok_time, valid = oracle.gather_tokens(inp.seq, inp.rt, creq[part],
+                                                                 idx[part], T)
+        oracle.encode(tok_emb, tok_act, tok_time, valid, inp.cand[part], W)
         t_enc += time.perf_counter() - t1
-        n += ids.size
-    per_cand = t_sel / total + t_enc / n
-    return {"value": 1.0 / per_cand, "unit": "candidates/s", "cores": int(threads),
+        n += part.size
+    per_cand = t_sel / ids.size + t_enc / n
+    return {"value": 1.0 / per_cand, "unit": "candidates/s", "cores": _threads(),
             "kind": "oracle",
-            "sample": (f"NN select of all {total} candidates ({t_sel:.2f} s) + gather and "
-                       f"encode of the first {n} candidates ({t_enc:.2f} s), float64 numpy, "
+            "sample": (f"NN select of {ids.size} of {inp.total} candidates ({t_sel:.2f} s) + "
+                       f"gather and encode of {n} of them ({t_enc:.2f} s), float64 numpy, "
                        f"scaled per candidate")}
 
 
@@ -157,8 +195,8 @@ def main():
     ap.add_argument("--workload", default="single_bf16",
                     help="tiny_f32 | single_bf16 | ragged_bf16 | mixed_bf16 | stress_bf16 | "
                          "select_i8 (the NN search alone over int8 codes)")
-    ap.add_argument("--cpu-budget", type=float, default=15.0,
-                    help="seconds of oracle encoder work in the CPU baseline sample")
+    ap.add_argument("--cpu-budget", type=float, default=20.0,
+                    help="seconds of oracle work in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one step captured as a HIP graph (the roofline "
@@ -256,41 +294,65 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
 
-    work = site_work(w, total, valid_tokens, int(lengths.max()), launches)
+    rows_total = int(lengths.sum())
+    pairs = float(np.sum(lengths * counts))
+    work = site_work(w, total, valid_tokens, pairs, launches, rows_total, w.k)
+    peak_flop = PEAK_BF16_TFLOPS if w.dtype in ("bf16", "i8") else PEAK_F32_TFLOPS
+
+    def position(kind, amount, seconds):
+        """(bound, achieved, peak, unit, frac) of `amount` of work done in `seconds`."""
+        if kind == "flop":
+            ach = amount / seconds / 1e12 if seconds > 0 else 0.0
+            return ("mfma" if w.dtype == "bf16" else "alu", ach, peak_flop, "TFLOP/s",
+                    ach / peak_flop)
+        ach = amount / seconds / 1e9 if seconds > 0 else 0.0
+        return "hbm", ach, PEAK_HBM_GBS, "GB/s", ach / PEAK_HBM_GBS
+
     cnt, dom_ms = dom.get(dominant, (0, 0.0))
     avg_s = dom_ms / max(cnt, 1) / 1000.0
-    kind, amount = work.get(dominant, ("flop", 0.0))
-    if kind == "flop":
-        peak = PEAK_BF16_TFLOPS if w.dtype in ("bf16", "i8") else PEAK_F32_TFLOPS
-        achieved = amount / avg_s / 1e12 if avg_s > 0 else 0.0
-        roof = {"bound": "mfma" if w.dtype == "bf16" else "alu", "achieved": round(achieved, 2),
-                "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                "traffic": None}
+    kind, amount, mat = work.get(dominant, ("flop", 0.0, None))
+    bound, achieved, peak, unit, frac = position(kind, amount, avg_s)
+    roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(frac, 4), "traffic": measured_traffic(dominant, w.name),
+            "kernel": dominant, "avg_launch_us": round(avg_s * 1e6, 2),
+            "work_per_launch": amount}
+    if mat is not None:
+        roof["materialised_bytes_per_launch"] = mat
+
+    # every kernel site: its algorithmic work against its own roofline (times from the
+    # profiled pass, which brackets each launch with events)
+    stages = {}
+    for s_, (c, t) in sorted(sites.items(), key=lambda kv: -kv[1][1]):
+        per_launch_s = t / max(c, 1) / 1000.0
+        st = {"launches_per_step": c // prof_steps, "us_per_launch": round(per_launch_s * 1e6, 2)}
+        if s_ in work:
+            k_, a_, m_ = work[s_]
+            b_, ach_, _, u_, f_ = position(k_, a_, per_launch_s)
+            st.update({"bound": b_, "achieved": round(ach_, 2), "unit": u_, "frac": round(f_, 4)})
+            if m_ is not None:
+                st["materialised_bytes_per_launch"] = m_
+        stages[s_] = st
+    # whole step against the roofline of the fused path: the score products and the
+    # encoder at the MFMA peak (bf16 workloads), or the search's algorithmic bytes at
+    # the HBM peak (int8 NN search)
+    if select_only:
+        roof_s = max((rows_total * w.d + 2.0 * total * w.d + 8.0 * total * w.k)
+                     / (PEAK_HBM_GBS * 1e9), 2.0 * pairs * w.d / (PEAK_BF16_TFLOPS * 1e12))
     else:
-        achieved = amount / avg_s / 1e9 if avg_s > 0 else 0.0
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None}
-    roof["traffic"] = measured_traffic(dominant, w.name)
-    roof["kernel"] = dominant
-    roof["avg_launch_us"] = round(avg_s * 1e6, 2)
-    roof["work_per_launch"] = amount
+        roof_s = (2.0 * pairs * w.d + encoder_flop(w, total, valid_tokens)) / (peak_flop * 1e12)
+    e2e_frac = roof_s / (ms_per_step / 1000.0)
 
     # stage breakdown for the log (stderr)
-    print(f"[bench] {w.name}: {ms_per_step:.3f} ms/step, wall {wall:.2f} s for {args.steps} steps",
-          file=sys.stderr)
-    for s, (c, t) in sorted(sites.items(), key=lambda kv: -kv[1][1]):
-        per_launch = t / max(c, 1)
-        extra = ""
-        if s in work:
-            k_, a_ = work[s]
-            extra = (f" {a_ / (per_launch / 1e3) / 1e12:.1f} TFLOP/s" if k_ == "flop"
-                     else f" {a_ / (per_launch / 1e3) / 1e9:.0f} GB/s")
-        print(f"[bench]   {s:16s} {c // prof_steps:3d}/step {t / prof_steps:9.3f} ms/step"
-              f" {per_launch * 1e3:9.1f} us/launch{extra}", file=sys.stderr)
+    print(f"[bench] {w.name}: {ms_per_step:.3f} ms/step, wall {wall:.2f} s for {args.steps} steps,"
+          f" roofline {roof_s * 1e6:.1f} us -> e2e fraction {e2e_frac:.3f}", file=sys.stderr)
+    for s_, st in stages.items():
+        extra = f" {st['achieved']:.1f} {st['unit']} ({st['frac']:.3f})" if "frac" in st else ""
+        print(f"[bench]   {s_:16s} {st['launches_per_step']:3d}/step "
+              f"{st['us_per_launch']:9.1f} us/launch{extra}", file=sys.stderr)
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = (cpu_baseline_select(inp, w.k) if select_only
+        cpu = (cpu_baseline_select(inp, w.k, args.cpu_budget) if select_only
                else cpu_baseline(inp, W, w.k, args.cpu_budget))
 
     config = {"workload": w.name, "requests": w.R, "L": w.L if w.L else list(w.L_range),
@@ -304,11 +366,12 @@ def main():
             "unit": "candidates/s", "n_gpus": 1,
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-            "dtype": "bf16" if w.dtype in ("bf16", "i8") else "f32",
+            "dtype": {"bf16": "bf16", "i8": "i8"}.get(w.dtype, "f32"),
             "data": ("synthetic (seeded int8 codes of random unit rows, 1/8-grid candidates)"
                      if select_only else
                      "synthetic (seeded 1/8-grid embeddings, N(0,0.02) weights)"),
-            "config": config, "roofline": roof, "cpu_baseline": cpu}
+            "config": config, "roofline": roof, "e2e_frac": round(e2e_frac, 4),
+            "e2e_roofline_us": round(roof_s * 1e6, 2), "stages": stages, "cpu_baseline": cpu}
     print(json.dumps(line), flush=True)
 
 

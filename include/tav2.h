@@ -60,7 +60,7 @@ typedef int32_t tav2_status;
 
 #define TAV2_F32  0   /* float32 storage and arithmetic */
 #define TAV2_BF16 1   /* bfloat16 storage, fp32 accumulation */
-#define TAV2_I8   2   /* int8 codes of the quantised sequence storage (Sec. 3.1): a
+#define TAV2_I8   2   /* int8 codes of the quantised sequence storage (Sec. 3.2.1): a
                          sequence dtype for tav2_nn_select only, with bf16 candidates */
 
 #define TAV2_K_MAX     1024  /* largest k of the NN search */
@@ -160,7 +160,7 @@ int32_t tav2_abi_version(void);
  *             k > len[r] (positions >= len[r]).
  *   out_score device [total, k] float32: the scores (fp32 accumulation; exact
  *             whenever the fp32 sum is exact), -inf in padded positions.
- * A TAV2_I8 sequence holds int8 codes q (Sec. 3.1); each row is dequantised and
+ * A TAV2_I8 sequence holds int8 codes q (Sec. 3.2.1); each row is dequantised and
  * L2-normalised before the dot product (Sec. 3.4.2, fused sequence
  * dequantisation), all inside the score kernel: the dequantisation scale cancels
  * and s[n, i] = <q_i, cand[n]> / |q_i| (0 for an all-zero row), from the fp32 dot

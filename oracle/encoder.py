@@ -15,8 +15,10 @@ Readings taken where the paper is silent or its widths disagree:
     1/sqrt(d_head), LayerNorm with population variance and eps = 1e-5.
   * Mask: causal over encoder positions (Sec. 3.2.2 and Sec. 3.3.2: a token sees
     itself and earlier tokens only).  Positions at or past a candidate's valid
-    length are padding; with a causal mask no valid position can see them, so
-    the oracle simply runs on the valid prefix.
+    length are padding; no valid position may see them, so the oracle simply
+    runs on the valid prefix.  `causal=False` drops the causal mask (every valid
+    token sees every valid token), the unmasked setting of the paper's appendix
+    comparison of its fused transformer (Appendix B).
   * Head: out = [max over valid positions of (X W_pool^T + b_pool) ; X at the
     last valid position], width 2 d_model.  A candidate with no valid token
     gets zeros.
@@ -55,19 +57,21 @@ def layer_norm(x, g, b, eps=LN_EPS):
     return (x - mu) / np.sqrt(var + eps) * _f64(g) + _f64(b)
 
 
-def causal_attention(q, k, v):
-    """q, k, v: [n, heads, T, d_head] -> [n, heads, T, d_head], causal."""
+def attention(q, k, v, causal=True):
+    """q, k, v: [n, heads, T, d_head] -> [n, heads, T, d_head]; scaled dot-product
+    attention over all T positions, causal unless causal=False."""
     T, dh = q.shape[-2], q.shape[-1]
     s = q @ np.swapaxes(k, -1, -2) / np.sqrt(dh)
-    future = np.triu(np.ones((T, T), dtype=bool), k=1)      # key j > query p
-    s = np.where(future, -np.inf, s)
+    if causal:
+        future = np.triu(np.ones((T, T), dtype=bool), k=1)  # key j > query p
+        s = np.where(future, -np.inf, s)
     s = s - s.max(axis=-1, keepdims=True)
     p = np.exp(s)
     p = p / p.sum(axis=-1, keepdims=True)
     return p @ v
 
 
-def encoder_layer(X, Lw, n_heads):
+def encoder_layer(X, Lw, n_heads, causal=True):
     """One post-LN encoder layer on X [n, T, d_model]."""
     n, T, dm = X.shape
     dh = dm // n_heads
@@ -77,7 +81,7 @@ def encoder_layer(X, Lw, n_heads):
     def heads(t):
         return t.reshape(n, T, n_heads, dh).transpose(0, 2, 1, 3)
 
-    o = causal_attention(heads(q), heads(k), heads(v))
+    o = attention(heads(q), heads(k), heads(v), causal)
     o = o.transpose(0, 2, 1, 3).reshape(n, T, dm)
     X = layer_norm(X + o @ _f64(Lw.W_o).T + _f64(Lw.b_o), Lw.ln1_g, Lw.ln1_b)
     h = np.maximum(X @ _f64(Lw.W_1).T + _f64(Lw.b_1), 0.0)
@@ -94,15 +98,15 @@ def pool(X, W):
     return np.concatenate([y.max(axis=1), X[:, T - 1, :]], axis=-1)
 
 
-def encode_states(tok_emb, tok_act, tok_time, cand, W):
+def encode_states(tok_emb, tok_act, tok_time, cand, W, causal=True):
     """All hidden states [X0, X1, ...] for a group with one valid length (pins use it)."""
     xs = [feature_encode(tok_emb, tok_act, tok_time, cand, W)]
     for Lw in W.layers:
-        xs.append(encoder_layer(xs[-1], Lw, W.n_heads))
+        xs.append(encoder_layer(xs[-1], Lw, W.n_heads, causal))
     return xs
 
 
-def encode(tok_emb, tok_act, tok_time, valid_len, cand, W, chunk=32, only=None):
+def encode(tok_emb, tok_act, tok_time, valid_len, cand, W, chunk=32, only=None, causal=True):
     """Pooled encoder output for every candidate (or the ids in `only`).
 
     tok_emb [total, T, d], tok_act/tok_time [total, T], valid_len [total],
@@ -119,12 +123,13 @@ def encode(tok_emb, tok_act, tok_time, valid_len, cand, W, chunk=32, only=None):
             continue
         for s in range(0, group.size, chunk):
             g = group[s:s + chunk]
-            xs = encode_states(tok_emb[g, :t], tok_act[g, :t], tok_time[g, :t], cand[g], W)
+            xs = encode_states(tok_emb[g, :t], tok_act[g, :t], tok_time[g, :t], cand[g], W,
+                               causal)
             out[g] = pool(xs[-1], W)
     return out
 
 
-def select_encode(inputs, W, k, only=None, chunk=32):
+def select_encode(inputs, W, k, only=None, chunk=32, causal=True):
     """The whole path: NN select (Eq. 3), token assembly (Eq. 2 with the kept
     real-time tail), feature encoding (Eq. 4), encoder and head.
 
@@ -139,7 +144,8 @@ def select_encode(inputs, W, k, only=None, chunk=32):
     ids = np.arange(inputs.cand.shape[0]) if only is None else np.asarray(only, dtype=np.int64)
     tok_emb, tok_act, tok_time, valid = gather_tokens(inputs.seq, inputs.rt, creq[ids],
                                                       idx[ids], T)
-    out_ids = encode(tok_emb, tok_act, tok_time, valid, inputs.cand[ids], W, chunk=chunk)
+    out_ids = encode(tok_emb, tok_act, tok_time, valid, inputs.cand[ids], W, chunk=chunk,
+                     causal=causal)
     out = np.zeros((inputs.cand.shape[0], 2 * W.d_model), dtype=np.float64)
     out[ids] = out_ids
     return idx, score, out

@@ -63,7 +63,7 @@ def rank_order(s: np.ndarray) -> np.ndarray:
 
 def normalised_scores(Q: np.ndarray, C: np.ndarray) -> np.ndarray:
     """Scores over the int8 sequence storage with dequantisation and L2
-    normalisation (Sec. 3.4.2, fused sequence dequantisation; codes of Sec. 3.1).
+    normalisation (Sec. 3.4.2, fused sequence dequantisation; codes of Sec. 3.2.1).
 
     Row i dequantises to e_i = (0.65 / 127) q_i and is normalised to unit length
     before the dot product of Eq. 3, so s[n, i] = <e_i / |e_i|, c_n>; the scale

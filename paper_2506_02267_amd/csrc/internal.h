@@ -9,7 +9,7 @@
 
 namespace tav2 {
 
-constexpr int SEL_MAX_LEN = 32768;
+constexpr int SEL_MAX_LEN = 32768;   // longest request sequence the NN search accepts
 
 // Brackets one kernel launch with HIP events when profiling is enabled
 // (tav2_profile_enable); a no-op otherwise.
@@ -24,7 +24,7 @@ class ProfScope {
   const char* name_;
   hipStream_t st_;
   void* start_;
-};   // longest request sequence the top-k kernel holds in registers
+};
 
 // ---- select.hip
 int64_t score_ld(int32_t max_len);

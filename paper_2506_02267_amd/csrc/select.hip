@@ -107,7 +107,7 @@ __global__ __launch_bounds__(256) void score_bf16_kernel(
 }
 
 // ---------------------------------------------------------------- scores, int8
-// The int8 sequence storage (codes q, Sec. 3.1) with dequantisation and L2
+// The int8 sequence storage (codes q, Sec. 3.2.1) with dequantisation and L2
 // normalisation fused into the score kernel (Sec. 3.4.2): s = <q_i, c> / |q_i|
 // (the dequantisation scale cancels in the normalisation).  Each lane converts
 // its 8 codes per k-block to bf16 (exact: |q| <= 127) for the MFMA and adds their squares (exact in fp32: the row's sum of

@@ -115,6 +115,17 @@ def _stream_handle(stream: Optional[torch.cuda.Stream]):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _used_on(stream: Optional[torch.cuda.Stream], *tensors):
+    """Tell torch's caching allocator that tensors allocated on the current stream
+    are in use on `stream` (a temporary workspace dropped on return must not be
+    handed out again before the kernels reading it on `stream` have finished)."""
+    if stream is None or stream == torch.cuda.current_stream():
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
+
+
 def torch_dtype(dtype: int):
     """Storage type of a sequence of this dtype (int8 codes for I8)."""
     return {BF16: torch.bfloat16, I8: torch.int8}.get(dtype, torch.float32)
@@ -271,6 +282,7 @@ def nn_select(seq: DeviceSeq, cands: DeviceCands, k: int, out_idx=None, out_scor
     _check("tav2_nn_select", lib.tav2_nn_select(ctypes.byref(s), ctypes.byref(c), k,
                                                 _ptr(out_idx), _ptr(out_score), wp, wb,
                                                 _stream_handle(stream)))
+    _used_on(stream, ws.buf, out_idx, out_score)
     return out_idx, out_score
 
 
@@ -289,6 +301,7 @@ def gather(seq: DeviceSeq, rt: Optional[DeviceSeq], cands: DeviceCands, idx: tor
     _check("tav2_gather", lib.tav2_gather(ctypes.byref(s), ctypes.byref(r) if r is not None else None,
                                           ctypes.byref(c), _ptr(idx), k, _ptr(emb), _ptr(act),
                                           _ptr(tim), _ptr(valid), _stream_handle(stream)))
+    _used_on(stream, emb, act, tim, valid)
     return DeviceTokens(emb=emb, act=act, time=tim, valid_len=valid, dtype=seq.dtype)
 
 
@@ -304,6 +317,7 @@ def encode(tokens: DeviceTokens, cand_emb: torch.Tensor, w: DeviceWeights, out=N
     wp, wb = ws.get(need)
     _check("tav2_encode", lib.tav2_encode(ctypes.byref(t), _ptr(cand_emb), ctypes.byref(w.s),
                                           _ptr(out), wp, wb, _stream_handle(stream)))
+    _used_on(stream, ws.buf, out)
     return out
 
 

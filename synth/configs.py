@@ -66,7 +66,7 @@ STRESS = Workload(5, "stress_bf16", "bf16", R=16, L=16384, L_range=None, d=256, 
                   tie_frac=0.01)
 
 WORKLOADS = {w.cid: w for w in (TINY, SINGLE, RAGGED, MIXED, STRESS)}
-# NN search over the paper's int8 sequence storage (32-d codes, Sec. 3.1) with
+# NN search over the paper's int8 sequence storage (32-d codes, Sec. 3.2.1) with
 # dequantisation and L2 normalisation fused into the score kernel (Sec. 3.4.2);
 # one request of the single workload's size.  The encoder fields are unused.
 SELECT_I8 = Workload(6, "select_i8", "i8", R=1, L=16384, L_range=None, d=32, N=1000, k=256,

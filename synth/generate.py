@@ -47,9 +47,9 @@ def grid_values(rng: np.random.Generator, shape) -> np.ndarray:
 
 
 def int8_codes(rng: np.random.Generator, shape) -> np.ndarray:
-    """Codes of the int8 embedding storage (Sec. 3.1, Eq. 1's quantised sequence
-    features): rows drawn as random unit vectors, scaled by 127 / 0.65, rounded half
-    to even and clamped to [-127, 127].  Returns int8."""
+    """Codes of the int8 embedding storage (the quantisation formula of Sec. 3.2.1):
+    rows drawn as random unit vectors, scaled by 127 / 0.65, rounded half to even
+    and clamped to [-127, 127].  Returns int8."""
     e = rng.standard_normal(shape)
     e /= np.maximum(np.linalg.norm(e, axis=-1, keepdims=True), 1e-30)
     return np.clip(np.rint(e * (127.0 / 0.65)), -127, 127).astype(np.int8)

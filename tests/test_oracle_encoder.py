@@ -1,9 +1,10 @@
 """Pins for the oracle's feature encoding (Eq. 4), encoder layers and head.
 
 Independent references: torch's own post-LN nn.TransformerEncoderLayer run in
-float64 on the CPU (the textbook layer, with a causal mask), the Eq. 4 special
-case d_model = 2 d / identity projection, the single-token closed form, and
-invariants (causal prefix, head permutation, W_q/W_k independence at one token).
+float64 on the CPU (the textbook layer, with a causal mask and without one), the
+Eq. 4 special case d_model = 2 d / identity projection, the single-token closed
+form, and invariants (causal prefix, head permutation, W_q/W_k independence at
+one token, token-permutation equivariance of the unmasked encoder).
 """
 import copy
 
@@ -184,3 +185,54 @@ def test_layer_norm_matches_torch():
     want = torch.nn.functional.layer_norm(torch.tensor(x), (32,), torch.tensor(g),
                                           torch.tensor(b), eps=1e-5).numpy()
     np.testing.assert_allclose(oracle.encoder.layer_norm(x, g, b), want, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("heads,T", [(1, 7), (2, 12), (4, 33)])
+def test_unmasked_layers_match_torch_transformer_encoder_layer(heads, T):
+    """causal=False is the textbook layer with no attention mask at all."""
+    w, W = small_weights(heads=heads, T=T)
+    tok, act, tim, cand = random_tokens(3, T, w.d)
+    xs = oracle.encode_states(tok, act, tim, cand, W, causal=False)
+    x = torch.tensor(xs[0])
+    for li, Lw in enumerate(W.layers):
+        layer = torch_layer(Lw, w.d_model, heads, w.d_ffn)
+        with torch.no_grad():
+            x = layer(x)
+        np.testing.assert_allclose(xs[li + 1], x.numpy(), rtol=0, atol=1e-10)
+
+
+def test_unmasked_encoder_is_permutation_equivariant_without_positions():
+    """With E_pos = 0 and no mask, permuting the tokens permutes every layer's
+    output the same way, so the max-pooled half of the head is unchanged and the
+    last-token half is the output of whichever token lands last."""
+    T = 11
+    w, W = small_weights(heads=2, T=T)
+    W.E_pos = np.zeros_like(W.E_pos)
+    tok, act, tim, cand = random_tokens(2, T, w.d, seed=4)
+    perm = np.random.default_rng(8).permutation(T)
+    xs = oracle.encode_states(tok, act, tim, cand, W, causal=False)
+    ys = oracle.encode_states(tok[:, perm], act[:, perm], tim[:, perm], cand, W, causal=False)
+    for x, y in zip(xs, ys):
+        np.testing.assert_allclose(y, x[:, perm], rtol=0, atol=1e-12)
+    valid = np.full(2, T)
+    out = oracle.encode(tok, act, tim, valid, cand, W, causal=False)
+    out_p = oracle.encode(tok[:, perm], act[:, perm], tim[:, perm], valid, cand, W, causal=False)
+    dm = w.d_model
+    np.testing.assert_allclose(out_p[:, :dm], out[:, :dm], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(out_p[:, dm:], xs[-1][:, perm[-1]], rtol=0, atol=1e-12)
+    # the causal encoder is not equivariant (a check that the permutation matters)
+    c = oracle.encode(tok, act, tim, valid, cand, W)
+    c_p = oracle.encode(tok[:, perm], act[:, perm], tim[:, perm], valid, cand, W)
+    assert np.abs(c_p[:, :dm] - c[:, :dm]).max() > 1e-6
+
+
+def test_unmasked_equals_causal_at_one_token_and_differs_after():
+    w, W = small_weights(heads=2, T=6)
+    tok, act, tim, cand = random_tokens(3, 6, w.d, seed=6)
+    one = np.ones(3, np.int32)
+    np.testing.assert_array_equal(oracle.encode(tok, act, tim, one, cand, W, causal=False),
+                                  oracle.encode(tok, act, tim, one, cand, W))
+    six = np.full(3, 6)
+    a = oracle.encode(tok, act, tim, six, cand, W, causal=False)
+    b = oracle.encode(tok, act, tim, six, cand, W)
+    assert np.abs(a - b).max() > 1e-6

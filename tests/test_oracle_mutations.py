@@ -46,7 +46,7 @@ def test_wrong_layer_norm_eps_is_caught(monkeypatch):
 
 
 def test_mask_off_by_one_is_caught(monkeypatch):
-    def leaky(q, k, v):
+    def leaky(q, k, v, causal=True):
         T, dh = q.shape[-2], q.shape[-1]
         s = q @ np.swapaxes(k, -1, -2) / np.sqrt(dh)
         s = np.where(np.triu(np.ones((T, T), dtype=bool), k=2), -np.inf, s)  # sees one future key
@@ -54,7 +54,7 @@ def test_mask_off_by_one_is_caught(monkeypatch):
         p = np.exp(s)
         return (p / p.sum(axis=-1, keepdims=True)) @ v
 
-    monkeypatch.setattr(enc, "causal_attention", leaky)
+    monkeypatch.setattr(enc, "attention", leaky)
     _fails(te.test_causal_prefix_invariance)
     _fails(te.test_layers_match_torch_transformer_encoder_layer, 2, 12)
 
@@ -62,11 +62,11 @@ def test_mask_off_by_one_is_caught(monkeypatch):
 def test_missing_output_bias_is_caught(monkeypatch):
     real = enc.encoder_layer
 
-    def no_bo(X, Lw, n_heads):
+    def no_bo(X, Lw, n_heads, causal=True):
         import copy
         L2 = copy.copy(Lw)
         L2.b_o = np.zeros_like(Lw.b_o)
-        return real(X, L2, n_heads)
+        return real(X, L2, n_heads, causal)
 
     monkeypatch.setattr(enc, "encoder_layer", no_bo)
     _fails(te.test_layers_match_torch_transformer_encoder_layer, 2, 12)
@@ -90,11 +90,11 @@ def test_swapped_concat_is_caught(monkeypatch):
 def test_transposed_ffn_weight_is_caught(monkeypatch):
     real = enc.encoder_layer
 
-    def transposed(X, Lw, n_heads):
+    def transposed(X, Lw, n_heads, causal=True):
         import copy
         L2 = copy.copy(Lw)
         L2.W_o = Lw.W_o.T.copy()
-        return real(X, L2, n_heads)
+        return real(X, L2, n_heads, causal)
 
     monkeypatch.setattr(enc, "encoder_layer", transposed)
     _fails(te.test_layers_match_torch_transformer_encoder_layer, 2, 12)
@@ -132,3 +132,10 @@ def test_int8_score_mistakes_are_caught(monkeypatch, kind):
     monkeypatch.setattr(oracle, "normalised_scores", bad)
     _fails(ts.test_normalised_closed_forms)
     _fails(ts.test_normalised_scores_match_the_dequantised_definition, 0)
+
+
+def test_unmasked_mode_that_keeps_the_causal_mask_is_caught(monkeypatch):
+    real = enc.attention
+    monkeypatch.setattr(enc, "attention", lambda q, k, v, causal=True: real(q, k, v, True))
+    _fails(te.test_unmasked_layers_match_torch_transformer_encoder_layer, 2, 12)
+    _fails(te.test_unmasked_encoder_is_permutation_equivariant_without_positions)

@@ -199,7 +199,7 @@ def test_empty_request_and_no_candidates():
 
 # ---------------------------------------------------------------- int8 storage
 # Scores over int8 codes with dequantisation and L2 normalisation (Sec. 3.4.2,
-# fused sequence dequantisation; the codes of Sec. 3.1).
+# fused sequence dequantisation; the codes of Sec. 3.2.1).
 
 def test_normalised_closed_forms():
     """Hand-computed values: <q, c> / |q| with |q| a perfect square root."""
