@@ -63,6 +63,15 @@ typedef int32_t tav2_status;
 #define TAV2_I8   2   /* int8 codes of the quantised sequence storage (Sec. 3.2.1): a
                          sequence dtype for tav2_nn_select only, with bf16 candidates */
 
+/* Attention mask of the encoder: the flags argument of tav2_encode and
+ * tav2_select_encode. */
+#define TAV2_MASK_CAUSAL 0u  /* position p attends to positions 0..p, the causal mask the
+                                encoder applies (Sec. 3.2.2, 'Transformer Encoder'); default */
+#define TAV2_MASK_NONE   1u  /* every valid position attends to every valid position: the
+                                unmasked setting of the paper's comparison of its fused
+                                transformer with FlashAttention-2 (Appendix B).  For tests and
+                                comparisons; bf16 encoders take it only when T <= 128 */
+
 #define TAV2_K_MAX     1024  /* largest k of the NN search */
 #define TAV2_T_MAX     1024  /* largest encoder sequence (k + real-time tail) */
 #define TAV2_N_ACT        8  /* action types: values in [0, 8) */
@@ -144,6 +153,9 @@ typedef struct tav2_weights {
   const void*  E_pos;                        /* device [max_pos, dm] */
   const tav2_layer* layers;                  /* HOST array of n_layers layer records */
   const void*  W_pool; const float* b_pool;  /* device [dm, dm]; [dm] */
+  const void*  packed;         /* device: these weights as tav2_pack_weights wrote them, or
+                                  NULL (then every call packs them into its workspace) */
+  uint64_t     packed_bytes;   /* size of `packed` (ignored when it is NULL) */
 } tav2_weights;
 
 /* Human-readable text of a status code (static storage). */
@@ -197,35 +209,57 @@ tav2_status tav2_gather(const tav2_seq* seq, const tav2_seq* rt, const tav2_cand
                         int32_t* valid_len, void* stream);
 
 /*
+ * Packed encoder weights: the bf16 encoder reads its matrices and side tables in
+ * its own fragment order.  tav2_pack_weights writes that form once into a
+ * caller-owned device buffer of tav2_pack_weights_bytes(w) bytes (256-byte
+ * aligned); a tav2_weights whose `packed` points at it skips the packing step
+ * of every later call (the paper's serving engine likewise keeps its model in
+ * pre-allocated device memory, Sec. 3.4.2).  The buffer stays valid while the
+ * weights it was packed from are unchanged; it is read-only to the library.
+ * float32 weights are used as given: 0 bytes, and packing them is a no-op.
+ * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_DTYPE, TAV2_ERR_UNSUPPORTED,
+ * TAV2_ERR_WORKSPACE (buffer NULL, misaligned or too small), TAV2_ERR_HIP.
+ */
+size_t tav2_pack_weights_bytes(const tav2_weights* w);
+tav2_status tav2_pack_weights(const tav2_weights* w, void* packed, size_t bytes, void* stream);
+
+/*
  * Encoder + head over explicit tokens (Eq. 4, Sec. 3.2.2):
  *   out device [total, 2 dm] float32:
  *     out[n, 0:dm]    = max over p < valid_len[n] of (X_p W_pool^T + b_pool)
  *     out[n, dm:2dm]  = X_{valid_len[n]-1}
- *   where X is the last layer's output under a causal mask; rows with
- *   valid_len = 0 are zero.
+ *   where X is the last layer's output under the mask `flags` selects
+ *   (TAV2_MASK_CAUSAL or TAV2_MASK_NONE); rows with valid_len = 0 are zero.
  *   cand_emb device [total, d] (the tokens' dtype).
  * Supported shapes: bf16 with dm == 256, dm / n_heads in {32, 64},
- * d_ffn a multiple of 256 up to 4096, d a multiple of 32 up to 512; float32
- * with dm <= 128, d_ffn <= 512, T <= 64 and d <= 256.
+ * d_ffn a multiple of 256 up to 4096, d a multiple of 32 up to 256, at most 8
+ * layers; float32 with dm <= 128, d_ffn <= 512, T <= 64 and d <= 256.  Other
+ * valid shapes return TAV2_ERR_UNSUPPORTED.
  * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_DTYPE, TAV2_ERR_UNSUPPORTED,
  * TAV2_ERR_WORKSPACE, TAV2_ERR_HIP.
  */
 size_t tav2_encode_workspace(const tav2_tokens* tok, const tav2_weights* w);
 tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2_weights* w,
-                        float* out, void* ws, size_t ws_bytes, void* stream);
+                        uint32_t flags, float* out, void* ws, size_t ws_bytes, void* stream);
 
 /*
- * The whole path for a request batch: NN search, token assembly and encoder in
- * one call; out_idx / out_score / out as in the calls above (out_idx and
- * out_score may not be NULL: the encoder reads the selection from them).
+ * The whole path for a request batch, as the lifelong-sequence module computes
+ * it at serving time: the candidate-anchored NN search of Eq. 3 over each
+ * request's de-duplicated sequence (Sec. 3.4.2, 'Request Level
+ * De-duplication'), the selected rows followed by the kept most-recent
+ * real-time actions (Eq. 2, NN(S_LL, c) + S_RT[:r]), the feature encoding of
+ * Eq. 4 and the encoder and head of Sec. 3.2.2, in one call.  out_idx /
+ * out_score / out as in the calls above (out_idx and out_score may not be NULL:
+ * the encoder reads the selection from them); flags as for tav2_encode.
  * T = k + (rt ? rt->max_len : 0) must not exceed w->max_pos.
+ * Errors: those of tav2_nn_select and tav2_encode.
  */
 size_t tav2_select_encode_workspace(const tav2_seq* seq, const tav2_seq* rt,
                                     const tav2_cands* cands, int32_t k,
                                     const tav2_weights* w);
 tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt,
                                const tav2_cands* cands, int32_t k, const tav2_weights* w,
-                               int32_t* out_idx, float* out_score, float* out,
+                               uint32_t flags, int32_t* out_idx, float* out_score, float* out,
                                void* ws, size_t ws_bytes, void* stream);
 
 /*
@@ -236,10 +270,11 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt,
  * After the caller has synchronised, tav2_profile_report() writes one line
  * "<site> <launches> <total_ms>" per site into buf (NUL-terminated, truncated
  * to buf_bytes), forgets the recorded launches and returns the untruncated
- * text length.  Site names: score_bf16, score_i8, score_f32, topk, gather, pack_weights,
- * cand_proj, encoder_fused (the fused bf16 encoder), gemm_cand, gemm_embed,
- * gemm_qkv, attention, gemm_oproj_ln1, gemm_ffn1, gemm_ffn2_ln2, fill, gemm_pool,
- * pool_finalize (the layer-wise bf16 encoder), encode_f32.
+ * text length.  Site names: nn_sample, nn_threshold, nn_filter, nn_select,
+ * nn_fallback (the NN search with on-chip scores, for bf16 and int8 sequences of
+ * more than 4096 rows), score_bf16, score_i8, score_f32, topk (the NN search over
+ * materialised score rows), gather, pack_weights, cand_proj, encoder_fused (the
+ * bf16 encoder), encode_f32.
  */
 int32_t tav2_profile_enable(int32_t on, const char* only_site);
 int64_t tav2_profile_report(char* buf, size_t buf_bytes);

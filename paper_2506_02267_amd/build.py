@@ -16,8 +16,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtav2.so")
-SOURCES = ["api.cpp", "profile.cpp", "select.hip", "gather.hip", "encoder_bf16.hip", "encoder_fused.hip",
-           "encoder_f32.hip"]
+SOURCES = ["api.cpp", "profile.cpp", "select.hip", "select_fused.hip", "gather.hip",
+           "encoder_fused.hip", "encoder_fused_unmasked.hip", "encoder_f32.hip"]
 ARCH = "gfx950"
 
 
@@ -35,13 +35,17 @@ def compile_flags():
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
-# Per-source extra flags.  The fused encoder's MFMA results are read by VALU code
-# (softmax, epilogues, LayerNorm): results kept in VGPRs save one accumulator
-# move per element.
-# The int8 score kernel's division and square root must round correctly (the
+# Per-source extra flags.  The fused encoder's and the fused NN search's MFMA
+# results are read by VALU code (softmax, epilogues, LayerNorm, the survivor
+# filter): results kept in VGPRs save one accumulator move per element (and keep
+# the filter's 128 accumulators from being copied out of AGPRs all at once).
+# The int8 score kernels' division and square root must round correctly (the
 # compiler's default for HIP, stated explicitly).
 EXTRA_FLAGS = {"encoder_fused.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-               "select.hip": ["-fhip-fp32-correctly-rounded-divide-sqrt"]}
+               "encoder_fused_unmasked.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+               "select.hip": ["-fhip-fp32-correctly-rounded-divide-sqrt"],
+               "select_fused.hip": ["-fhip-fp32-correctly-rounded-divide-sqrt", "-mllvm",
+                                    "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src: str) -> str:

@@ -9,7 +9,7 @@ using namespace tav2;
 
 namespace {
 
-constexpr int32_t ABI_VERSION = 1;
+constexpr int32_t ABI_VERSION = 2;
 constexpr size_t WS_ALIGN = 256;
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -79,14 +79,24 @@ tav2_status check_weights(const tav2_weights* w, int d, int dtype, int T, bool h
       if (!aligned(p, 16)) return TAV2_ERR_SHAPE;
     }
   }
-  const int dh = w->d_model / w->n_heads;
   if (dtype == TAV2_BF16) {
-    if (w->d_model != 256 || (dh != 32 && dh != 64)) return TAV2_ERR_UNSUPPORTED;
-    if (w->d_ffn % 256 || w->d_ffn > 4096) return TAV2_ERR_UNSUPPORTED;
-    if (d % 32) return TAV2_ERR_UNSUPPORTED;
+    if (!encode_fused_supported(d, *w) || w->d_ffn > 4096) return TAV2_ERR_UNSUPPORTED;
+    if (w->packed) {   // packed by tav2_pack_weights
+      if (!aligned(w->packed, WS_ALIGN) || w->packed_bytes < encode_fused_packed_bytes(*w))
+        return TAV2_ERR_WORKSPACE;
+    }
   } else {
     if (!encode_f32_fits(T, *w) || d > 256) return TAV2_ERR_UNSUPPORTED;
   }
+  return TAV2_OK;
+}
+
+// The encoder's mask flags: TAV2_MASK_CAUSAL, or TAV2_MASK_NONE (the bf16 encoder
+// keeps positions in blocks of 128 that see only earlier blocks: unmasked, T must
+// fit one block).
+tav2_status check_flags(uint32_t flags, int dtype, int T) {
+  if (flags != TAV2_MASK_CAUSAL && flags != TAV2_MASK_NONE) return TAV2_ERR_SHAPE;
+  if (flags == TAV2_MASK_NONE && dtype == TAV2_BF16 && T > 128) return TAV2_ERR_UNSUPPORTED;
   return TAV2_OK;
 }
 
@@ -109,25 +119,36 @@ tav2_status check_rt(const tav2_seq* rt, const tav2_seq* seq) {
   return TAV2_OK;
 }
 
-size_t select_ws_bytes(const tav2_seq* s, const tav2_cands* c) {
+// The NN search's workspace: survivor lists when the scores stay on chip, else
+// the materialised score rows.
+size_t select_ws_bytes(const tav2_seq* s, const tav2_cands* c, int k) {
+  if (select_fused_applies(*s)) return align_up(select_fused_workspace(*c, k), WS_ALIGN);
   return align_up(size_t(c->total) * size_t(score_ld(s->max_len)) * 4, WS_ALIGN);
+}
+
+hipError_t run_select(const tav2_seq& s, const tav2_cands& c, int k, int32_t* out_idx,
+                      float* out_score, int32_t* cand_req, void* ws, hipStream_t st) {
+  if (select_fused_applies(s))
+    return launch_select_fused(s, c, k, out_idx, out_score, cand_req, ws, st);
+  float* scores = static_cast<float*>(ws);
+  const int64_t ld = score_ld(s.max_len);
+  hipError_t e = launch_scores(s, c, scores, ld, st);
+  if (e == hipSuccess) e = launch_topk(s, c, scores, ld, k, out_idx, out_score, cand_req, st);
+  return e;
 }
 
 size_t encode_ws_bytes(int64_t total, int T, const tav2_weights* w) {
   if (w->dtype == TAV2_F32) return 0;
-  if (encode_fused_supported(w->d_in, *w)) return align_up(encode_fused_workspace(total, T, *w), WS_ALIGN);
-  return align_up(encode_bf16_workspace(total, T, *w), WS_ALIGN);
+  return align_up(encode_fused_workspace(total, T, *w), WS_ALIGN);
 }
 
 tav2_status run_encode(const TokenSource& src, const void* cand_emb, int64_t total,
-                       const tav2_weights* w, float* out, void* ws, size_t ws_bytes,
+                       const tav2_weights* w, uint32_t flags, float* out, void* ws,
                        hipStream_t st) {
-  if (w->dtype == TAV2_BF16) {
-    if (encode_fused_supported(w->d_in, *w))
-      return hip_status(launch_encode_fused(src, cand_emb, total, *w, out, ws, st));
-    return hip_status(launch_encode_bf16(src, cand_emb, total, *w, out, ws, ws_bytes, st));
-  }
-  return hip_status(launch_encode_f32(src, cand_emb, total, *w, out, st));
+  const bool unmasked = flags == TAV2_MASK_NONE;
+  if (w->dtype == TAV2_BF16)
+    return hip_status(launch_encode_fused(src, cand_emb, total, *w, out, ws, unmasked, st));
+  return hip_status(launch_encode_f32(src, cand_emb, total, *w, out, unmasked, st));
 }
 
 }  // namespace
@@ -151,7 +172,7 @@ int32_t tav2_abi_version(void) { return ABI_VERSION; }
 
 size_t tav2_nn_select_workspace(const tav2_seq* seq, const tav2_cands* cands, int32_t k) {
   if (check_seq(seq, true) || check_cands(cands, seq) || check_k(k)) return 0;
-  return select_ws_bytes(seq, cands);
+  return select_ws_bytes(seq, cands, k);
 }
 
 tav2_status tav2_nn_select(const tav2_seq* seq, const tav2_cands* cands, int32_t k,
@@ -163,13 +184,9 @@ tav2_status tav2_nn_select(const tav2_seq* seq, const tav2_cands* cands, int32_t
     return TAV2_ERR_DTYPE;
   if (cands->total == 0) return TAV2_OK;
   if (!out_idx || !out_score) return TAV2_ERR_NULL;
-  if ((st = check_ws(ws, ws_bytes, select_ws_bytes(seq, cands)))) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  float* scores = static_cast<float*>(ws);
-  const int64_t ld = score_ld(seq->max_len);
-  hipError_t e = launch_scores(*seq, *cands, scores, ld, s);
-  if (e == hipSuccess) e = launch_topk(*seq, *cands, scores, ld, k, out_idx, out_score, nullptr, s);
-  return hip_status(e);
+  if ((st = check_ws(ws, ws_bytes, select_ws_bytes(seq, cands, k)))) return st;
+  return hip_status(run_select(*seq, *cands, k, out_idx, out_score, nullptr, ws,
+                               static_cast<hipStream_t>(stream)));
 }
 
 tav2_status tav2_gather(const tav2_seq* seq, const tav2_seq* rt, const tav2_cands* cands,
@@ -194,8 +211,26 @@ size_t tav2_encode_workspace(const tav2_tokens* tok, const tav2_weights* w) {
   return encode_ws_bytes(tok->total, tok->T, w);
 }
 
+size_t tav2_pack_weights_bytes(const tav2_weights* w) {
+  if (!w || w->dtype != TAV2_BF16) return 0;
+  if (check_weights(w, w->d_in, TAV2_BF16, 1, w->E_time != nullptr)) return 0;
+  return align_up(encode_fused_packed_bytes(*w), WS_ALIGN);
+}
+
+tav2_status tav2_pack_weights(const tav2_weights* w, void* packed, size_t bytes, void* stream) {
+  if (!w) return TAV2_ERR_NULL;
+  tav2_status st;
+  if ((st = check_dtype(w->dtype))) return st;
+  if (w->d_in < 16 || w->d_in > 512 || w->d_in % 16) return TAV2_ERR_SHAPE;
+  if ((st = check_weights(w, w->d_in, w->dtype, 1, w->E_time != nullptr))) return st;
+  if (w->dtype == TAV2_F32) return TAV2_OK;
+  if (!packed || !aligned(packed, WS_ALIGN) || bytes < encode_fused_packed_bytes(*w))
+    return TAV2_ERR_WORKSPACE;
+  return hip_status(launch_encode_fused_pack(*w, packed, static_cast<hipStream_t>(stream)));
+}
+
 tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2_weights* w,
-                        float* out, void* ws, size_t ws_bytes, void* stream) {
+                        uint32_t flags, float* out, void* ws, size_t ws_bytes, void* stream) {
   if (!tok || !w) return TAV2_ERR_NULL;
   tav2_status st;
   if (tok->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;   // codes are for the NN search
@@ -203,6 +238,7 @@ tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2
   if (tok->total < 0 || tok->d < 16 || tok->d > 512 || tok->d % 16) return TAV2_ERR_SHAPE;
   if (tok->total > (int64_t(1) << 31) - 1) return TAV2_ERR_UNSUPPORTED;
   if ((st = check_weights(w, tok->d, tok->dtype, tok->T, tok->time_bucket != nullptr))) return st;
+  if ((st = check_flags(flags, tok->dtype, tok->T))) return st;
   if (tok->total == 0) return TAV2_OK;
   if (!tok->emb || !tok->action_type || !tok->valid_len || !cand_emb || !out) return TAV2_ERR_NULL;
   if (!aligned(tok->emb, 16) || !aligned(cand_emb, 16) || !aligned(out, 16)) return TAV2_ERR_SHAPE;
@@ -215,7 +251,7 @@ tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2
   src.valid_len = tok->valid_len;
   src.T = tok->T;
   src.d = tok->d;
-  return run_encode(src, cand_emb, tok->total, w, out, ws, ws_bytes,
+  return run_encode(src, cand_emb, tok->total, w, flags, out, ws,
                     static_cast<hipStream_t>(stream));
 }
 
@@ -224,37 +260,34 @@ size_t tav2_select_encode_workspace(const tav2_seq* seq, const tav2_seq* rt,
   if (check_seq(seq, true) || check_cands(cands, seq) || check_k(k) || check_rt(rt, seq)) return 0;
   const int T = k + rt_len_max(rt);
   if (check_weights(w, seq->d, seq->dtype, T, seq->time_bucket != nullptr)) return 0;
-  return select_ws_bytes(seq, cands) + align_up(size_t(cands->total) * 4, WS_ALIGN) +
+  return select_ws_bytes(seq, cands, k) + align_up(size_t(cands->total) * 4, WS_ALIGN) +
          encode_ws_bytes(cands->total, T, w);
 }
 
 tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt, const tav2_cands* cands,
-                               int32_t k, const tav2_weights* w, int32_t* out_idx,
-                               float* out_score, float* out, void* ws, size_t ws_bytes,
-                               void* stream) {
+                               int32_t k, const tav2_weights* w, uint32_t flags,
+                               int32_t* out_idx, float* out_score, float* out, void* ws,
+                               size_t ws_bytes, void* stream) {
   tav2_status st;
   if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
   if (seq->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;
   if ((st = check_rt(rt, seq))) return st;
   const int T = k + rt_len_max(rt);
   if ((st = check_weights(w, seq->d, seq->dtype, T, seq->time_bucket != nullptr))) return st;
+  if ((st = check_flags(flags, seq->dtype, T))) return st;
   if (cands->total == 0) return TAV2_OK;
   if (!out_idx || !out_score || !out) return TAV2_ERR_NULL;
   if (!aligned(out, 16)) return TAV2_ERR_SHAPE;
-  const size_t sel_b = select_ws_bytes(seq, cands);
+  const size_t sel_b = select_ws_bytes(seq, cands, k);
   const size_t req_b = align_up(size_t(cands->total) * 4, WS_ALIGN);
   const size_t enc_b = encode_ws_bytes(cands->total, T, w);
   if ((st = check_ws(ws, ws_bytes, sel_b + req_b + enc_b))) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   uint8_t* base = static_cast<uint8_t*>(ws);
-  float* scores = reinterpret_cast<float*>(base);
   int32_t* cand_req = reinterpret_cast<int32_t*>(base + sel_b);
   void* enc_ws = base + sel_b + req_b;
-  const int64_t ld = score_ld(seq->max_len);
-  hipError_t e = launch_scores(*seq, *cands, scores, ld, s);
-  if (e == hipSuccess)
-    e = launch_topk(*seq, *cands, scores, ld, k, out_idx, out_score, cand_req, s);
-  if (e != hipSuccess) return TAV2_ERR_HIP;
+  if (run_select(*seq, *cands, k, out_idx, out_score, cand_req, base, s) != hipSuccess)
+    return TAV2_ERR_HIP;
   TokenSource src{};
   src.explicit_tokens = false;
   src.seq_emb = seq->emb;
@@ -274,7 +307,7 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt, const ta
   src.k = k;
   src.T = T;
   src.d = seq->d;
-  return run_encode(src, cands->emb, cands->total, w, out, enc_ws, enc_b, s);
+  return run_encode(src, cands->emb, cands->total, w, flags, out, enc_ws, s);
 }
 
 }  // extern "C"

@@ -2,7 +2,8 @@
 // whole candidate (tokens, Q/K/V, FFN hidden state) in LDS and runs Eq. 4's
 // feature encoding, the causal post-LN layers and the linear + max-pool head
 // (Sec. 3.2.2) with fp32 FMA.  Only the valid prefix of each candidate is
-// computed: under the causal mask no valid position sees padding.
+// computed: no valid position sees padding (under the causal mask, or in the
+// unmasked mode, where a position sees the whole valid prefix).
 #include "common.h"
 #include "internal.h"
 #include "token_source.h"
@@ -18,6 +19,7 @@ struct EncF32Args {
   const float *W_in, *b_in, *E_act, *E_time, *E_pos, *W_pool, *b_pool;
   tav2_layer layers[F32_MAX_LAYERS];
   float* out;
+  int unmasked;   // 1: every valid position sees every valid position
 };
 
 __device__ void layer_norm_rows(float* src, float* dst, int rows, int dm, const float* g,
@@ -84,20 +86,21 @@ __global__ __launch_bounds__(256) void encode_f32_kernel(EncF32Args a) {
       B1[p * wide + c] = acc;
     }
     __syncthreads();
-    // causal attention: output element (p, head, i)
+    // attention (causal: keys j <= p; unmasked: every valid key): element (p, head, i)
     for (int e = tid; e < Tv * dm; e += 256) {
       const int p = e / dm, c = e % dm;
       const int hh = c / dh;
+      const int jend = a.unmasked ? Tv - 1 : p;
       const float* q = B1 + p * wide + hh * dh;
       float m = -__builtin_inff();
-      for (int j = 0; j <= p; ++j) {
+      for (int j = 0; j <= jend; ++j) {
         const float* kj = B1 + j * wide + dm + hh * dh;
         float s = 0.f;
         for (int i = 0; i < dh; ++i) s = fmaf(q[i], kj[i], s);
         m = fmaxf(m, s * scale);
       }
       float l = 0.f, o = 0.f;
-      for (int j = 0; j <= p; ++j) {
+      for (int j = 0; j <= jend; ++j) {
         const float* kj = B1 + j * wide + dm + hh * dh;
         float s = 0.f;
         for (int i = 0; i < dh; ++i) s = fmaf(q[i], kj[i], s);
@@ -155,7 +158,7 @@ bool encode_f32_fits(int T, const tav2_weights& w) {
 }
 
 hipError_t launch_encode_f32(const TokenSource& src, const void* cand_emb, int64_t total,
-                             const tav2_weights& w, float* out, hipStream_t st) {
+                             const tav2_weights& w, float* out, bool unmasked, hipStream_t st) {
   if (total == 0) return hipSuccess;
   EncF32Args a{};
   a.s = src;
@@ -174,6 +177,7 @@ hipError_t launch_encode_f32(const TokenSource& src, const void* cand_emb, int64
   a.b_pool = w.b_pool;
   for (int i = 0; i < w.n_layers; ++i) a.layers[i] = w.layers[i];
   a.out = out;
+  a.unmasked = unmasked ? 1 : 0;
   ProfScope prof("encode_f32", st);
   encode_f32_kernel<<<unsigned(total), 256, 0, st>>>(a);
   return hipGetLastError();

@@ -35,6 +35,16 @@ hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* sc
                        int k, int32_t* out_idx, float* out_score, int32_t* cand_req,
                        hipStream_t st);
 
+// ---- select_fused.hip: NN search with the scores kept on chip (bf16 and int8
+// sequences whose longest request exceeds FUSED_MIN_LEN rows)
+constexpr int FUSED_MIN_LEN = 4096;
+bool select_fused_applies(const tav2_seq& seq);
+size_t select_fused_workspace(const tav2_cands& c, int k);
+// cand_req (nullable): also receives each candidate's request index.
+hipError_t launch_select_fused(const tav2_seq& seq, const tav2_cands& c, int k,
+                               int32_t* out_idx, float* out_score, int32_t* cand_req, void* ws,
+                               hipStream_t st);
+
 // ---- gather.hip
 // Where encoder tokens come from: either explicit token tensors, or the
 // selection (idx) into the request sequence plus an optional real-time tail.
@@ -67,17 +77,14 @@ hipError_t launch_gather(const tav2_seq& seq, const tav2_seq* rt, const tav2_can
                          const int32_t* idx, int k, int T, void* tok_emb, uint8_t* tok_act,
                          uint8_t* tok_time, int32_t* valid_len, hipStream_t st);
 
-// ---- encoder_bf16.hip
-size_t encode_bf16_workspace(int64_t total, int T, const tav2_weights& w);
-hipError_t launch_encode_bf16(const TokenSource& src, const void* cand_emb, int64_t total,
-                              const tav2_weights& w, float* out, void* ws, size_t ws_bytes,
-                              hipStream_t st);
-
 // ---- encoder_fused.hip
 bool encode_fused_supported(int d, const tav2_weights& w);
 size_t encode_fused_workspace(int64_t total, int T, const tav2_weights& w);
+size_t encode_fused_packed_bytes(const tav2_weights& w);
+hipError_t launch_encode_fused_pack(const tav2_weights& w, void* dst, hipStream_t st);
 hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int64_t total,
-                               const tav2_weights& w, float* out, void* ws, hipStream_t st);
+                               const tav2_weights& w, float* out, void* ws, bool unmasked,
+                               hipStream_t st);
 
 // ---- encoder_f32.hip
 constexpr int F32_MAX_T = 64;
@@ -86,6 +93,6 @@ constexpr int F32_MAX_FFN = 512;
 constexpr int F32_LDS_FLOATS = 36 * 1024;
 bool encode_f32_fits(int T, const tav2_weights& w);
 hipError_t launch_encode_f32(const TokenSource& src, const void* cand_emb, int64_t total,
-                             const tav2_weights& w, float* out, hipStream_t st);
+                             const tav2_weights& w, float* out, bool unmasked, hipStream_t st);
 
 }  // namespace tav2

@@ -20,6 +20,7 @@
 
 #include "common.h"
 #include "internal.h"
+#include "select_common.h"
 
 namespace tav2 {
 
@@ -109,23 +110,8 @@ __global__ __launch_bounds__(256) void score_bf16_kernel(
 // ---------------------------------------------------------------- scores, int8
 // The int8 sequence storage (codes q, Sec. 3.2.1) with dequantisation and L2
 // normalisation fused into the score kernel (Sec. 3.4.2): s = <q_i, c> / |q_i|
-// (the dequantisation scale cancels in the normalisation).  Each lane converts
-// its 8 codes per k-block to bf16 (exact: |q| <= 127) for the MFMA and adds their squares (exact in fp32: the row's sum of
-// squares is an integer below 2^24), the two lanes holding a row's halves
-// combine them, and the epilogue divides by the square root (both rounded to
-// nearest: the build keeps division and square root correctly rounded).
-__device__ __forceinline__ bf16x8 codes_to_bf16(uint2 raw, float& sq) {
-  bf16x8 v;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const uint32_t word = j < 4 ? raw.x : raw.y;
-    const float x = float(int8_t((word >> (8 * (j & 3))) & 0xFF));
-    sq = fmaf(x, x, sq);
-    v[j] = static_cast<__bf16>(x);
-  }
-  return v;
-}
-
+// (the dequantisation scale cancels in the normalisation); codes_to_bf16 and
+// i8_score (select_common.h) give the products' operands and the epilogue.
 // Block: 4 waves, 32 candidates x 256 rows (a narrow candidate tile: the codes are
 // short, so the block count, not operand reuse, sets the speed).  The normalised
 // scores are staged in LDS and leave as one 1 KB non-temporal store per candidate
@@ -188,11 +174,10 @@ __global__ __launch_bounds__(256) void score_i8_kernel(
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     const float ss = sq[t] + __shfl_xor(sq[t], 32, WAVE);   // the row's other half
-    const float nrm = sqrtf(ss);
 #pragma unroll
     for (int reg = 0; reg < 16; ++reg)
       stile[(8 * (reg / 4) + 4 * h + (reg % 4)) * SI_SLD + 64 * w + 32 * t + l32] =
-          ss > 0.f ? acc[t][reg] / nrm : 0.f;
+          i8_score(acc[t][reg], ss);
   }
   __syncthreads();
   const int nv = min(SI_ROWS, L - ib);   // valid rows of this block

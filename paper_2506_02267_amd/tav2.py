@@ -18,6 +18,7 @@ import torch
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtav2.so")
 
 F32, BF16, I8 = 0, 1, 2
+MASK_CAUSAL, MASK_NONE = 0, 1
 K_MAX, T_MAX = 1024, 1024
 STATUS = {0: "ok", -1: "null", -2: "shape", -3: "dtype", -4: "unsupported", -5: "workspace",
           -6: "hip"}
@@ -51,7 +52,7 @@ class Weights(ctypes.Structure):
                 ("dtype", c_int32), ("reserved", c_int32), ("W_in", c_void_p),
                 ("b_in", c_void_p), ("E_act", c_void_p), ("E_time", c_void_p),
                 ("E_pos", c_void_p), ("layers", POINTER(Layer)), ("W_pool", c_void_p),
-                ("b_pool", c_void_p)]
+                ("b_pool", c_void_p), ("packed", c_void_p), ("packed_bytes", ctypes.c_uint64)]
 
 
 FUNCTIONS = {
@@ -63,13 +64,15 @@ FUNCTIONS = {
     "tav2_gather": (c_int32, [POINTER(Seq), POINTER(Seq), POINTER(Cands), c_void_p, c_int32,
                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
     "tav2_encode_workspace": (c_size_t, [POINTER(Tokens), POINTER(Weights)]),
-    "tav2_encode": (c_int32, [POINTER(Tokens), c_void_p, POINTER(Weights), c_void_p, c_void_p,
-                              c_size_t, c_void_p]),
+    "tav2_pack_weights_bytes": (c_size_t, [POINTER(Weights)]),
+    "tav2_pack_weights": (c_int32, [POINTER(Weights), c_void_p, c_size_t, c_void_p]),
+    "tav2_encode": (c_int32, [POINTER(Tokens), c_void_p, POINTER(Weights), ctypes.c_uint32,
+                              c_void_p, c_void_p, c_size_t, c_void_p]),
     "tav2_select_encode_workspace": (c_size_t, [POINTER(Seq), POINTER(Seq), POINTER(Cands),
                                                 c_int32, POINTER(Weights)]),
     "tav2_select_encode": (c_int32, [POINTER(Seq), POINTER(Seq), POINTER(Cands), c_int32,
-                                     POINTER(Weights), c_void_p, c_void_p, c_void_p, c_void_p,
-                                     c_size_t, c_void_p]),
+                                     POINTER(Weights), ctypes.c_uint32, c_void_p, c_void_p,
+                                     c_void_p, c_void_p, c_size_t, c_void_p]),
     "tav2_profile_enable": (c_int32, [c_int32, ctypes.c_char_p]),
     "tav2_profile_report": (ctypes.c_int64, [ctypes.c_char_p, c_size_t]),
 }
@@ -213,9 +216,13 @@ class DeviceTokens:
 
 
 class DeviceWeights:
-    """Encoder weights on the GPU (matrices/tables in the compute dtype, vectors fp32)."""
+    """Encoder weights on the GPU (matrices/tables in the compute dtype, vectors fp32).
 
-    def __init__(self, w, device="cuda"):
+    pack=True also packs them once (tav2_pack_weights) and points the struct at
+    the packed copy, so that later calls skip the packing step.
+    """
+
+    def __init__(self, w, device="cuda", pack=False):
         self.dtype = BF16 if w.dtype == "bf16" else F32
         md = torch_dtype(self.dtype)
         f32 = torch.float32
@@ -240,8 +247,29 @@ class DeviceWeights:
                          n_layers=len(w.layers), max_pos=w.max_pos, dtype=self.dtype, reserved=0,
                          W_in=m(w.W_in), b_in=v(w.b_in), E_act=m(w.E_act),
                          E_time=None if w.E_time is None else m(w.E_time), E_pos=m(w.E_pos),
-                         layers=self.layers, W_pool=m(w.W_pool), b_pool=v(w.b_pool))
+                         layers=self.layers, W_pool=m(w.W_pool), b_pool=v(w.b_pool),
+                         packed=None, packed_bytes=0)
         self.d_model = w.d_model
+        self.packed: Optional[torch.Tensor] = None
+        if pack:
+            self.pack()
+
+    def pack(self, stream=None):
+        """Pack the matrices once into a device buffer the struct then refers to."""
+        lib = load_library()
+        self.s.packed, self.s.packed_bytes = None, 0
+        need = lib.tav2_pack_weights_bytes(ctypes.byref(self.s))
+        if need == 0:
+            return self
+        buf = torch.empty(need + 256, dtype=torch.uint8, device=self.keep[0].device)
+        p = buf.data_ptr()
+        off = (-p) % 256
+        _check("tav2_pack_weights", lib.tav2_pack_weights(ctypes.byref(self.s),
+                                                          ctypes.c_void_p(p + off), need,
+                                                          _stream_handle(stream)))
+        self.packed = buf
+        self.s.packed, self.s.packed_bytes = p + off, need
+        return self
 
 
 class Workspace:
@@ -306,7 +334,7 @@ def gather(seq: DeviceSeq, rt: Optional[DeviceSeq], cands: DeviceCands, idx: tor
 
 
 def encode(tokens: DeviceTokens, cand_emb: torch.Tensor, w: DeviceWeights, out=None,
-           ws: Optional[Workspace] = None, stream=None) -> torch.Tensor:
+           ws: Optional[Workspace] = None, stream=None, flags: int = MASK_CAUSAL) -> torch.Tensor:
     lib = load_library()
     t = tokens.struct()
     dev = tokens.emb.device
@@ -316,7 +344,7 @@ def encode(tokens: DeviceTokens, cand_emb: torch.Tensor, w: DeviceWeights, out=N
     need = lib.tav2_encode_workspace(ctypes.byref(t), ctypes.byref(w.s))
     wp, wb = ws.get(need)
     _check("tav2_encode", lib.tav2_encode(ctypes.byref(t), _ptr(cand_emb), ctypes.byref(w.s),
-                                          _ptr(out), wp, wb, _stream_handle(stream)))
+                                          flags, _ptr(out), wp, wb, _stream_handle(stream)))
     _used_on(stream, ws.buf, out)
     return out
 
@@ -334,9 +362,10 @@ class SelectEncode:
     """Prepared call of tav2_select_encode: structs, outputs and workspace built once."""
 
     def __init__(self, seq: DeviceSeq, rt: Optional[DeviceSeq], cands: DeviceCands, k: int,
-                 w: DeviceWeights):
+                 w: DeviceWeights, flags: int = MASK_CAUSAL):
         self.lib = load_library()
         self.seq, self.rt, self.cands, self.k, self.w = seq, rt, cands, k, w
+        self.flags = flags
         self.s, self.c = seq.struct(), cands.struct()
         self.r = rt.struct() if rt is not None else None
         dev = seq.emb.device
@@ -353,7 +382,7 @@ class SelectEncode:
     def __call__(self, stream=None):
         _check("tav2_select_encode", self.lib.tav2_select_encode(
             ctypes.byref(self.s), ctypes.byref(self.r) if self.r is not None else None,
-            ctypes.byref(self.c), self.k, ctypes.byref(self.w.s), _ptr(self.idx),
+            ctypes.byref(self.c), self.k, ctypes.byref(self.w.s), self.flags, _ptr(self.idx),
             _ptr(self.score), _ptr(self.out), self.wp, self.wb, _stream_handle(stream)))
         return self.idx, self.score, self.out
 
@@ -377,5 +406,5 @@ def profile_report() -> dict:
     return out
 
 
-def select_encode(seq, rt, cands, k, w, stream=None):
-    return SelectEncode(seq, rt, cands, k, w)(stream)
+def select_encode(seq, rt, cands, k, w, stream=None, flags: int = MASK_CAUSAL):
+    return SelectEncode(seq, rt, cands, k, w, flags)(stream)

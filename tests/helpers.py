@@ -1,4 +1,8 @@
-"""Shared plumbing for the GPU parity tests (device upload, oracle sampling)."""
+"""Shared plumbing for the GPU parity tests (device upload, oracle sampling,
+the oracle spread over the host's cores)."""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import torch
 
@@ -22,20 +26,6 @@ def upload(inp, device="cuda"):
     return seq, rt, cands
 
 
-def sample_ids(inp, per_request):
-    ids = []
-    for r in range(inp.seq.R):
-        a, b = int(inp.cand_offset[r]), int(inp.cand_offset[r + 1])
-        n = b - a
-        if n == 0:
-            continue
-        step = max(1, n // per_request)
-        ids.extend(range(a, b, step)[:per_request])
-        if b - 1 not in ids:
-            ids.append(b - 1)
-    return np.array(sorted(set(ids)), dtype=np.int64)
-
-
 def assert_select_equal(idx_gpu, score_gpu, idx_ref, score_ref, ids=None):
     ig = idx_gpu.cpu().numpy()
     sg = score_gpu.cpu().numpy()
@@ -53,3 +43,73 @@ def max_abs(out_gpu, out_ref, ids=None):
         og, out_ref = og[ids], out_ref[ids]
     assert np.all(np.isfinite(og))
     return float(np.abs(og - out_ref).max()) if og.size else 0.0
+
+
+def host_workers():
+    """Threads for oracle work: the host's cores, at most 16 (one GPU's share)."""
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def parallel_map(fn, parts):
+    """fn over parts on host_workers() threads with single-threaded BLAS (numpy
+    releases the GIL in its array loops and BLAS calls, so the oracle's pieces
+    run side by side)."""
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(1):
+        with ThreadPoolExecutor(host_workers()) as ex:
+            return list(ex.map(fn, parts))
+
+
+def chunks(ids, size):
+    ids = np.asarray(ids, dtype=np.int64)
+    return [ids[i:i + size] for i in range(0, ids.size, size)]
+
+
+def oracle_select(inp, k, ids=None, chunk=64):
+    """oracle.nn_select_batch for the candidates in ids (all by default), split
+    into chunks computed in parallel; rows outside ids are padding."""
+    total = inp.total
+    ids = np.arange(total) if ids is None else np.asarray(ids, dtype=np.int64)
+    idx = np.full((total, k), -1, dtype=np.int32)
+    score = np.full((total, k), -np.inf, dtype=np.float32)
+
+    def one(part):
+        i, s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k, only=part)
+        return part, i[part], s[part]
+
+    for part, i, s in parallel_map(one, chunks(ids, chunk)):
+        idx[part], score[part] = i, s
+    return idx, score
+
+
+def oracle_select_encode(inp, W, k, ids=None, chunk=16, causal=True):
+    """oracle.select_encode for the candidates in ids (all by default), in
+    parallel chunks.  Returns idx, score, out as oracle.select_encode does."""
+    total = inp.total
+    ids = np.arange(total) if ids is None else np.asarray(ids, dtype=np.int64)
+    idx = np.full((total, k), -1, dtype=np.int32)
+    score = np.full((total, k), -np.inf, dtype=np.float32)
+    out = np.zeros((total, 2 * W.d_model), dtype=np.float64)
+
+    def one(part):
+        i, s, o = oracle.select_encode(inp, W, k, only=part, causal=causal)
+        return part, i[part], s[part], o[part]
+
+    for part, i, s, o in parallel_map(one, chunks(ids, chunk)):
+        idx[part], score[part], out[part] = i, s, o
+    return idx, score, out
+
+
+def strided_ids(inp, stride, boundaries=()):
+    """Every stride-th candidate of every request (from its first), the last
+    candidate of each request, and both candidates on each side of every global
+    index in boundaries (launch chunk edges)."""
+    ids = set()
+    for r in range(inp.seq.R):
+        a, b = int(inp.cand_offset[r]), int(inp.cand_offset[r + 1])
+        ids.update(range(a, b, stride))
+        if b > a:
+            ids.add(b - 1)
+    for e in boundaries:
+        ids.update(x for x in (e - 1, e) if 0 <= x < inp.total)
+    return np.array(sorted(ids), dtype=np.int64)

@@ -67,7 +67,8 @@ def fake_weights(d=64, dm=256, heads=4, ffn=512, layers=2, max_pos=64, dtype=T.B
     L = (T.Layer * layers)(*[T.Layer(*([FAKE] * 12)) for _ in range(layers)])
     w = T.Weights(d_in=d, d_model=dm, n_heads=heads, d_ffn=ffn, n_layers=layers,
                   max_pos=max_pos, dtype=dtype, reserved=0, W_in=FAKE, b_in=FAKE, E_act=FAKE,
-                  E_time=FAKE if time else None, E_pos=FAKE, layers=L, W_pool=FAKE, b_pool=FAKE)
+                  E_time=FAKE if time else None, E_pos=FAKE, layers=L, W_pool=FAKE, b_pool=FAKE,
+                  packed=None, packed_bytes=0)
     w._keep = L
     return w
 
@@ -165,6 +166,8 @@ def test_empty_candidate_set_is_a_no_op():
     ("dtype_mismatch", -3), ("heads", -2), ("dm_unsupported", -4), ("ffn", -4),
     ("max_pos", -2), ("time_mismatch", -2), ("null_layer_ptr", -1), ("T_too_big", -2),
     ("f32_too_big", -4), ("null_out", -1), ("ws", -5), ("d_in", -2),
+    ("flags", -2), ("unmasked_two_blocks", -4), ("packed_small", -5), ("packed_misaligned", -5),
+    ("d_wide", -4), ("nine_layers", -4),
 ])
 def test_encode_argument_errors(case, status):
     lib = T.load_library()
@@ -200,8 +203,58 @@ def test_encode_argument_errors(case, status):
         wsb = 10
     elif case == "d_in":
         w.d_in = 32
-    st = lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), out, ws, wsb, None)
+    elif case == "d_wide":   # bf16 token embeddings wider than 256
+        tok.d, w.d_in = 512, 512
+    elif case == "nine_layers":
+        w = fake_weights(layers=9)
+    flags = T.MASK_CAUSAL
+    if case == "flags":
+        flags = 7
+    elif case == "unmasked_two_blocks":   # bf16 unmasked: one block of 128 positions
+        flags = T.MASK_NONE
+        tok.T = 129
+        w.max_pos = 129
+    elif case == "packed_small":
+        w.packed, w.packed_bytes = FAKE, 1024
+    elif case == "packed_misaligned":
+        w.packed, w.packed_bytes = FAKE + 16, 1 << 40
+    st = lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), flags, out, ws, wsb, None)
     assert st == status
+
+
+def test_unmasked_encoder_accepted_within_one_block():
+    """TAV2_MASK_NONE passes the checks at T = 128 (the error then comes from the
+    missing output), and for float32 at any supported T."""
+    lib = T.load_library()
+    w = fake_weights(max_pos=128)
+    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10,
+                   T=128, d=64, dtype=T.BF16, reserved=0)
+    assert lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), T.MASK_NONE, None, FAKE,
+                           1 << 40, None) == -1
+    wf = fake_weights(dm=64, heads=2, ffn=128, layers=1, dtype=T.F32)
+    tokf = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10,
+                    T=64, d=64, dtype=T.F32, reserved=0)
+    assert lib.tav2_encode(ctypes.byref(tokf), FAKE, ctypes.byref(wf), T.MASK_NONE, None, FAKE,
+                           1 << 40, None) == -1
+
+
+def test_packed_weights_queries_and_errors():
+    lib = T.load_library()
+    w = fake_weights()
+    need = lib.tav2_pack_weights_bytes(ctypes.byref(w))
+    assert need > 0 and need % 256 == 0
+    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
+                   d=64, dtype=T.BF16, reserved=0)
+    ws_unpacked = lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w))
+    w.packed, w.packed_bytes = FAKE, need
+    # with packed weights the workspace no longer holds a packed copy
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == ws_unpacked - need
+    assert lib.tav2_pack_weights(ctypes.byref(w), None, need, None) == -5
+    assert lib.tav2_pack_weights(ctypes.byref(w), FAKE, need - 256, None) == -5
+    assert lib.tav2_pack_weights(None, FAKE, need, None) == -1
+    wf = fake_weights(dm=64, heads=2, ffn=128, layers=1, dtype=T.F32)
+    assert lib.tav2_pack_weights_bytes(ctypes.byref(wf)) == 0
+    assert lib.tav2_pack_weights(ctypes.byref(wf), None, 0, None) == 0   # nothing to pack
 
 
 def test_select_encode_checks_realtime_and_positions():
@@ -210,17 +263,21 @@ def test_select_encode_checks_realtime_and_positions():
     rt = fake_seq(d=64, max_len=100)
     w = fake_weights(max_pos=64 + 99)
     st = lib.tav2_select_encode(ctypes.byref(s), ctypes.byref(rt), ctypes.byref(c), 64,
-                                ctypes.byref(w), FAKE, FAKE, FAKE, FAKE, 1 << 40, None)
+                                ctypes.byref(w), 0, FAKE, FAKE, FAKE, FAKE, 1 << 40, None)
     assert st == -2          # k + rt->max_len exceeds max_pos
     rt2 = fake_seq(R=3, d=64, max_len=10)
     st = lib.tav2_select_encode(ctypes.byref(s), ctypes.byref(rt2), ctypes.byref(c), 64,
-                                ctypes.byref(fake_weights(max_pos=100)), FAKE, FAKE, FAKE, FAKE,
-                                1 << 40, None)
+                                ctypes.byref(fake_weights(max_pos=100)), 0, FAKE, FAKE, FAKE,
+                                FAKE, 1 << 40, None)
     assert st == -2          # real-time batch with a different request count
     st = lib.tav2_select_encode(ctypes.byref(s), None, ctypes.byref(c), 64,
-                                ctypes.byref(fake_weights(time=False)), FAKE, FAKE, FAKE, FAKE,
+                                ctypes.byref(fake_weights(time=False)), 0, FAKE, FAKE, FAKE, FAKE,
                                 1 << 40, None)
     assert st == -2          # sequence has time buckets, weights have no time table
+    st = lib.tav2_select_encode(ctypes.byref(s), None, ctypes.byref(c), 64,
+                                ctypes.byref(fake_weights(max_pos=200)), 2, FAKE, FAKE, FAKE,
+                                FAKE, 1 << 40, None)
+    assert st == -2          # unknown flags
 
 
 def test_status_strings():
@@ -244,8 +301,31 @@ def test_int8_sequence_is_for_the_nn_search_only():
     w = fake_weights(d=32)
     tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
                    d=32, dtype=T.I8, reserved=0)
-    assert lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), FAKE, FAKE, 1 << 40,
+    assert lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), 0, FAKE, FAKE, 1 << 40,
                            None) == -4
-    st = lib.tav2_select_encode(ctypes.byref(s), None, ctypes.byref(c), 8, ctypes.byref(w), FAKE,
-                                FAKE, FAKE, FAKE, 1 << 40, None)
+    st = lib.tav2_select_encode(ctypes.byref(s), None, ctypes.byref(c), 8, ctypes.byref(w), 0,
+                                FAKE, FAKE, FAKE, FAKE, 1 << 40, None)
     assert st == -4
+
+
+def test_fused_search_workspace_does_not_scale_with_the_sequence():
+    """Sequences of more than 4096 rows (bf16 and int8) keep their scores on chip:
+    the workspace holds per candidate 1024 sampled 16-bit keys, a threshold, a
+    count, a survivor list of 2 k + 1024 (rounded up to 64) 8-byte values and a
+    queue slot; shorter ones, and float32, hold the score rows."""
+    lib = T.load_library()
+    c = fake_cands(total=10, max_count=10)
+
+    def a256(x):
+        return (x + 255) // 256 * 256
+
+    for dt in (T.BF16, T.I8):
+        for L in (16384, 32768):
+            s = fake_seq(R=1, d=64, dtype=dt, max_len=L)
+            want = (a256(10 * 1024 * 2) + a256(40) + a256(40) + a256(10 * 1536 * 8) + a256(80)
+                    + a256(4))
+            assert lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 256) == want
+        s = fake_seq(R=1, d=64, dtype=dt, max_len=4096)
+        assert lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 256) == 10 * 4096 * 4
+    s = fake_seq(R=1, d=64, dtype=T.F32, max_len=16384)
+    assert lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 256) == 10 * 16384 * 4

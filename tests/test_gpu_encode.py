@@ -7,27 +7,32 @@ import torch
 
 import oracle
 import synth
-from helpers import BF16_TOL, F32_TOL, assert_select_equal, max_abs, sample_ids, upload
+from helpers import (BF16_TOL, F32_TOL, assert_select_equal, max_abs, oracle_select_encode,
+                     strided_ids, upload)
 from paper_2506_02267_amd import tav2 as T
 
 pytestmark = pytest.mark.gpu
 
 
-def run_path(inp, W):
+def run_path(inp, W, flags=T.MASK_CAUSAL, pack=False):
     seq, rt, cands = upload(inp)
-    dw = T.DeviceWeights(W)
-    idx, score, out = T.select_encode(seq, rt, cands, inp.w.k, dw)
+    dw = T.DeviceWeights(W, pack=pack)
+    idx, score, out = T.select_encode(seq, rt, cands, inp.w.k, dw, flags=flags)
     torch.cuda.synchronize()
     return idx, score, out
 
 
-def check_workload(w, per_request=None, W=None, inp=None):
+def check_workload(w, ids=None, W=None, inp=None, gpu=None, flags=T.MASK_CAUSAL):
+    """The whole path against the oracle on the candidates in ids (all by default);
+    gpu: outputs of an earlier run of the same inputs, reused."""
     inp = inp if inp is not None else synth.make_inputs(w)
     W = W if W is not None else synth.make_weights(w)
-    print(f"select_encode workload {w.name} R={w.R} N={w.N} T={w.T}", flush=True)
-    idx, score, out = run_path(inp, W)
-    ids = None if per_request is None else sample_ids(inp, per_request)
-    ref_i, ref_s, ref_out = oracle.select_encode(inp, W, w.k, only=ids)
+    n_ids = inp.total if ids is None else len(ids)
+    print(f"select_encode workload {w.name} R={w.R} N={w.N} T={w.T}: {n_ids} of {inp.total} "
+          f"candidates, flags {flags}", flush=True)
+    idx, score, out = gpu if gpu is not None else run_path(inp, W, flags)
+    ref_i, ref_s, ref_out = oracle_select_encode(inp, W, w.k, ids=ids,
+                                                 causal=flags == T.MASK_CAUSAL)
     assert_select_equal(idx, score, ref_i, ref_s, ids=ids)
     err = max_abs(out, ref_out, ids=ids)
     tol = F32_TOL if w.dtype == "f32" else BF16_TOL
@@ -65,9 +70,38 @@ def test_small_mixed_realtime_tail():
     check_workload(w)
 
 
-@pytest.mark.parametrize("cid,per", [(2, 40), (3, 2), (4, 24), (5, 2)])
-def test_full_workload_sampled(cid, per):
-    check_workload(synth.WORKLOADS[cid], per_request=per)
+@pytest.mark.parametrize("cid", [2, 4])
+def test_full_workload_all_candidates(cid):
+    """Every candidate of the single-request workloads (1000 each)."""
+    check_workload(synth.WORKLOADS[cid])
+
+
+def test_ragged_workload_every_8th_candidate():
+    """Every 8th candidate of each of the 64 requests (4,000 of 32,000) and the
+    last one of each; T = 128 is one encoder block, one launch."""
+    w = synth.RAGGED
+    inp = synth.make_inputs(w)
+    check_workload(w, ids=strided_ids(inp, 8), inp=inp)
+
+
+_STRESS = {}
+
+
+@pytest.mark.parametrize("part", range(4))
+def test_stress_workload_every_8th_candidate(part):
+    """Every 8th candidate of each request (8,000 of 64,000), the last one of each,
+    and both candidates at every edge of the encoder's 2048-candidate launches
+    (T = 512 positions: four blocks joined by a K/V cache of 1 MB per candidate,
+    2 GB per launch), checked four requests at a time; the GPU runs once."""
+    w = synth.STRESS
+    if "run" not in _STRESS:
+        inp = synth.make_inputs(w)
+        W = synth.make_weights(w)
+        _STRESS["run"] = (inp, W, run_path(inp, W))
+    inp, W, gpu = _STRESS["run"]
+    ids = strided_ids(inp, 8, boundaries=range(2048, inp.total, 2048))
+    lo, hi = int(inp.cand_offset[4 * part]), int(inp.cand_offset[4 * part + 4])
+    check_workload(w, ids=ids[(ids >= lo) & (ids < hi)], W=W, inp=inp, gpu=gpu)
 
 
 def test_short_and_empty_requests_pad_and_zero():
@@ -133,3 +167,42 @@ def test_repeated_runs_bitwise_identical():
         again = call()
         for a, b in zip(first, again):
             assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("case", ["bf16_4heads", "bf16_8heads_ragged", "bf16_rt_tail_128",
+                                  "f32_tiny"])
+def test_unmasked_encoder(case):
+    """TAV2_MASK_NONE: every valid position attends to every valid position (the
+    oracle's causal=False), with padding keys excluded; bf16 within one block of
+    128 positions."""
+    if case == "bf16_4heads":
+        w = synth.scaled(synth.SINGLE, R=2, L=3000, N=24, k=64)
+    elif case == "bf16_8heads_ragged":   # k past some row counts: valid lengths 40 and 17
+        w = synth.scaled(synth.STRESS, R=2, L=None, L_range=(17, 45), N=12, k=40, tie_frac=0.0)
+    elif case == "bf16_rt_tail_128":     # T = 100 + 28 = 128 exactly
+        w = synth.scaled(synth.MIXED, L=2000, N=16, k=100, rt_len=28)
+    else:
+        w = synth.TINY
+    check_workload(w, flags=T.MASK_NONE)
+
+
+def test_unmasked_differs_from_causal():
+    w = synth.scaled(synth.SINGLE, R=1, L=2000, N=8, k=64)
+    inp = synth.make_inputs(w)
+    W = synth.make_weights(w)
+    _, _, causal = run_path(inp, W)
+    _, _, unmasked = run_path(inp, W, flags=T.MASK_NONE)
+    assert float((causal - unmasked).abs().max()) > 1e-3
+
+
+@pytest.mark.parametrize("k", [64, 256])   # one block; two blocks joined by the K/V cache
+def test_packed_weights_equal_per_call_packing(k):
+    """Weights packed once (tav2_pack_weights) give the outputs of the per-call
+    packing bit for bit."""
+    w = synth.scaled(synth.MIXED, L=3000, N=40, k=k, rt_len=20)
+    inp = synth.make_inputs(w, seed=55)
+    W = synth.make_weights(w)
+    a = run_path(inp, W)
+    b = run_path(inp, W, pack=True)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)

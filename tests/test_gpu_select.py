@@ -1,16 +1,16 @@
 """GPU parity of tav2_nn_select (Eq. 3) against the oracle: indices and scores
-bit for bit, on the five workloads (full runs, all or sampled candidates) and
-on edge cases (ragged, empty and short requests, k = 1 and k = K_MAX, heavy
-ties, padded layout, every register-tile size of the short-row top-k and the
-long-row (streaming) top-k with short rows in its batch, ties inside its
-sampled-threshold path and inputs that make it fall back)."""
+bit for bit, on the five workloads (every candidate of each) and on edge cases
+(ragged, empty and short requests, k = 1 and k = K_MAX, heavy ties, padded
+layout, every register-tile size of the short-row top-k, the fused search for
+long rows with short rows in its batch, ties inside its survivor lists, inputs
+that send it to its exhaustive fallback, and the float32 streaming top-k)."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
 import synth
-from helpers import assert_select_equal, sample_ids, upload
+from helpers import assert_select_equal, oracle_select, upload
 from paper_2506_02267_amd import tav2 as T
 
 pytestmark = pytest.mark.gpu
@@ -23,25 +23,15 @@ def run_select(inp, k):
     return idx, score
 
 
-@pytest.mark.parametrize("cid", [1, 2, 4])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
 def test_full_workload_all_candidates(cid):
+    """Every candidate of every workload (32,000 at ragged, 64,000 at stress)."""
     w = synth.WORKLOADS[cid]
     inp = synth.make_inputs(w)
-    print(f"select workload {w.name}", flush=True)
+    print(f"select workload {w.name}: all {inp.total} candidates", flush=True)
     idx, score = run_select(inp, w.k)
-    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, w.k)
+    ref_i, ref_s = oracle_select(inp, w.k)
     assert_select_equal(idx, score, ref_i, ref_s)
-
-
-@pytest.mark.parametrize("cid,per", [(3, 6), (5, 12)])
-def test_full_workload_sampled_candidates(cid, per):
-    w = synth.WORKLOADS[cid]
-    inp = synth.make_inputs(w)
-    print(f"select workload {w.name}", flush=True)
-    idx, score = run_select(inp, w.k)
-    ids = sample_ids(inp, per)
-    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, w.k, only=ids)
-    assert_select_equal(idx, score, ref_i, ref_s, ids=ids)
 
 
 def custom_inputs(lengths, counts, d=64, dtype="bf16", levels=8, seed=0):
@@ -121,11 +111,12 @@ def test_sampled_threshold_with_tied_rows(k):
 
 @pytest.mark.parametrize("case", ["all_equal", "sample_misses_top"])
 def test_sampled_threshold_falls_back(case):
-    # inputs for which the sample gives no usable threshold: all scores equal (far
-    # more than the candidate capacity at the threshold), or the largest scores
-    # only on rows the sample never looks at (the sample of a 16384-row request is
-    # the 64-row blocks starting at multiples of 512: big scores on rows = 2 mod 4
-    # outside those blocks)
+    # inputs for which the sample gives no usable threshold, so every candidate
+    # takes the exhaustive fallback: all scores equal (16384 survivors, far above
+    # the list capacity), or the largest scores only on rows the sample never
+    # looks at (the sample of a 16384-row request is the 32-row blocks starting at
+    # multiples of 512: big scores on rows = 2 mod 4 outside those blocks, about
+    # 3600 of them, again above the capacity)
     inp = custom_inputs([16384], [4], d=32, levels=8, seed=5)
     e = inp.seq.emb
     if case == "all_equal":
@@ -139,6 +130,36 @@ def test_sampled_threshold_falls_back(case):
     idx, score = run_select(inp, 512)
     ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, 512)
     assert_select_equal(idx, score, ref_i, ref_s)
+
+
+@pytest.mark.parametrize("lengths", [[4096, 300], [4097, 5], [6000, 4000, 0, 1]])
+def test_materialised_and_fused_paths_meet(lengths):
+    # the longest request decides the path: at most 4096 rows keep the score rows
+    # in memory (register top-k), beyond it the scores stay on chip
+    inp = custom_inputs(lengths, [3] * len(lengths), d=48, seed=sum(lengths))
+    for k in (1, 100, 1024):
+        idx, score = run_select(inp, k)
+        ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
+        assert_select_equal(idx, score, ref_i, ref_s)
+
+
+def test_many_candidate_tiles_with_a_ragged_tail():
+    # 3 requests x 300 candidates: three 128-candidate tiles, the last one partial
+    inp = custom_inputs([9000, 16384, 5000], [300, 300, 300], d=64, seed=41)
+    idx, score = run_select(inp, 256)
+    ref_i, ref_s = oracle_select(inp, 256)
+    assert_select_equal(idx, score, ref_i, ref_s)
+
+
+@pytest.mark.parametrize("L", [5000, 20000])
+def test_f32_long_rows_stream_topk(L):
+    # float32 sequences keep the materialised score rows at every length: rows of
+    # more than 4096 keys take the streaming top-k
+    inp = custom_inputs([L, 700], [5, 3], d=32, dtype="f32", seed=L + 1)
+    for k in (1, 256, 1024):
+        idx, score = run_select(inp, k)
+        ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, k)
+        assert_select_equal(idx, score, ref_i, ref_s)
 
 
 def test_zero_scores_are_positive_zero():

@@ -41,11 +41,35 @@ def test_several_long_requests_large_k():
     check(w, seed=25, zero_every=2003)
 
 
+@pytest.mark.parametrize("case", ["all_equal", "sample_misses_top"])
+def test_fused_search_falls_back(case):
+    """Inputs whose sample gives no usable threshold: every candidate takes the
+    exhaustive fallback, whose recomputed scores must match the oracle's."""
+    w = synth.scaled(synth.SELECT_I8, N=5, k=512)
+    inp = synth.make_inputs(w, seed=26)
+    e = inp.seq.emb
+    if case == "all_equal":
+        e[:] = e[7]
+    else:
+        rows = np.arange(e.shape[0])
+        big = (rows % 4 == 2) & (rows % 512 >= 64)
+        e[:] = -np.abs(e)
+        e[big] = np.abs(e[big])
+        inp.cand[:] = np.abs(inp.cand) + 0.125
+    seq, _, cands = upload(inp)
+    idx, score = T.nn_select(seq, cands, w.k)
+    torch.cuda.synchronize()
+    ref_i, ref_s = oracle.nn_select_batch(inp.seq, inp.cand, inp.cand_offset, w.k)
+    assert_select_equal(idx, score, ref_i, ref_s)
+
+
 @pytest.mark.parametrize("d,R,Lr,N,k,seed", [
     (32, 3, (1, 700), 130, 64, 21),       # 2 candidate tiles, ragged tails, short rows
     (256, 2, (300, 2100), 40, 256, 22),   # wide codes, k above some row counts
     (16, 2, (37, 37), 1, 100, 23),        # narrowest rows, k > L (padding)
-    (512, 1, (5000, 5000), 9, 33, 24),    # widest rows, long-row top-k
+    (512, 1, (5000, 5000), 9, 33, 24),    # widest rows, long rows (fused search)
+    (64, 3, (4000, 4096), 50, 128, 27),   # longest request 4096: materialised scores
+    (64, 3, (4000, 4097), 50, 128, 28),   # longest 4097: fused search, short rows inside
 ])
 def test_ragged_batches(d, R, Lr, N, k, seed):
     w = synth.scaled(synth.SELECT_I8, R=R, L=None, L_range=Lr, d=d, N=N, k=k, tie_frac=0.05)
