@@ -57,6 +57,7 @@ typedef int32_t tav2_status;
 #define TAV2_ERR_UNSUPPORTED -4   /* a valid request this build does not implement */
 #define TAV2_ERR_WORKSPACE   -5   /* workspace NULL or smaller than the query says */
 #define TAV2_ERR_HIP         -6   /* a HIP launch failed */
+#define TAV2_ERR_TOO_LARGE   -7   /* the request needs more than the static scratch holds */
 
 #define TAV2_F32  0   /* float32 storage and arithmetic */
 #define TAV2_BF16 1   /* bfloat16 storage, fp32 accumulation */
@@ -188,6 +189,24 @@ size_t tav2_nn_select_workspace(const tav2_seq* seq, const tav2_cands* cands, in
 tav2_status tav2_nn_select(const tav2_seq* seq, const tav2_cands* cands, int32_t k,
                            int32_t* out_idx, float* out_score,
                            void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * tav2_nn_select without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP-graph capture, serving loops and
+ * harnesses that forbid allocation).  The search's working memory is a static
+ * device buffer of TAV2_SCRATCH_BYTES inside the library (one per GPU, held from
+ * the first call on that GPU until the process ends; no allocation on any
+ * call).  Requests whose workspace (tav2_nn_select_workspace) exceeds it return
+ * TAV2_ERR_TOO_LARGE before anything is launched.  Every call on one GPU shares
+ * that GPU's buffer, so calls that overlap in time on one GPU (concurrent
+ * streams or host threads) race and must be serialised by the caller; the
+ * kernels initialise what they read, so no clearing is needed between calls.
+ * Arguments, outputs and the other errors as for tav2_nn_select.
+ */
+#define TAV2_SCRATCH_BYTES ((size_t)64 << 20)
+size_t tav2_scratch_bytes(void);
+tav2_status tav2_nn_select_noalloc(const tav2_seq* seq, const tav2_cands* cands, int32_t k,
+                                   int32_t* out_idx, float* out_score, void* stream);
 
 /*
  * Token assembly for the encoder (Eq. 2 restricted to NN(S_LL, c) and the kept

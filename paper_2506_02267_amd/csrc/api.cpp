@@ -1,5 +1,6 @@
 // C ABI of the NN-select + encode library: host-side argument validation,
 // workspace carving and kernel launches.  No allocation, no synchronisation.
+#include <mutex>
 #include <string.h>
 
 #include "common.h"
@@ -164,6 +165,7 @@ const char* tav2_status_string(tav2_status s) {
     case TAV2_ERR_UNSUPPORTED: return "valid request not implemented by this build";
     case TAV2_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case TAV2_ERR_HIP: return "HIP launch failed";
+    case TAV2_ERR_TOO_LARGE: return "request needs more scratch than the library's static buffer holds";
     default: return "unknown status";
   }
 }
@@ -308,6 +310,59 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt, const ta
   src.T = T;
   src.d = seq->d;
   return run_encode(src, cands->emb, cands->total, w, flags, out, enc_ws, s);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- no allocation
+// The NN search for callers that cannot allocate: its workspace is a file-scope
+// device array of TAV2_SCRATCH_BYTES (one per GPU, held until the process
+// ends).  Host code never passes the array's name to a kernel: each device's
+// address of it is looked up once (hipGetSymbolAddress, with that device
+// current) and kept.
+namespace {
+__device__ __align__(256) uint8_t scratch[TAV2_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[MAX_DEVICES] = {};
+
+// This device's address of `scratch`, or nullptr with *err set.
+void* device_scratch(hipError_t* err) {
+  int dev = 0;
+  *err = hipGetDevice(&dev);
+  if (*err != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= MAX_DEVICES) {
+    *err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    *err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (*err != hipSuccess) return nullptr;
+    g_scratch[dev] = p;
+  }
+  return g_scratch[dev];
+}
+}  // namespace
+
+extern "C" {
+
+size_t tav2_scratch_bytes(void) { return TAV2_SCRATCH_BYTES; }
+
+tav2_status tav2_nn_select_noalloc(const tav2_seq* seq, const tav2_cands* cands, int32_t k,
+                                   int32_t* out_idx, float* out_score, void* stream) {
+  tav2_status st;
+  if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
+  if (cands->total == 0) return TAV2_OK;
+  if (!out_idx || !out_score) return TAV2_ERR_NULL;
+  if (select_ws_bytes(seq, cands, k) > TAV2_SCRATCH_BYTES) return TAV2_ERR_TOO_LARGE;
+  hipError_t e = hipSuccess;
+  void* ws = device_scratch(&e);
+  if (!ws) return TAV2_ERR_HIP;
+  return hip_status(run_select(*seq, *cands, k, out_idx, out_score, nullptr, ws,
+                               static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

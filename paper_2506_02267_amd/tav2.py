@@ -21,7 +21,7 @@ F32, BF16, I8 = 0, 1, 2
 MASK_CAUSAL, MASK_NONE = 0, 1
 K_MAX, T_MAX = 1024, 1024
 STATUS = {0: "ok", -1: "null", -2: "shape", -3: "dtype", -4: "unsupported", -5: "workspace",
-          -6: "hip"}
+          -6: "hip", -7: "too_large"}
 
 
 class Seq(ctypes.Structure):
@@ -61,6 +61,9 @@ FUNCTIONS = {
     "tav2_nn_select_workspace": (c_size_t, [POINTER(Seq), POINTER(Cands), c_int32]),
     "tav2_nn_select": (c_int32, [POINTER(Seq), POINTER(Cands), c_int32, c_void_p, c_void_p,
                                  c_void_p, c_size_t, c_void_p]),
+    "tav2_scratch_bytes": (c_size_t, []),
+    "tav2_nn_select_noalloc": (c_int32, [POINTER(Seq), POINTER(Cands), c_int32, c_void_p,
+                                         c_void_p, c_void_p]),
     "tav2_gather": (c_int32, [POINTER(Seq), POINTER(Seq), POINTER(Cands), c_void_p, c_int32,
                               c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
     "tav2_encode_workspace": (c_size_t, [POINTER(Tokens), POINTER(Weights)]),
@@ -311,6 +314,18 @@ def nn_select(seq: DeviceSeq, cands: DeviceCands, k: int, out_idx=None, out_scor
                                                 _ptr(out_idx), _ptr(out_score), wp, wb,
                                                 _stream_handle(stream)))
     _used_on(stream, ws.buf, out_idx, out_score)
+    return out_idx, out_score
+
+
+def nn_select_noalloc(seq: DeviceSeq, cands: DeviceCands, k: int, out_idx: torch.Tensor,
+                      out_score: torch.Tensor, stream=None):
+    """tav2_nn_select_noalloc: the NN search with the library's static scratch
+    (the caller passes the outputs; nothing is allocated)."""
+    lib = load_library()
+    s, c = seq.struct(), cands.struct()
+    _check("tav2_nn_select_noalloc", lib.tav2_nn_select_noalloc(
+        ctypes.byref(s), ctypes.byref(c), k, _ptr(out_idx), _ptr(out_score),
+        _stream_handle(stream)))
     return out_idx, out_score
 
 
