@@ -149,3 +149,43 @@ def select_encode(inputs, W, k, only=None, chunk=32, causal=True):
     out = np.zeros((inputs.cand.shape[0], 2 * W.d_model), dtype=np.float64)
     out[ids] = out_ids
     return idx, score, out
+
+
+def select_encode_eq2(inputs, W, only=None, chunk=32, causal=True):
+    """The whole path with every source of Eq. 2: NN(S_LL, c) with k rows,
+    S_RT[:r], NN(S_RT[r:], c) with k_rt rows and NN(S_imp, c) with k_imp rows
+    (the workload's fields), token assembly, Eq. 4, encoder and head.
+
+    Returns idx [total, k + k_rt + k_imp] int32 (the three searches' rows in
+    rank order side by side: S_LL rows, then S_RT[r:] rows counted from S_RT[r],
+    then S_imp rows; -1 padded), score of the same shape (float32, -inf padded)
+    and out [total, 2 d_model] float64.
+    """
+    from .nn_select import nn_select_batch, eq2_tokens
+    w = inputs.w
+    k, r = w.k, w.r
+    k_rt = w.k_rt if inputs.rt is not None else 0
+    k_imp = w.k_imp if inputs.imp is not None else 0
+    total = inputs.cand.shape[0]
+    idx_ll, s_ll = nn_select_batch(inputs.seq, inputs.cand, inputs.cand_offset, k, only=only)
+    idx_rt = s_rt = idx_imp = s_imp = None
+    if k_rt > 0:
+        idx_rt, s_rt = nn_select_batch(inputs.rt, inputs.cand, inputs.cand_offset, k_rt,
+                                       only=only, skip=r)
+    if k_imp > 0:
+        idx_imp, s_imp = nn_select_batch(inputs.imp, inputs.cand, inputs.cand_offset, k_imp,
+                                         only=only)
+    creq = np.empty(total, dtype=np.int32)
+    for q in range(inputs.seq.R):
+        creq[inputs.cand_offset[q]:inputs.cand_offset[q + 1]] = q
+    ids = np.arange(total) if only is None else np.asarray(only, dtype=np.int64)
+    pick = lambda a: None if a is None else a[ids]
+    tok_emb, tok_act, tok_time, valid, _ = eq2_tokens(
+        inputs.seq, inputs.rt, inputs.imp, creq[ids], idx_ll[ids], r, pick(idx_rt),
+        pick(idx_imp), w.T)
+    out = np.zeros((total, 2 * W.d_model), dtype=np.float64)
+    out[ids] = encode(tok_emb, tok_act, tok_time, valid, inputs.cand[ids], W, chunk=chunk,
+                      causal=causal)
+    idx = np.concatenate([a for a in (idx_ll, idx_rt, idx_imp) if a is not None], axis=1)
+    score = np.concatenate([a for a in (s_ll, s_rt, s_imp) if a is not None], axis=1)
+    return idx, score, out

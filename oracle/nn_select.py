@@ -127,12 +127,14 @@ def nn_select_i8(Q: np.ndarray, C: np.ndarray, k: int) -> Tuple[np.ndarray, np.n
 
 
 def nn_select_batch(seq, cand: np.ndarray, cand_offset: np.ndarray, k: int,
-                    only: Optional[np.ndarray] = None):
+                    only: Optional[np.ndarray] = None, skip: int = 0):
     """nn_select over a de-duplicated batch: candidates of request r are
     cand[cand_offset[r]:cand_offset[r+1]] and see only request r's rows.
 
     `only`, if given, restricts the work to those candidate ids (sampling);
-    the rows of other candidates are left as padding.
+    the rows of other candidates are left as padding.  `skip` searches only the
+    rows from skip on of each request (Eq. 2's S_RT[r:]); the indices are then
+    relative to that row.
     """
     total = cand.shape[0]
     idx = np.full((total, k), -1, dtype=np.int32)
@@ -147,7 +149,7 @@ def nn_select_batch(seq, cand: np.ndarray, cand_offset: np.ndarray, k: int,
             ids = ids[want[a:b]]
         if ids.size == 0:
             continue
-        E = seq.emb[seq.rows(r)]
+        E = seq.emb[seq.rows(r)][skip:]
         i, s = (nn_select_i8 if E.dtype == np.int8 else nn_select)(E, cand[ids], k)
         idx[ids], score[ids] = i, s
     return idx, score
@@ -199,3 +201,51 @@ def gather_tokens(seq, rt, cand_request: np.ndarray, idx: np.ndarray, T: int):
             p += Lrt
         valid[n] = p
     return tok_emb, tok_act, tok_time, valid
+
+
+def eq2_tokens(seq, rt, imp, cand_request: np.ndarray, idx_ll: np.ndarray, r: int,
+               idx_rt: Optional[np.ndarray], idx_imp: Optional[np.ndarray], T: int):
+    """S_all of Eq. 2 for every candidate, in encoder order:
+
+        NN(S_LL, c) + S_RT[:r] + NN(S_RT[r:], c) + NN(S_imp, c)
+
+    idx_ll, idx_rt, idx_imp are the three searches' rows in rank order (best
+    first, -1 padded); idx_rt counts rows from S_RT[r]; None (or an absent
+    sequence) contributes nothing.  Each NN part enters in ascending score (as
+    Eq. 3's argsort returns it) and the kept real-time rows oldest first; the
+    valid tokens of all parts are packed from position 0.  Returns tok_emb
+    [total, T, d] float32, tok_act / tok_time [total, T] uint8, valid_len
+    [total] int32 and prov [total, T, 2] int32: the (source, row) of every
+    token, source 0 = S_LL, 1 = S_RT, 2 = S_imp (-1 for padding).
+    """
+    total = idx_ll.shape[0]
+    d = seq.emb.shape[1]
+    tok_emb = np.zeros((total, T, d), dtype=np.float32)
+    tok_act = np.zeros((total, T), dtype=np.uint8)
+    tok_time = np.zeros((total, T), dtype=np.uint8)
+    valid = np.zeros(total, dtype=np.int32)
+    prov = np.full((total, T, 2), -1, dtype=np.int32)
+    for n in range(total):
+        q = int(cand_request[n])
+        parts = [(0, seq, token_positions(idx_ll[n]))]
+        if rt is not None:
+            Lrt = int(rt.length[q])
+            keep = min(r, Lrt)
+            parts.append((1, rt, np.arange(keep - 1, -1, -1)))          # oldest first
+            if idx_rt is not None:
+                parts.append((1, rt, keep + token_positions(idx_rt[n])))  # S_RT[r:] rows
+        if imp is not None and idx_imp is not None:
+            parts.append((2, imp, token_positions(idx_imp[n])))
+        p = 0
+        for src_id, src, rows in parts:
+            m = rows.size
+            at = int(src.offset[q]) + rows
+            tok_emb[n, p:p + m] = src.emb[at]
+            tok_act[n, p:p + m] = src.act[at]
+            if src.time is not None:
+                tok_time[n, p:p + m] = src.time[at]
+            prov[n, p:p + m, 0] = src_id
+            prov[n, p:p + m, 1] = rows
+            p += m
+        valid[n] = p
+    return tok_emb, tok_act, tok_time, valid, prov

@@ -31,13 +31,26 @@ class Workload:
     d_ffn: int
     n_layers: int
     has_time: bool                # time-bucket feature present
-    rt_len: int = 0               # real-time actions appended after the NN tokens
+    rt_len: int = 0               # real-time actions per request
     tie_frac: float = 0.0         # fraction of rows overwritten with another row's embedding
+    # Eq. 2's other sources: rt_keep of the real-time rows kept as they are (-1: all
+    # of them), an NN top-k_rt over the rest, and an NN top-k_imp over an
+    # impression sequence of imp_len rows
+    rt_keep: int = -1
+    k_rt: int = 0
+    imp_len: int = 0
+    k_imp: int = 0
+
+    @property
+    def r(self) -> int:
+        """Real-time rows kept unconditionally (S_RT[:r] of Eq. 2)."""
+        return self.rt_len if self.rt_keep < 0 else self.rt_keep
 
     @property
     def T(self) -> int:
-        """Encoder positions: k NN tokens plus the real-time tail."""
-        return self.k + self.rt_len
+        """Encoder positions: the k NN tokens, the kept real-time rows and the NN
+        tokens of the real-time rest and of the impressions."""
+        return self.k + self.r + self.k_rt + self.k_imp
 
     @property
     def total_candidates(self) -> int:
@@ -72,7 +85,13 @@ WORKLOADS = {w.cid: w for w in (TINY, SINGLE, RAGGED, MIXED, STRESS)}
 SELECT_I8 = Workload(6, "select_i8", "i8", R=1, L=16384, L_range=None, d=32, N=1000, k=256,
                      d_model=256, n_heads=4, d_ffn=1024, n_layers=2, has_time=True,
                      tie_frac=0.01)
-BY_NAME = {w.name: w for w in list(WORKLOADS.values()) + [SELECT_I8]}
+# The whole of Eq. 2 (Sec. 3.2.2): NN(S_LL, c) + S_RT[:r] + NN(S_RT[r:], c) +
+# NN(S_imp, c), with real-time and impression sequences of O(10^2) actions; the
+# single workload's lifelong sequence, candidates and encoder.
+EQ2 = Workload(7, "eq2_bf16", "bf16", R=1, L=16384, L_range=None, d=256, N=1000, k=256,
+               d_model=256, n_heads=4, d_ffn=1024, n_layers=2, has_time=True, rt_len=200,
+               rt_keep=32, k_rt=32, imp_len=300, k_imp=64)
+BY_NAME = {w.name: w for w in list(WORKLOADS.values()) + [SELECT_I8, EQ2]}
 
 
 def scaled(w: Workload, **changes) -> Workload:

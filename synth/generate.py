@@ -88,6 +88,7 @@ class Inputs:
     cand: np.ndarray                # [total, d] float32
     cand_offset: np.ndarray         # [R+1] int64
     rt: Optional[SeqBatch] = None   # real-time sequence per request (mixed workload)
+    imp: Optional[SeqBatch] = None  # impression sequence per request (Eq. 2 workload)
 
     @property
     def total(self) -> int:
@@ -178,7 +179,10 @@ def make_inputs(w: Workload, seed: Optional[int] = None) -> Inputs:
     rt = None
     if w.rt_len > 0:
         rt = _draw_seq(rng, [w.rt_len] * w.R, w.d, w.has_time, 0.0)
-    return Inputs(w=w, seq=seq, cand=cand, cand_offset=cand_offset, rt=rt)
+    imp = None
+    if w.imp_len > 0:
+        imp = _draw_seq(rng, [w.imp_len] * w.R, w.d, w.has_time, 0.0)
+    return Inputs(w=w, seq=seq, cand=cand, cand_offset=cand_offset, rt=rt, imp=imp)
 
 
 def make_weights(w: Workload, seed: Optional[int] = None, scale: float = 0.02) -> Weights:
@@ -250,4 +254,4 @@ def subset_candidates(inp: Inputs, per_request: int) -> Inputs:
         offs.append(offs[-1] + sel.size)
     idx = np.concatenate(keep) if keep else np.zeros(0, dtype=np.int64)
     return Inputs(w=inp.w, seq=inp.seq, cand=inp.cand[idx].copy(),
-                  cand_offset=np.asarray(offs, dtype=np.int64), rt=inp.rt)
+                  cand_offset=np.asarray(offs, dtype=np.int64), rt=inp.rt, imp=inp.imp)

@@ -16,6 +16,7 @@ enc = sys.modules["oracle.encoder"]
 sel = sys.modules["oracle.nn_select"]
 
 import test_oracle_encoder as te  # noqa: E402
+import test_oracle_eq2 as t2  # noqa: E402
 import test_oracle_select as ts  # noqa: E402
 
 
@@ -139,3 +140,58 @@ def test_unmasked_mode_that_keeps_the_causal_mask_is_caught(monkeypatch):
     monkeypatch.setattr(enc, "attention", lambda q, k, v, causal=True: real(q, k, v, True))
     _fails(te.test_unmasked_layers_match_torch_transformer_encoder_layer, 2, 12)
     _fails(te.test_unmasked_encoder_is_permutation_equivariant_without_positions)
+
+
+def _eq2_mutant(kind):
+    """eq2_tokens with one plausible mistake in the order of Eq. 2's parts."""
+    real = sel.eq2_tokens
+
+    def tokens(seq, rt, imp, cand_request, idx_ll, r, idx_rt, idx_imp, T):
+        if kind == "imp_before_rt_rest":   # S_imp's part ahead of S_RT[r:]'s
+            out = real(seq, rt, None, cand_request, idx_ll, r, idx_rt, None, T)
+            if imp is None or idx_imp is None:
+                return out
+            emb, act, tim, valid, prov = real(seq, rt, imp, cand_request, idx_ll, r, None,
+                                              idx_imp, T)
+            e2, a2, t2_, v2, p2 = real(seq, rt, imp, cand_request, idx_ll, r, idx_rt, idx_imp, T)
+            for n in range(valid.shape[0]):
+                q = int(cand_request[n])
+                keep = min(r, int(rt.length[q])) if rt is not None else 0
+                start = int((prov[n, :, 0] == 0).sum()) + keep
+                rest = v2[n] - valid[n]                  # S_RT[r:] tokens
+                n_imp = valid[n] - start
+                order = list(range(start + rest, v2[n])) + list(range(start, start + rest))
+                for arr in (e2, a2, t2_, p2):
+                    arr[n, start:v2[n]] = arr[n, order]
+            return e2, a2, t2_, v2, p2
+        # "kept_newest_first": S_RT[:r] in stored order instead of oldest first
+        emb, act, tim, valid, prov = real(seq, rt, imp, cand_request, idx_ll, r, idx_rt, idx_imp, T)
+        for n in range(valid.shape[0]):
+            if rt is None:
+                break
+            q = int(cand_request[n])
+            keep = min(r, int(rt.length[q]))
+            start = int((prov[n, :, 0] == 0).sum())
+            for arr in (emb, act, tim, prov):
+                arr[n, start:start + keep] = arr[n, start:start + keep][::-1].copy()
+        return emb, act, tim, valid, prov
+    return tokens
+
+
+@pytest.mark.parametrize("kind", ["imp_before_rt_rest", "kept_newest_first"])
+def test_eq2_part_order_mistakes_are_caught(monkeypatch, kind):
+    bad = _eq2_mutant(kind)
+    monkeypatch.setattr(sel, "eq2_tokens", bad)
+    monkeypatch.setattr(oracle, "eq2_tokens", bad)
+    _fails(t2.test_hand_worked_example)
+
+
+def test_eq2_rest_search_over_all_rows_is_caught(monkeypatch):
+    real = sel.nn_select_batch
+
+    def no_skip(seq, cand, cand_offset, k, only=None, skip=0):
+        return real(seq, cand, cand_offset, k, only=only, skip=0)
+
+    monkeypatch.setattr(sel, "nn_select_batch", no_skip)
+    monkeypatch.setattr(oracle, "nn_select_batch", no_skip)
+    _fails(t2.test_hand_worked_example)
