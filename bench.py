@@ -187,6 +187,22 @@ def cpu_baseline(inp, W, k, budget_s):
                        f"scaled per candidate")}
 
 
+def cpu_baseline_eq2(inp, W, budget_s):
+    """The oracle's whole Eq. 2 path, untuned, over candidate chunks until
+    budget_s has passed."""
+    import oracle
+    n, t = 0, 0.0
+    while n < inp.total and (t < budget_s or n == 0):
+        ids = np.arange(n, min(inp.total, n + 8))
+        t0 = time.perf_counter()
+        oracle.select_encode_eq2(inp, W, only=ids)
+        t += time.perf_counter() - t0
+        n += ids.size
+    return {"value": n / t, "unit": "candidates/s", "cores": _threads(), "kind": "oracle",
+            "sample": (f"the three NN searches, token assembly and encoder of {n} of {inp.total} "
+                       f"candidates ({t:.2f} s), float64 numpy")}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -194,7 +210,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="single_bf16",
                     help="tiny_f32 | single_bf16 | ragged_bf16 | mixed_bf16 | stress_bf16 | "
-                         "select_i8 (the NN search alone over int8 codes)")
+                         "select_i8 (the NN search alone over int8 codes) | eq2_bf16 (all four "
+                         "parts of Eq. 2)")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -218,6 +235,7 @@ def main():
     w = synth.BY_NAME[args.workload]
     inp = synth.make_inputs(w)
     select_only = w.dtype == "i8"
+    eq2 = w.k_rt > 0 or w.k_imp > 0 or w.rt_keep >= 0
     W = None if select_only else synth.make_weights(w)
     dt = {"bf16": T.BF16, "i8": T.I8}.get(w.dtype, T.F32)
     seq = T.DeviceSeq.from_host(inp.seq, dt)
@@ -231,12 +249,23 @@ def main():
 
         def call():
             T.nn_select(seq, cands, w.k, out_idx, out_score, ws)
+    elif eq2:
+        imp = T.DeviceSeq.from_host(inp.imp, dt) if inp.imp is not None else None
+        call = T.SelectEncodeEq2(seq, rt, w.r, w.k_rt if rt is not None else 0, imp,
+                                 w.k_imp if imp is not None else 0, cands, w.k,
+                                 T.DeviceWeights(W))
     else:
         call = T.SelectEncode(seq, rt, cands, w.k, T.DeviceWeights(W))
     stream = torch.cuda.current_stream()
     total = inp.total
     lengths = inp.seq.length.astype(np.int64)
-    per_req_valid = np.minimum(w.k, lengths) + (w.rt_len if inp.rt is not None else 0)
+    per_req_valid = np.minimum(w.k, lengths)
+    if inp.rt is not None:
+        lrt = inp.rt.length.astype(np.int64)
+        keep = np.minimum(w.r, lrt)
+        per_req_valid = per_req_valid + keep + np.minimum(w.k_rt, lrt - keep)
+    if inp.imp is not None:
+        per_req_valid = per_req_valid + np.minimum(w.k_imp, inp.imp.length.astype(np.int64))
     counts = np.diff(inp.cand_offset)
     valid_tokens = int(np.sum(per_req_valid * counts))
 
@@ -296,6 +325,10 @@ def main():
 
     rows_total = int(lengths.sum())
     pairs = float(np.sum(lengths * counts))
+    if inp.rt is not None and w.k_rt > 0:   # the searches over S_RT[r:] and S_imp
+        pairs += float(np.sum(np.maximum(inp.rt.length.astype(np.int64) - w.r, 0) * counts))
+    if inp.imp is not None and w.k_imp > 0:
+        pairs += float(np.sum(inp.imp.length.astype(np.int64) * counts))
     work = site_work(w, total, valid_tokens, pairs, launches, rows_total, w.k)
     peak_flop = PEAK_BF16_TFLOPS if w.dtype in ("bf16", "i8") else PEAK_F32_TFLOPS
 
@@ -352,8 +385,12 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = (cpu_baseline_select(inp, w.k, args.cpu_budget) if select_only
-               else cpu_baseline(inp, W, w.k, args.cpu_budget))
+        if select_only:
+            cpu = cpu_baseline_select(inp, w.k, args.cpu_budget)
+        elif eq2:
+            cpu = cpu_baseline_eq2(inp, W, args.cpu_budget)
+        else:
+            cpu = cpu_baseline(inp, W, w.k, args.cpu_budget)
 
     config = {"workload": w.name, "requests": w.R, "L": w.L if w.L else list(w.L_range),
               "d": w.d, "candidates": total, "k": w.k}
@@ -362,6 +399,8 @@ def main():
     if not select_only:
         config.update({"rt_len": w.rt_len, "T": w.T, "d_model": w.d_model, "heads": w.n_heads,
                        "d_ffn": w.d_ffn, "layers": w.n_layers})
+    if eq2:
+        config.update({"r": w.r, "k_rt": w.k_rt, "imp_len": w.imp_len, "k_imp": w.k_imp})
     line = {"metric": METRIC_SELECT if select_only else METRIC, "value": round(value, 1),
             "unit": "candidates/s", "n_gpus": 1,
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),

@@ -282,6 +282,40 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt,
                                void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * The whole of Eq. 2 (Sec. 3.2.2): S_all = NN(S_LL, c) + S_RT[:r] +
+ * NN(S_RT[r:], c) + NN(S_imp, c).  Besides the lifelong search of `seq` (k rows,
+ * Eq. 3), the real-time sequence's most recent r rows are kept as they are, its
+ * remaining rows are searched for k_rt rows, and the impression sequence is
+ * searched for k_imp rows; the tokens of each search enter the encoder by
+ * ascending score, the kept real-time rows oldest first, all valid tokens
+ * packed from position 0.  Real-time and impression batches have the same
+ * requests, width, dtype and time feature as `seq` (requests may be shorter
+ * than r, k_rt or k_imp: their tokens are fewer).
+ *   out_idx, out_score: device [total, k + k_rt + k_imp]: the lifelong rows, the
+ *     real-time rest's rows (counted from S_RT[r]) and the impression rows, each
+ *     in rank order and padded as tav2_nn_select pads.
+ *   T = k + min(r, rt->max_len) + k_rt + k_imp positions; T <= w->max_pos.
+ * tav2_select_encode(seq, rt, ...) is the case r = rt->max_len, k_rt = k_imp = 0.
+ * Errors: those of tav2_select_encode; TAV2_ERR_NULL when a search or r > 0
+ * names a missing sequence.
+ */
+typedef struct tav2_eq2 {
+  const tav2_seq* rt;          /* real-time sequence S_RT (row 0 newest), or NULL */
+  int32_t r;                   /* rows of S_RT kept unconditionally, >= 0 */
+  int32_t k_rt;                /* NN top-k over S_RT[r:], 0..TAV2_K_MAX (0: no search) */
+  const tav2_seq* imp;         /* impression sequence S_imp, or NULL */
+  int32_t k_imp;               /* NN top-k over S_imp, 0..TAV2_K_MAX (0: no search) */
+  int32_t reserved;            /* set to 0 */
+} tav2_eq2;
+size_t tav2_select_encode_eq2_workspace(const tav2_seq* seq, const tav2_eq2* eq2,
+                                        const tav2_cands* cands, int32_t k,
+                                        const tav2_weights* w);
+tav2_status tav2_select_encode_eq2(const tav2_seq* seq, const tav2_eq2* eq2,
+                                   const tav2_cands* cands, int32_t k, const tav2_weights* w,
+                                   uint32_t flags, int32_t* out_idx, float* out_score, float* out,
+                                   void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Measurement hook for benchmarks and profilers (not needed for serving).
  * tav2_profile_enable(1, site) makes every later kernel launch of the library
  * whose site name equals `site` (NULL: every site) record a HIP event before
@@ -289,7 +323,7 @@ tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt,
  * After the caller has synchronised, tav2_profile_report() writes one line
  * "<site> <launches> <total_ms>" per site into buf (NUL-terminated, truncated
  * to buf_bytes), forgets the recorded launches and returns the untruncated
- * text length.  Site names: nn_sample, nn_threshold, nn_filter, nn_select,
+ * text length.  Site names: seq_view, nn_sample, nn_threshold, nn_filter, nn_select,
  * nn_fallback (the NN search with on-chip scores, for bf16 and int8 sequences of
  * more than 4096 rows), score_bf16, score_i8, score_f32, topk (the NN search over
  * materialised score rows), gather, pack_weights, cand_proj, encoder_fused (the

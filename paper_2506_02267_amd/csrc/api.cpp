@@ -1,5 +1,6 @@
 // C ABI of the NN-select + encode library: host-side argument validation,
 // workspace carving and kernel launches.  No allocation, no synchronisation.
+#include <algorithm>
 #include <mutex>
 #include <string.h>
 
@@ -127,14 +128,16 @@ size_t select_ws_bytes(const tav2_seq* s, const tav2_cands* c, int k) {
   return align_up(size_t(c->total) * size_t(score_ld(s->max_len)) * 4, WS_ALIGN);
 }
 
+// NN search writing rows of out_ld elements (the k results first).
 hipError_t run_select(const tav2_seq& s, const tav2_cands& c, int k, int32_t* out_idx,
-                      float* out_score, int32_t* cand_req, void* ws, hipStream_t st) {
+                      float* out_score, int out_ld, int32_t* cand_req, void* ws, hipStream_t st) {
   if (select_fused_applies(s))
-    return launch_select_fused(s, c, k, out_idx, out_score, cand_req, ws, st);
+    return launch_select_fused(s, c, k, out_idx, out_score, out_ld, cand_req, ws, st);
   float* scores = static_cast<float*>(ws);
   const int64_t ld = score_ld(s.max_len);
   hipError_t e = launch_scores(s, c, scores, ld, st);
-  if (e == hipSuccess) e = launch_topk(s, c, scores, ld, k, out_idx, out_score, cand_req, st);
+  if (e == hipSuccess)
+    e = launch_topk(s, c, scores, ld, k, out_idx, out_score, out_ld, cand_req, st);
   return e;
 }
 
@@ -150,6 +153,158 @@ tav2_status run_encode(const TokenSource& src, const void* cand_emb, int64_t tot
   if (w->dtype == TAV2_BF16)
     return hip_status(launch_encode_fused(src, cand_emb, total, *w, out, ws, unmasked, st));
   return hip_status(launch_encode_f32(src, cand_emb, total, *w, out, unmasked, st));
+}
+
+// Eq. 2's sources besides the lifelong sequence: the real-time rows kept
+// (S_RT[:r]) and searched (NN(S_RT[r:], c), k_rt rows), the impressions
+// searched (k_imp rows).
+struct Sources {
+  const tav2_seq* rt;
+  int r, k_rt;
+  const tav2_seq* imp;
+  int k_imp;
+};
+Sources keep_all(const tav2_seq* rt) { return Sources{rt, rt ? rt->max_len : 0, 0, nullptr, 0}; }
+Sources sources_of(const tav2_eq2& e) { return Sources{e.rt, e.r, e.k_rt, e.imp, e.k_imp}; }
+
+// Encoder positions: the searched rows, the kept real-time rows (at most the
+// longest real-time request) and the other searches' rows.
+int positions(const Sources& src, int k) {
+  const int keep = src.rt ? (src.r < src.rt->max_len ? src.r : src.rt->max_len) : 0;
+  return k + keep + src.k_rt + src.k_imp;
+}
+
+// A sequence that must look like the lifelong one (requests, width, dtype, time
+// feature); `search`: an NN search runs over it.
+tav2_status check_source(const tav2_seq* x, const tav2_seq* seq, bool search) {
+  tav2_status st;
+  if ((st = check_rt(x, seq))) return st;
+  if (search && x->max_len > SEL_MAX_LEN) return TAV2_ERR_UNSUPPORTED;
+  return TAV2_OK;
+}
+
+tav2_status check_select_encode(const tav2_seq* seq, const Sources& src, const tav2_cands* cands,
+                                int k, const tav2_weights* w, uint32_t flags, int* T_out) {
+  tav2_status st;
+  if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
+  if (seq->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;
+  if (src.r < 0 || src.k_rt < 0 || src.k_imp < 0) return TAV2_ERR_SHAPE;
+  if (src.k_rt > TAV2_K_MAX || src.k_imp > TAV2_K_MAX) return TAV2_ERR_SHAPE;
+  if ((src.k_rt > 0 || src.r > 0) && !src.rt) return TAV2_ERR_NULL;
+  if (src.k_imp > 0 && !src.imp) return TAV2_ERR_NULL;
+  if (src.rt && (st = check_source(src.rt, seq, src.k_rt > 0))) return st;
+  if (src.imp && (st = check_source(src.imp, seq, true))) return st;
+  const int64_t T = int64_t(k) + (src.rt ? std::min(src.r, src.rt->max_len) : 0) + src.k_rt +
+                    src.k_imp;
+  if (T > TAV2_T_MAX) return TAV2_ERR_SHAPE;
+  if ((st = check_weights(w, seq->d, seq->dtype, int(T), seq->time_bucket != nullptr))) return st;
+  if ((st = check_flags(flags, seq->dtype, int(T)))) return st;
+  *T_out = int(T);
+  return TAV2_OK;
+}
+
+// The S_RT[r:] view of the real-time batch (offsets and lengths in the workspace).
+tav2_seq rest_view(const tav2_seq& rt, int r, int64_t* off, int32_t* len) {
+  tav2_seq v = rt;
+  v.offset = off;
+  v.len = len;
+  v.max_len = rt.max_len > r ? rt.max_len - r : 0;
+  return v;
+}
+
+// Workspace: one NN-search region reused by the searches in turn, the S_RT[r:]
+// view, each candidate's request, the encoder's part.
+struct SeLayout {
+  size_t sel, view_off, view_len, req, enc, total;
+};
+SeLayout select_encode_layout(const tav2_seq* seq, const Sources& src, const tav2_cands* cands,
+                              int k, const tav2_weights* w, int T) {
+  size_t sel = select_ws_bytes(seq, cands, k);
+  const size_t R = size_t(seq->num_requests);
+  if (src.k_rt > 0) {
+    const tav2_seq v = rest_view(*src.rt, src.r, nullptr, nullptr);
+    sel = std::max(sel, select_ws_bytes(&v, cands, src.k_rt));
+  }
+  if (src.k_imp > 0) sel = std::max(sel, select_ws_bytes(src.imp, cands, src.k_imp));
+  SeLayout l{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align_up(bytes, WS_ALIGN);
+    return at;
+  };
+  l.sel = take(sel);
+  l.view_off = take(src.k_rt > 0 ? R * 8 : 0);
+  l.view_len = take(src.k_rt > 0 ? R * 4 : 0);
+  l.req = take(size_t(cands->total) * 4);
+  l.enc = take(encode_ws_bytes(cands->total, T, w));
+  l.total = off;
+  return l;
+}
+
+tav2_status select_encode(const tav2_seq* seq, const Sources& src, const tav2_cands* cands,
+                          int32_t k, const tav2_weights* w, uint32_t flags, int32_t* out_idx,
+                          float* out_score, float* out, void* ws, size_t ws_bytes,
+                          hipStream_t s) {
+  tav2_status st;
+  int T = 0;
+  if ((st = check_select_encode(seq, src, cands, k, w, flags, &T))) return st;
+  if (cands->total == 0) return TAV2_OK;
+  if (!out_idx || !out_score || !out) return TAV2_ERR_NULL;
+  if (!aligned(out, 16)) return TAV2_ERR_SHAPE;
+  const SeLayout lay = select_encode_layout(seq, src, cands, k, w, T);
+  if ((st = check_ws(ws, ws_bytes, lay.total))) return st;
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  int32_t* cand_req = reinterpret_cast<int32_t*>(base + lay.req);
+  const int ld = k + src.k_rt + src.k_imp;   // the searches' results side by side
+  // the searches, one after the other in the same workspace region
+  if (run_select(*seq, *cands, k, out_idx, out_score, ld, cand_req, base + lay.sel, s))
+    return TAV2_ERR_HIP;
+  if (src.k_rt > 0) {
+    int64_t* voff = reinterpret_cast<int64_t*>(base + lay.view_off);
+    int32_t* vlen = reinterpret_cast<int32_t*>(base + lay.view_len);
+    if (launch_seq_view(*src.rt, src.r, voff, vlen, s)) return TAV2_ERR_HIP;
+    const tav2_seq v = rest_view(*src.rt, src.r, voff, vlen);
+    if (run_select(v, *cands, src.k_rt, out_idx + k, out_score + k, ld, nullptr, base + lay.sel, s))
+      return TAV2_ERR_HIP;
+  }
+  if (src.k_imp > 0 &&
+      run_select(*src.imp, *cands, src.k_imp, out_idx + k + src.k_rt, out_score + k + src.k_rt,
+                 ld, nullptr, base + lay.sel, s))
+    return TAV2_ERR_HIP;
+  TokenSource ts{};
+  ts.explicit_tokens = false;
+  ts.seq_emb = seq->emb;
+  ts.seq_act = seq->action_type;
+  ts.seq_time = seq->time_bucket;
+  ts.seq_off = seq->offset;
+  ts.seq_len = seq->len;
+  ts.idx = out_idx;
+  ts.k = k;
+  ts.idx_ld = ld;
+  if (src.rt) {
+    ts.rt_emb = src.rt->emb;
+    ts.rt_act = src.rt->action_type;
+    ts.rt_time = src.rt->time_bucket;
+    ts.rt_off = src.rt->offset;
+    ts.rt_len = src.rt->len;
+    ts.rt_keep = src.r;
+    ts.idx_rt = out_idx + k;
+    ts.k_rt = src.k_rt;
+  }
+  if (src.k_imp > 0) {
+    ts.imp_emb = src.imp->emb;
+    ts.imp_act = src.imp->action_type;
+    ts.imp_time = src.imp->time_bucket;
+    ts.imp_off = src.imp->offset;
+    ts.imp_len = src.imp->len;
+    ts.idx_imp = out_idx + k + src.k_rt;
+    ts.k_imp = src.k_imp;
+  }
+  ts.cand_req = cand_req;
+  ts.T = T;
+  ts.d = seq->d;
+  return run_encode(ts, cands->emb, cands->total, w, flags, out, base + lay.enc, s);
 }
 
 }  // namespace
@@ -187,7 +342,7 @@ tav2_status tav2_nn_select(const tav2_seq* seq, const tav2_cands* cands, int32_t
   if (cands->total == 0) return TAV2_OK;
   if (!out_idx || !out_score) return TAV2_ERR_NULL;
   if ((st = check_ws(ws, ws_bytes, select_ws_bytes(seq, cands, k)))) return st;
-  return hip_status(run_select(*seq, *cands, k, out_idx, out_score, nullptr, ws,
+  return hip_status(run_select(*seq, *cands, k, out_idx, out_score, k, nullptr, ws,
                                static_cast<hipStream_t>(stream)));
 }
 
@@ -259,57 +414,37 @@ tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2
 
 size_t tav2_select_encode_workspace(const tav2_seq* seq, const tav2_seq* rt,
                                     const tav2_cands* cands, int32_t k, const tav2_weights* w) {
-  if (check_seq(seq, true) || check_cands(cands, seq) || check_k(k) || check_rt(rt, seq)) return 0;
-  const int T = k + rt_len_max(rt);
-  if (check_weights(w, seq->d, seq->dtype, T, seq->time_bucket != nullptr)) return 0;
-  return select_ws_bytes(seq, cands, k) + align_up(size_t(cands->total) * 4, WS_ALIGN) +
-         encode_ws_bytes(cands->total, T, w);
+  const Sources src = keep_all(rt);
+  int T = 0;
+  if (check_select_encode(seq, src, cands, k, w, TAV2_MASK_CAUSAL, &T)) return 0;
+  return select_encode_layout(seq, src, cands, k, w, T).total;
 }
 
 tav2_status tav2_select_encode(const tav2_seq* seq, const tav2_seq* rt, const tav2_cands* cands,
                                int32_t k, const tav2_weights* w, uint32_t flags,
                                int32_t* out_idx, float* out_score, float* out, void* ws,
                                size_t ws_bytes, void* stream) {
-  tav2_status st;
-  if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
-  if (seq->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;
-  if ((st = check_rt(rt, seq))) return st;
-  const int T = k + rt_len_max(rt);
-  if ((st = check_weights(w, seq->d, seq->dtype, T, seq->time_bucket != nullptr))) return st;
-  if ((st = check_flags(flags, seq->dtype, T))) return st;
-  if (cands->total == 0) return TAV2_OK;
-  if (!out_idx || !out_score || !out) return TAV2_ERR_NULL;
-  if (!aligned(out, 16)) return TAV2_ERR_SHAPE;
-  const size_t sel_b = select_ws_bytes(seq, cands, k);
-  const size_t req_b = align_up(size_t(cands->total) * 4, WS_ALIGN);
-  const size_t enc_b = encode_ws_bytes(cands->total, T, w);
-  if ((st = check_ws(ws, ws_bytes, sel_b + req_b + enc_b))) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  uint8_t* base = static_cast<uint8_t*>(ws);
-  int32_t* cand_req = reinterpret_cast<int32_t*>(base + sel_b);
-  void* enc_ws = base + sel_b + req_b;
-  if (run_select(*seq, *cands, k, out_idx, out_score, cand_req, base, s) != hipSuccess)
-    return TAV2_ERR_HIP;
-  TokenSource src{};
-  src.explicit_tokens = false;
-  src.seq_emb = seq->emb;
-  src.seq_act = seq->action_type;
-  src.seq_time = seq->time_bucket;
-  src.seq_off = seq->offset;
-  src.seq_len = seq->len;
-  if (rt) {
-    src.rt_emb = rt->emb;
-    src.rt_act = rt->action_type;
-    src.rt_time = rt->time_bucket;
-    src.rt_off = rt->offset;
-    src.rt_len = rt->len;
-  }
-  src.idx = out_idx;
-  src.cand_req = cand_req;
-  src.k = k;
-  src.T = T;
-  src.d = seq->d;
-  return run_encode(src, cands->emb, cands->total, w, flags, out, enc_ws, s);
+  return select_encode(seq, keep_all(rt), cands, k, w, flags, out_idx, out_score, out, ws,
+                       ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+size_t tav2_select_encode_eq2_workspace(const tav2_seq* seq, const tav2_eq2* eq2,
+                                        const tav2_cands* cands, int32_t k,
+                                        const tav2_weights* w) {
+  if (!eq2) return 0;
+  const Sources src = sources_of(*eq2);
+  int T = 0;
+  if (check_select_encode(seq, src, cands, k, w, TAV2_MASK_CAUSAL, &T)) return 0;
+  return select_encode_layout(seq, src, cands, k, w, T).total;
+}
+
+tav2_status tav2_select_encode_eq2(const tav2_seq* seq, const tav2_eq2* eq2,
+                                   const tav2_cands* cands, int32_t k, const tav2_weights* w,
+                                   uint32_t flags, int32_t* out_idx, float* out_score, float* out,
+                                   void* ws, size_t ws_bytes, void* stream) {
+  if (!eq2) return TAV2_ERR_NULL;
+  return select_encode(seq, sources_of(*eq2), cands, k, w, flags, out_idx, out_score, out, ws,
+                       ws_bytes, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"
@@ -361,7 +496,7 @@ tav2_status tav2_nn_select_noalloc(const tav2_seq* seq, const tav2_cands* cands,
   hipError_t e = hipSuccess;
   void* ws = device_scratch(&e);
   if (!ws) return TAV2_ERR_HIP;
-  return hip_status(run_select(*seq, *cands, k, out_idx, out_score, nullptr, ws,
+  return hip_status(run_select(*seq, *cands, k, out_idx, out_score, k, nullptr, ws,
                                static_cast<hipStream_t>(stream)));
 }
 

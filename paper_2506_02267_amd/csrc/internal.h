@@ -31,8 +31,9 @@ int64_t score_ld(int32_t max_len);
 hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores, int64_t ld,
                          hipStream_t st);
 // cand_req (nullable): also receives each candidate's request index.
+// out_ld: row stride (elements) of out_idx and out_score (>= k).
 hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* scores, int64_t ld,
-                       int k, int32_t* out_idx, float* out_score, int32_t* cand_req,
+                       int k, int32_t* out_idx, float* out_score, int out_ld, int32_t* cand_req,
                        hipStream_t st);
 
 // ---- select_fused.hip: NN search with the scores kept on chip (bf16 and int8
@@ -40,38 +41,59 @@ hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* sc
 constexpr int FUSED_MIN_LEN = 4096;
 bool select_fused_applies(const tav2_seq& seq);
 size_t select_fused_workspace(const tav2_cands& c, int k);
-// cand_req (nullable): also receives each candidate's request index.
+// cand_req (nullable): also receives each candidate's request index; out_ld: row
+// stride of the outputs.
 hipError_t launch_select_fused(const tav2_seq& seq, const tav2_cands& c, int k,
-                               int32_t* out_idx, float* out_score, int32_t* cand_req, void* ws,
-                               hipStream_t st);
+                               int32_t* out_idx, float* out_score, int out_ld, int32_t* cand_req,
+                               void* ws, hipStream_t st);
 
 // ---- gather.hip
 // Where encoder tokens come from: either explicit token tensors, or the
-// selection (idx) into the request sequence plus an optional real-time tail.
+// selections into the request-level sources of Eq. 2: NN(S_LL, c), the kept
+// real-time rows S_RT[:r], NN(S_RT[r:], c) and NN(S_imp, c).
 struct TokenSource {
   // explicit tokens [total, T, ...]
   const void* tok_emb;
   const uint8_t* tok_act;
   const uint8_t* tok_time;
   const int32_t* valid_len;
-  // selection path
+  // selection path: the lifelong sequence and its top-k rows
   const void* seq_emb;
   const uint8_t* seq_act;
   const uint8_t* seq_time;
   const int64_t* seq_off;
   const int32_t* seq_len;
+  const int32_t* idx;        // [total, idx_ld]: rank order, -1 padded
+  int k;
+  int idx_ld;
+  // real-time sequence (rt_len == nullptr: none): rows [0, rt_keep) kept, and
+  // the top-k_rt of the rest (idx_rt counts rows from rt_keep; k_rt = 0: none)
   const void* rt_emb;
   const uint8_t* rt_act;
   const uint8_t* rt_time;
   const int64_t* rt_off;
   const int32_t* rt_len;
-  const int32_t* idx;        // [total, k]
+  int rt_keep;
+  const int32_t* idx_rt;     // [total, idx_ld]
+  int k_rt;
+  // impression sequence (imp_len == nullptr: none) and its top-k_imp rows
+  const void* imp_emb;
+  const uint8_t* imp_act;
+  const uint8_t* imp_time;
+  const int64_t* imp_off;
+  const int32_t* imp_len;
+  const int32_t* idx_imp;    // [total, idx_ld]
+  int k_imp;
   const int32_t* cand_req;   // [total] request of each candidate
-  int k;
   int T;
   int d;
   bool explicit_tokens;
 };
+
+// The view S_RT[r:] of a sequence batch: off_out[q] = off[q] + min(r, len[q]),
+// len_out[q] = max(len[q] - r, 0) (device arrays of num_requests entries).
+hipError_t launch_seq_view(const tav2_seq& s, int r, int64_t* off_out, int32_t* len_out,
+                           hipStream_t st);
 
 hipError_t launch_gather(const tav2_seq& seq, const tav2_seq* rt, const tav2_cands& c,
                          const int32_t* idx, int k, int T, void* tok_emb, uint8_t* tok_act,

@@ -269,7 +269,7 @@ template <int PT>
 __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     const float* __restrict__ scores, int64_t ld, const int64_t* __restrict__ cand_off,
     const int32_t* __restrict__ seq_len, int max_len, int k, int32_t* __restrict__ out_idx,
-    float* __restrict__ out_score, int32_t* __restrict__ cand_req) {
+    float* __restrict__ out_score, int out_ld, int32_t* __restrict__ cand_req) {
   __shared__ int red[2][TK_THREADS / WAVE];
   __shared__ uint64_t scan_w[(TK_THREADS / WAVE) * 5];
   __shared__ uint64_t sel[TAV2_K_MAX];
@@ -281,8 +281,8 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
   const int L = min(seq_len[r], max_len);
   const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
   const int kk = k < L ? k : L;
-  int32_t* oi = out_idx + n * k;
-  float* os = out_score + n * k;
+  int32_t* oi = out_idx + n * out_ld;
+  float* os = out_score + n * out_ld;
   for (int p = kk + tid; p < k; p += TK_THREADS) {
     oi[p] = -1;
     os[p] = -__builtin_inff();
@@ -442,7 +442,7 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 __global__ __launch_bounds__(TS_THREADS) void topk_stream_kernel(
     const float* __restrict__ scores, int64_t ld, const int64_t* __restrict__ cand_off,
     const int32_t* __restrict__ seq_len, int max_len, int k, int32_t* __restrict__ out_idx,
-    float* __restrict__ out_score, int32_t* __restrict__ cand_req) {
+    float* __restrict__ out_score, int out_ld, int32_t* __restrict__ cand_req) {
   __shared__ int red[2][TS_NW];
   __shared__ uint64_t scan_w[TS_NW];
   __shared__ uint64_t sel[TAV2_K_MAX];
@@ -457,8 +457,8 @@ __global__ __launch_bounds__(TS_THREADS) void topk_stream_kernel(
   const int L = min(seq_len[r], max_len);
   const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
   const int kk = k < L ? k : L;
-  int32_t* oi = out_idx + n * k;
-  float* os = out_score + n * k;
+  int32_t* oi = out_idx + n * out_ld;
+  float* os = out_score + n * out_ld;
   for (int p = kk + tid; p < k; p += TS_THREADS) {
     oi[p] = -1;
     os[p] = -__builtin_inff();
@@ -728,7 +728,7 @@ hipError_t launch_scores(const tav2_seq& seq, const tav2_cands& c, float* scores
 }
 
 hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* scores, int64_t ld,
-                       int k, int32_t* out_idx, float* out_score, int32_t* cand_req,
+                       int k, int32_t* out_idx, float* out_score, int out_ld, int32_t* cand_req,
                        hipStream_t st) {
   if (seq.num_requests == 0 || c.total == 0) return hipSuccess;
   dim3 grid(unsigned(c.max_count), unsigned(seq.num_requests));
@@ -736,12 +736,12 @@ hipError_t launch_topk(const tav2_seq& seq, const tav2_cands& c, const float* sc
   ProfScope prof("topk", st);
 #define TAV2_TOPK(PT) \
   topk_kernel<PT><<<grid, TK_THREADS, 0, st>>>(scores, ld, c.offset, seq.len, seq.max_len, k, \
-                                               out_idx, out_score, cand_req)
+                                               out_idx, out_score, out_ld, cand_req)
   if (per <= 4) TAV2_TOPK(4);
   else if (per <= 8) TAV2_TOPK(8);
   else
     topk_stream_kernel<<<grid, TS_THREADS, 0, st>>>(scores, ld, c.offset, seq.len, seq.max_len, k,
-                                                     out_idx, out_score, cand_req);
+                                                     out_idx, out_score, out_ld, cand_req);
 #undef TAV2_TOPK
   return hipGetLastError();
 }

@@ -75,6 +75,7 @@ struct FusedArgs {
   const bf16_t* cand;          // [total, d]
   const int64_t* cand_off;     // [R + 1]
   int d, max_len, k, cap;
+  int out_ld;                  // row stride of the outputs (>= k)
   uint16_t* samp;              // [total][FS_NS] top 16 bits of the sampled keys
   uint32_t* thr;               // [total] threshold key
   uint32_t* cnt;               // [total] survivors appended (may exceed cap)
@@ -579,8 +580,8 @@ __global__ __launch_bounds__(FT_THREADS) void fsel_select(FusedArgs A, int32_t* 
   const int L = min(A.seq_len[r], A.max_len);
   const int k = A.k;
   const int kk = k < L ? k : L;
-  int32_t* oi = out_idx + n * k;
-  float* os = out_score + n * k;
+  int32_t* oi = out_idx + n * A.out_ld;
+  float* os = out_score + n * A.out_ld;
   for (int p = kk + tid; p < k; p += FT_THREADS) {
     oi[p] = -1;
     os[p] = -__builtin_inff();
@@ -730,7 +731,7 @@ __global__ __launch_bounds__(FF_THREADS) void fsel_fallback(FusedArgs A, int32_t
       eq_before += all;
     }
     __syncthreads();
-    place_by_rank<FF_THREADS>(sel, kk, out_idx + n * A.k, out_score + n * A.k);
+    place_by_rank<FF_THREADS>(sel, kk, out_idx + n * A.out_ld, out_score + n * A.out_ld);
     __syncthreads();   // keys and sel are rewritten by the next queued candidate
   }
 }
@@ -783,8 +784,8 @@ size_t select_fused_workspace(const tav2_cands& c, int k) {
 }
 
 hipError_t launch_select_fused(const tav2_seq& seq, const tav2_cands& c, int k,
-                               int32_t* out_idx, float* out_score, int32_t* cand_req, void* ws,
-                               hipStream_t st) {
+                               int32_t* out_idx, float* out_score, int out_ld, int32_t* cand_req,
+                               void* ws, hipStream_t st) {
   if (seq.num_requests == 0 || c.total == 0) return hipSuccess;
   const FusedLayout lay = fused_layout(c.total, k);
   uint8_t* base = static_cast<uint8_t*>(ws);
@@ -798,6 +799,7 @@ hipError_t launch_select_fused(const tav2_seq& seq, const tav2_cands& c, int k,
   A.max_len = seq.max_len;
   A.k = k;
   A.cap = int(fused_cap(k));
+  A.out_ld = out_ld;
   A.samp = reinterpret_cast<uint16_t*>(base + lay.samp);
   A.thr = reinterpret_cast<uint32_t*>(base + lay.thr);
   A.cnt = reinterpret_cast<uint32_t*>(base + lay.cnt);

@@ -1,24 +1,17 @@
 // Where encoder position p of candidate n reads its action row from (shared by
-// the standalone gather and the encoder's fused gather).
+// the standalone gather and the encoders' fused gathers).
+//
+// The token set is Eq. 2's S_all = NN(S_LL, c) + S_RT[:r] + NN(S_RT[r:], c) +
+// NN(S_imp, c): each NN part by ascending score (rank t - 1 - q at its q-th
+// position, as Eq. 3's ascending argsort returns it, best match last), the kept
+// real-time rows oldest first; the valid tokens of all parts are packed from
+// position 0 and later positions are padding.
 #pragma once
 
 #include "common.h"
 #include "internal.h"
 
 namespace tav2 {
-
-// Selected rows in ascending score order (rank t_ll-1-p at position p), then the
-// real-time tail oldest first.  Returns a sequence row (>= 0), a real-time row
-// encoded as -2 - row, or -1 for padding.
-__device__ __forceinline__ int64_t token_row(int p, int t_ll, int lrt, const int32_t* idx_n,
-                                             int L, int64_t seq_base, int64_t rt_base) {
-  if (p < t_ll) {
-    const int i = idx_n[t_ll - 1 - p];
-    return (i >= 0 && i < L) ? seq_base + i : -1;
-  }
-  if (p < t_ll + lrt) return -2 - (rt_base + (lrt - 1 - (p - t_ll)));
-  return -1;
-}
 
 struct TokenRef {
   const uint8_t* emb;   // row start (bytes), nullptr for padding
@@ -29,34 +22,76 @@ struct TokenRef {
 __device__ __forceinline__ int clamp_act(int a) { return a < 8 ? a : 7; }
 __device__ __forceinline__ int clamp_time(int t) { return t < 64 ? t : 63; }
 
+__device__ __forceinline__ TokenRef source_row(const void* emb, const uint8_t* act,
+                                               const uint8_t* time, int64_t row, int row_bytes) {
+  TokenRef t;
+  t.emb = static_cast<const uint8_t*>(emb) + row * row_bytes;
+  t.act = clamp_act(act[row]);
+  t.time = time ? clamp_time(time[row]) : 0;
+  return t;
+}
+
+// Valid tokens of each part for candidate n of request r.
+struct TokenParts {
+  int t_ll, keep, t_rt, t_imp;
+};
+__device__ __forceinline__ TokenParts token_parts(const TokenSource& s, int r) {
+  TokenParts q{0, 0, 0, 0};
+  const int L = s.seq_len[r];
+  q.t_ll = s.k < L ? s.k : L;
+  if (s.rt_len) {
+    const int lrt = s.rt_len[r];
+    q.keep = s.rt_keep < lrt ? s.rt_keep : lrt;
+    const int rest = lrt - q.keep;
+    q.t_rt = s.k_rt < rest ? s.k_rt : rest;
+  }
+  if (s.imp_len) {
+    const int li = s.imp_len[r];
+    q.t_imp = s.k_imp < li ? s.k_imp : li;
+  }
+  return q;
+}
+
+// Position p of candidate n of request r, selection path.
+__device__ __forceinline__ TokenRef selected_token(const TokenSource& s, int64_t n, int r, int p,
+                                                   int row_bytes) {
+  TokenRef t{nullptr, 0, 0};
+  const TokenParts q = token_parts(s, r);
+  if (p < q.t_ll) {
+    const int i = s.idx[n * s.idx_ld + q.t_ll - 1 - p];
+    if (i >= 0 && i < s.seq_len[r])
+      t = source_row(s.seq_emb, s.seq_act, s.seq_time, s.seq_off[r] + i, row_bytes);
+    return t;
+  }
+  p -= q.t_ll;
+  if (p < q.keep)
+    return source_row(s.rt_emb, s.rt_act, s.rt_time, s.rt_off[r] + (q.keep - 1 - p), row_bytes);
+  p -= q.keep;
+  if (p < q.t_rt) {
+    const int i = s.idx_rt[n * s.idx_ld + q.t_rt - 1 - p];
+    if (i >= 0 && q.keep + i < s.rt_len[r])
+      t = source_row(s.rt_emb, s.rt_act, s.rt_time, s.rt_off[r] + q.keep + i, row_bytes);
+    return t;
+  }
+  p -= q.t_rt;
+  if (p < q.t_imp) {
+    const int i = s.idx_imp[n * s.idx_ld + q.t_imp - 1 - p];
+    if (i >= 0 && i < s.imp_len[r])
+      t = source_row(s.imp_emb, s.imp_act, s.imp_time, s.imp_off[r] + i, row_bytes);
+  }
+  return t;
+}
+
 // Resolve (candidate n, position p) for either source kind; `row_bytes` = d * sizeof(elem).
 __device__ __forceinline__ TokenRef resolve_token(const TokenSource& s, int64_t n, int p,
                                                   int row_bytes) {
+  if (!s.explicit_tokens) return selected_token(s, n, s.cand_req[n], p, row_bytes);
   TokenRef t{nullptr, 0, 0};
-  if (s.explicit_tokens) {
-    if (p < s.valid_len[n]) {
-      const int64_t m = n * s.T + p;
-      t.emb = static_cast<const uint8_t*>(s.tok_emb) + m * row_bytes;
-      t.act = clamp_act(s.tok_act[m]);
-      t.time = s.tok_time ? clamp_time(s.tok_time[m]) : 0;
-    }
-    return t;
-  }
-  const int r = s.cand_req[n];
-  const int L = s.seq_len[r];
-  const int t_ll = s.k < L ? s.k : L;
-  const int lrt = s.rt_len ? s.rt_len[r] : 0;
-  const int64_t row = token_row(p, t_ll, lrt, s.idx + n * s.k, L, s.seq_off[r],
-                                s.rt_len ? s.rt_off[r] : 0);
-  if (row >= 0) {
-    t.emb = static_cast<const uint8_t*>(s.seq_emb) + row * row_bytes;
-    t.act = clamp_act(s.seq_act[row]);
-    t.time = s.seq_time ? clamp_time(s.seq_time[row]) : 0;
-  } else if (row <= -2) {
-    const int64_t rr = -2 - row;
-    t.emb = static_cast<const uint8_t*>(s.rt_emb) + rr * row_bytes;
-    t.act = clamp_act(s.rt_act[rr]);
-    t.time = s.rt_time ? clamp_time(s.rt_time[rr]) : 0;
+  if (p < s.valid_len[n]) {
+    const int64_t m = n * s.T + p;
+    t.emb = static_cast<const uint8_t*>(s.tok_emb) + m * row_bytes;
+    t.act = clamp_act(s.tok_act[m]);
+    t.time = s.tok_time ? clamp_time(s.tok_time[m]) : 0;
   }
   return t;
 }
@@ -66,9 +101,8 @@ __device__ __forceinline__ int token_valid_len(const TokenSource& s, int64_t n) 
   if (s.explicit_tokens) {
     v = s.valid_len[n];
   } else {
-    const int r = s.cand_req[n];
-    const int L = s.seq_len[r];
-    v = (s.k < L ? s.k : L) + (s.rt_len ? s.rt_len[r] : 0);
+    const TokenParts q = token_parts(s, s.cand_req[n]);
+    v = q.t_ll + q.keep + q.t_rt + q.t_imp;
   }
   return v < 0 ? 0 : (v > s.T ? s.T : v);
 }

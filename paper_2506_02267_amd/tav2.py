@@ -41,6 +41,11 @@ class Tokens(ctypes.Structure):
                 ("dtype", c_int32), ("reserved", c_int32)]
 
 
+class Eq2(ctypes.Structure):
+    _fields_ = [("rt", POINTER(Seq)), ("r", c_int32), ("k_rt", c_int32), ("imp", POINTER(Seq)),
+                ("k_imp", c_int32), ("reserved", c_int32)]
+
+
 class Layer(ctypes.Structure):
     _fields_ = [(n, c_void_p) for n in ("W_qkv", "b_qkv", "W_o", "b_o", "ln1_g", "ln1_b",
                                         "W_1", "b_1", "W_2", "b_2", "ln2_g", "ln2_b")]
@@ -76,6 +81,11 @@ FUNCTIONS = {
     "tav2_select_encode": (c_int32, [POINTER(Seq), POINTER(Seq), POINTER(Cands), c_int32,
                                      POINTER(Weights), ctypes.c_uint32, c_void_p, c_void_p,
                                      c_void_p, c_void_p, c_size_t, c_void_p]),
+    "tav2_select_encode_eq2_workspace": (c_size_t, [POINTER(Seq), POINTER(Eq2), POINTER(Cands),
+                                                    c_int32, POINTER(Weights)]),
+    "tav2_select_encode_eq2": (c_int32, [POINTER(Seq), POINTER(Eq2), POINTER(Cands), c_int32,
+                                         POINTER(Weights), ctypes.c_uint32, c_void_p, c_void_p,
+                                         c_void_p, c_void_p, c_size_t, c_void_p]),
     "tav2_profile_enable": (c_int32, [c_int32, ctypes.c_char_p]),
     "tav2_profile_report": (ctypes.c_int64, [ctypes.c_char_p, c_size_t]),
 }
@@ -399,6 +409,43 @@ class SelectEncode:
             ctypes.byref(self.s), ctypes.byref(self.r) if self.r is not None else None,
             ctypes.byref(self.c), self.k, ctypes.byref(self.w.s), self.flags, _ptr(self.idx),
             _ptr(self.score), _ptr(self.out), self.wp, self.wb, _stream_handle(stream)))
+        return self.idx, self.score, self.out
+
+
+class SelectEncodeEq2:
+    """Prepared call of tav2_select_encode_eq2 (Eq. 2's four parts): structs,
+    outputs [total, k + k_rt + k_imp] and workspace built once."""
+
+    def __init__(self, seq: DeviceSeq, rt: Optional[DeviceSeq], r: int, k_rt: int,
+                 imp: Optional[DeviceSeq], k_imp: int, cands: DeviceCands, k: int,
+                 w: DeviceWeights, flags: int = MASK_CAUSAL):
+        self.lib = load_library()
+        self.args = (seq, rt, imp, cands, w)
+        self.s, self.c = seq.struct(), cands.struct()
+        self.r_s = rt.struct() if rt is not None else None
+        self.i_s = imp.struct() if imp is not None else None
+        self.e = Eq2(rt=ctypes.pointer(self.r_s) if self.r_s is not None else None, r=r,
+                     k_rt=k_rt, imp=ctypes.pointer(self.i_s) if self.i_s is not None else None,
+                     k_imp=k_imp, reserved=0)
+        self.k, self.w, self.flags = k, w, flags
+        dev = seq.emb.device
+        K = k + k_rt + k_imp
+        self.idx = torch.empty((cands.total, K), dtype=torch.int32, device=dev)
+        self.score = torch.empty((cands.total, K), dtype=torch.float32, device=dev)
+        self.out = torch.empty((cands.total, 2 * w.d_model), dtype=torch.float32, device=dev)
+        need = self.lib.tav2_select_encode_eq2_workspace(ctypes.byref(self.s), ctypes.byref(self.e),
+                                                         ctypes.byref(self.c), k,
+                                                         ctypes.byref(w.s))
+        if need == 0 and cands.total > 0:
+            need = 1   # invalid arguments: the call reports why
+        self.ws = Workspace(dev)
+        self.wp, self.wb = self.ws.get(need)
+
+    def __call__(self, stream=None):
+        _check("tav2_select_encode_eq2", self.lib.tav2_select_encode_eq2(
+            ctypes.byref(self.s), ctypes.byref(self.e), ctypes.byref(self.c), self.k,
+            ctypes.byref(self.w.s), self.flags, _ptr(self.idx), _ptr(self.score), _ptr(self.out),
+            self.wp, self.wb, _stream_handle(stream)))
         return self.idx, self.score, self.out
 
 

@@ -113,3 +113,23 @@ def strided_ids(inp, stride, boundaries=()):
     for e in boundaries:
         ids.update(x for x in (e - 1, e) if 0 <= x < inp.total)
     return np.array(sorted(ids), dtype=np.int64)
+
+
+def oracle_select_encode_eq2(inp, W, ids=None, chunk=16, causal=True):
+    """oracle.select_encode_eq2 for the candidates in ids (all by default), in
+    parallel chunks."""
+    w = inp.w
+    total = inp.total
+    K = w.k + (w.k_rt if inp.rt is not None else 0) + (w.k_imp if inp.imp is not None else 0)
+    ids = np.arange(total) if ids is None else np.asarray(ids, dtype=np.int64)
+    idx = np.full((total, K), -1, dtype=np.int32)
+    score = np.full((total, K), -np.inf, dtype=np.float32)
+    out = np.zeros((total, 2 * W.d_model), dtype=np.float64)
+
+    def one(part):
+        i, s, o = oracle.select_encode_eq2(inp, W, only=part, causal=causal)
+        return part, i[part], s[part], o[part]
+
+    for part, i, s, o in parallel_map(one, chunks(ids, chunk)):
+        idx[part], score[part], out[part] = i, s, o
+    return idx, score, out

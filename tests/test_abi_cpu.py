@@ -329,3 +329,47 @@ def test_fused_search_workspace_does_not_scale_with_the_sequence():
         assert lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 256) == 10 * 4096 * 4
     s = fake_seq(R=1, d=64, dtype=T.F32, max_len=16384)
     assert lib.tav2_nn_select_workspace(ctypes.byref(s), ctypes.byref(c), 256) == 10 * 16384 * 4
+
+
+def test_eq2_struct_layout_and_argument_errors(tmp_path):
+    src = tmp_path / "eq2.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "tav2.h"\n'
+                   'int main(void){printf("%zu %zu %zu\\n", sizeof(tav2_eq2),'
+                   'offsetof(tav2_eq2, imp), offsetof(tav2_eq2, k_imp));return 0;}\n')
+    exe = tmp_path / "eq2"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    assert got == [ctypes.sizeof(T.Eq2), T.Eq2.imp.offset, T.Eq2.k_imp.offset]
+
+    lib = T.load_library()
+    s, c = fake_seq(d=64), fake_cands()
+    rt, imp = fake_seq(d=64, max_len=100), fake_seq(d=64, max_len=80)
+
+    def call(eq2, k=64, w=None):
+        w = w or fake_weights(max_pos=1024)
+        return lib.tav2_select_encode_eq2(ctypes.byref(s), ctypes.byref(eq2) if eq2 else None,
+                                          ctypes.byref(c), k, ctypes.byref(w), 0, FAKE, FAKE, None,
+                                          FAKE, 1 << 40, None)
+
+    P = ctypes.pointer
+    assert call(None) == -1
+    assert call(T.Eq2(rt=None, r=0, k_rt=8, imp=None, k_imp=0)) == -1      # k_rt without S_RT
+    assert call(T.Eq2(rt=None, r=4, k_rt=0, imp=None, k_imp=0)) == -1      # r without S_RT
+    assert call(T.Eq2(rt=P(rt), r=4, k_rt=0, imp=None, k_imp=8)) == -1     # k_imp without S_imp
+    assert call(T.Eq2(rt=P(rt), r=-1, k_rt=0, imp=None, k_imp=0)) == -2
+    assert call(T.Eq2(rt=P(rt), r=4, k_rt=2000, imp=None, k_imp=0)) == -2  # k_rt > K_MAX
+    assert call(T.Eq2(rt=P(rt), r=100, k_rt=512, imp=P(imp), k_imp=512)) == -2   # T > 1024
+    assert call(T.Eq2(rt=P(rt), r=8, k_rt=8, imp=P(imp), k_imp=8),
+                w=fake_weights(max_pos=64 + 8 + 8 + 7)) == -2              # T > max_pos
+    other = fake_seq(R=3, d=64, max_len=80)
+    assert call(T.Eq2(rt=P(rt), r=8, k_rt=8, imp=P(other), k_imp=8)) == -2  # request count
+    # valid: the error comes from the missing output
+    assert call(T.Eq2(rt=P(rt), r=8, k_rt=8, imp=P(imp), k_imp=8)) == -1
+    need = lib.tav2_select_encode_eq2_workspace(
+        ctypes.byref(s), ctypes.byref(T.Eq2(rt=P(rt), r=8, k_rt=8, imp=P(imp), k_imp=8)),
+        ctypes.byref(c), 64, ctypes.byref(fake_weights(max_pos=1024)))
+    plain = lib.tav2_select_encode_workspace(ctypes.byref(s), None, ctypes.byref(c), 64,
+                                             ctypes.byref(fake_weights(max_pos=1024)))
+    assert need > plain > 0
