@@ -74,7 +74,7 @@ typedef int32_t tav2_status;
                                 comparisons; bf16 encoders take it only when T <= 128 */
 
 #define TAV2_K_MAX     1024  /* largest k of the NN search */
-#define TAV2_T_MAX     1024  /* largest encoder sequence (k + real-time tail) */
+#define TAV2_T_MAX     2048  /* largest encoder sequence (all token parts) */
 #define TAV2_N_ACT        8  /* action types: values in [0, 8) */
 #define TAV2_N_TIME      64  /* time buckets: values in [0, 64) */
 
@@ -252,8 +252,12 @@ tav2_status tav2_pack_weights(const tav2_weights* w, void* packed, size_t bytes,
  *   cand_emb device [total, d] (the tokens' dtype).
  * Supported shapes: bf16 with dm == 256, dm / n_heads in {32, 64},
  * d_ffn a multiple of 256 up to 4096, d a multiple of 32 up to 256, at most 8
- * layers; float32 with dm <= 128, d_ffn <= 512, T <= 64 and d <= 256.  Other
- * valid shapes return TAV2_ERR_UNSUPPORTED.
+ * layers; bf16 with dm == 64 (the paper's production encoder, Sec. 3.2.2),
+ * dm / n_heads in {32, 64}, d_ffn a multiple of 32 up to 256, d a multiple of
+ * 32 up to 256, at most 4 layers, all layer weights fitting the 160 KiB of LDS
+ * next to the activations (2 layers of FFN 32 do); float32 with dm <= 128,
+ * d_ffn <= 512, T <= 64 and d <= 256.  Other valid shapes return
+ * TAV2_ERR_UNSUPPORTED.  TAV2_MASK_NONE: T <= 128 for dm 256, T <= 64 for dm 64.
  * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_DTYPE, TAV2_ERR_UNSUPPORTED,
  * TAV2_ERR_WORKSPACE, TAV2_ERR_HIP.
  */

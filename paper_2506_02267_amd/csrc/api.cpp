@@ -82,6 +82,7 @@ tav2_status check_weights(const tav2_weights* w, int d, int dtype, int T, bool h
     }
   }
   if (dtype == TAV2_BF16) {
+    if (encode_small_supported(d, *w)) return TAV2_OK;   // d_model 64: weights used as given
     if (!encode_fused_supported(d, *w) || w->d_ffn > 4096) return TAV2_ERR_UNSUPPORTED;
     if (w->packed) {   // packed by tav2_pack_weights
       if (!aligned(w->packed, WS_ALIGN) || w->packed_bytes < encode_fused_packed_bytes(*w))
@@ -96,9 +97,11 @@ tav2_status check_weights(const tav2_weights* w, int d, int dtype, int T, bool h
 // The encoder's mask flags: TAV2_MASK_CAUSAL, or TAV2_MASK_NONE (the bf16 encoder
 // keeps positions in blocks of 128 that see only earlier blocks: unmasked, T must
 // fit one block).
-tav2_status check_flags(uint32_t flags, int dtype, int T) {
+tav2_status check_flags(uint32_t flags, const tav2_weights* w, int T) {
   if (flags != TAV2_MASK_CAUSAL && flags != TAV2_MASK_NONE) return TAV2_ERR_SHAPE;
-  if (flags == TAV2_MASK_NONE && dtype == TAV2_BF16 && T > 128) return TAV2_ERR_UNSUPPORTED;
+  if (flags == TAV2_MASK_NONE && w->dtype == TAV2_BF16 &&
+      T > (encode_small_supported(w->d_in, *w) ? SMALL_UNMASKED_MAX_T : 128))
+    return TAV2_ERR_UNSUPPORTED;
   return TAV2_OK;
 }
 
@@ -143,6 +146,8 @@ hipError_t run_select(const tav2_seq& s, const tav2_cands& c, int k, int32_t* ou
 
 size_t encode_ws_bytes(int64_t total, int T, const tav2_weights* w) {
   if (w->dtype == TAV2_F32) return 0;
+  if (encode_small_supported(w->d_in, *w))
+    return align_up(encode_small_workspace(total, T, *w), WS_ALIGN);
   return align_up(encode_fused_workspace(total, T, *w), WS_ALIGN);
 }
 
@@ -150,6 +155,8 @@ tav2_status run_encode(const TokenSource& src, const void* cand_emb, int64_t tot
                        const tav2_weights* w, uint32_t flags, float* out, void* ws,
                        hipStream_t st) {
   const bool unmasked = flags == TAV2_MASK_NONE;
+  if (w->dtype == TAV2_BF16 && encode_small_supported(w->d_in, *w))
+    return hip_status(launch_encode_small(src, cand_emb, total, *w, out, ws, unmasked, st));
   if (w->dtype == TAV2_BF16)
     return hip_status(launch_encode_fused(src, cand_emb, total, *w, out, ws, unmasked, st));
   return hip_status(launch_encode_f32(src, cand_emb, total, *w, out, unmasked, st));
@@ -198,7 +205,7 @@ tav2_status check_select_encode(const tav2_seq* seq, const Sources& src, const t
                     src.k_imp;
   if (T > TAV2_T_MAX) return TAV2_ERR_SHAPE;
   if ((st = check_weights(w, seq->d, seq->dtype, int(T), seq->time_bucket != nullptr))) return st;
-  if ((st = check_flags(flags, seq->dtype, int(T)))) return st;
+  if ((st = check_flags(flags, w, int(T)))) return st;
   *T_out = int(T);
   return TAV2_OK;
 }
@@ -369,7 +376,7 @@ size_t tav2_encode_workspace(const tav2_tokens* tok, const tav2_weights* w) {
 }
 
 size_t tav2_pack_weights_bytes(const tav2_weights* w) {
-  if (!w || w->dtype != TAV2_BF16) return 0;
+  if (!w || w->dtype != TAV2_BF16 || encode_small_supported(w->d_in, *w)) return 0;
   if (check_weights(w, w->d_in, TAV2_BF16, 1, w->E_time != nullptr)) return 0;
   return align_up(encode_fused_packed_bytes(*w), WS_ALIGN);
 }
@@ -380,7 +387,7 @@ tav2_status tav2_pack_weights(const tav2_weights* w, void* packed, size_t bytes,
   if ((st = check_dtype(w->dtype))) return st;
   if (w->d_in < 16 || w->d_in > 512 || w->d_in % 16) return TAV2_ERR_SHAPE;
   if ((st = check_weights(w, w->d_in, w->dtype, 1, w->E_time != nullptr))) return st;
-  if (w->dtype == TAV2_F32) return TAV2_OK;
+  if (w->dtype == TAV2_F32 || encode_small_supported(w->d_in, *w)) return TAV2_OK;
   if (!packed || !aligned(packed, WS_ALIGN) || bytes < encode_fused_packed_bytes(*w))
     return TAV2_ERR_WORKSPACE;
   return hip_status(launch_encode_fused_pack(*w, packed, static_cast<hipStream_t>(stream)));
@@ -395,7 +402,7 @@ tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2
   if (tok->total < 0 || tok->d < 16 || tok->d > 512 || tok->d % 16) return TAV2_ERR_SHAPE;
   if (tok->total > (int64_t(1) << 31) - 1) return TAV2_ERR_UNSUPPORTED;
   if ((st = check_weights(w, tok->d, tok->dtype, tok->T, tok->time_bucket != nullptr))) return st;
-  if ((st = check_flags(flags, tok->dtype, tok->T))) return st;
+  if ((st = check_flags(flags, w, tok->T))) return st;
   if (tok->total == 0) return TAV2_OK;
   if (!tok->emb || !tok->action_type || !tok->valid_len || !cand_emb || !out) return TAV2_ERR_NULL;
   if (!aligned(tok->emb, 16) || !aligned(cand_emb, 16) || !aligned(out, 16)) return TAV2_ERR_SHAPE;

@@ -108,6 +108,14 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
                                const tav2_weights& w, float* out, void* ws, bool unmasked,
                                hipStream_t st);
 
+// ---- encoder_small.hip: bf16 encoder for d_model 64 (all layer weights in LDS)
+constexpr int SMALL_UNMASKED_MAX_T = 64;   // the unmasked mode: one 64-position block
+bool encode_small_supported(int d, const tav2_weights& w);
+size_t encode_small_workspace(int64_t total, int T, const tav2_weights& w);
+hipError_t launch_encode_small(const TokenSource& src, const void* cand_emb, int64_t total,
+                               const tav2_weights& w, float* out, void* ws, bool unmasked,
+                               hipStream_t st);
+
 // ---- encoder_f32.hip
 constexpr int F32_MAX_T = 64;
 constexpr int F32_MAX_DM = 128;

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtav2.so"
 
 F32, BF16, I8 = 0, 1, 2
 MASK_CAUSAL, MASK_NONE = 0, 1
-K_MAX, T_MAX = 1024, 1024
+K_MAX, T_MAX = 1024, 2048
 STATUS = {0: "ok", -1: "null", -2: "shape", -3: "dtype", -4: "unsupported", -5: "workspace",
           -6: "hip", -7: "too_large"}
 

@@ -1,10 +1,10 @@
-"""The five workload shapes of the lifelong-sequence NN-select + encode path.
+"""The workload shapes of the lifelong-sequence NN-select + encode path.
 
 Each shape follows the paper's scales: a lifelong sequence of O(10^4) actions
 (Sec. 3.2.2, after Eq. 3), a selected sequence of O(10^2) tokens, and thousands
 of candidate items per ranking request (Sec. 1).  The encoder sizes are fixed
-per workload (the paper's own production encoder, d_model 64 / 1 head / FFN 32 /
-2 layers of Sec. 3.2.2, is smaller than all but the tiny workload).
+per workload; the paper's own production encoder (d_model 64 / 1 head / FFN 32 /
+2 layers of Sec. 3.2.2) is the paper workload's.
 
 This module holds shapes only: no arithmetic of the method.
 """
@@ -91,7 +91,13 @@ SELECT_I8 = Workload(6, "select_i8", "i8", R=1, L=16384, L_range=None, d=32, N=1
 EQ2 = Workload(7, "eq2_bf16", "bf16", R=1, L=16384, L_range=None, d=256, N=1000, k=256,
                d_model=256, n_heads=4, d_ffn=1024, n_layers=2, has_time=True, rt_len=200,
                rt_keep=32, k_rt=32, imp_len=300, k_imp=64)
-BY_NAME = {w.name: w for w in list(WORKLOADS.values()) + [SELECT_I8, EQ2]}
+# The paper's production encoder (Sec. 3.2.2: d_model 64, one head, FFN 32, two
+# layers; Sec. 4.4.2: 192 positions) on its 32-d PinSage embeddings (Sec. 3.2.1),
+# for a batch of 256 candidates (the production batch of Sec. 4.4.3); the 192
+# positions are the top-128 NN tokens and 64 real-time actions.
+PAPER = Workload(8, "paper_bf16", "bf16", R=1, L=16384, L_range=None, d=32, N=256, k=128,
+                 d_model=64, n_heads=1, d_ffn=32, n_layers=2, has_time=True, rt_len=64)
+BY_NAME = {w.name: w for w in list(WORKLOADS.values()) + [SELECT_I8, EQ2, PAPER]}
 
 
 def scaled(w: Workload, **changes) -> Workload:

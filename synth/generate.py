@@ -221,6 +221,37 @@ def make_weights(w: Workload, seed: Optional[int] = None, scale: float = 0.02) -
                    E_pos=E_pos, layers=layers, W_pool=W_pool, b_pool=b_pool)
 
 
+@dataclass
+class TokenBatch:
+    """Explicit encoder inputs (the encoder run on its own): per candidate T token
+    rows with their action types, time buckets and valid length, and the
+    candidate's embedding.  Rows at or past a valid length hold grid values too."""
+    emb: np.ndarray                 # [total, T, d] float32 on the 1/8 grid
+    act: np.ndarray                 # [total, T] uint8
+    time: Optional[np.ndarray]      # [total, T] uint8 or None
+    valid_len: np.ndarray           # [total] int32
+    cand: np.ndarray                # [total, d] float32 on the 1/8 grid
+
+    @property
+    def total(self) -> int:
+        return int(self.emb.shape[0])
+
+
+def make_tokens(total: int, T: int, d: int, has_time: bool = True, seed: int = 0,
+                valid_len=None) -> TokenBatch:
+    """Seeded explicit tokens: grid rows, uniform action types, sorted time buckets;
+    valid_len defaults to T for every candidate."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    emb = grid_values(rng, (total, T, d))
+    act = rng.integers(0, N_ACT, size=(total, T)).astype(np.uint8)
+    time = np.sort(rng.integers(0, N_TIME, size=(total, T)), axis=1).astype(np.uint8) \
+        if has_time else None
+    cand = grid_values(rng, (total, d))
+    vl = np.full(total, T, dtype=np.int32) if valid_len is None else \
+        np.asarray(valid_len, dtype=np.int32)
+    return TokenBatch(emb=emb, act=act, time=time, valid_len=vl, cand=cand)
+
+
 def to_padded(seq: SeqBatch, pad_to: Optional[int] = None) -> SeqBatch:
     """Same requests laid out with a fixed stride (offset[r] = r * stride).
 

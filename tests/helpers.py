@@ -133,3 +133,32 @@ def oracle_select_encode_eq2(inp, W, ids=None, chunk=16, causal=True):
     for part, i, s, o in parallel_map(one, chunks(ids, chunk)):
         idx[part], score[part], out[part] = i, s, o
     return idx, score, out
+
+
+def upload_tokens(tb, dtype=T.BF16, device="cuda"):
+    """A synth.TokenBatch as explicit device tokens and candidate embeddings."""
+    td = T.torch_dtype(dtype)
+    tok = T.DeviceTokens(
+        emb=torch.from_numpy(tb.emb).to(device=device, dtype=td).contiguous(),
+        act=torch.from_numpy(tb.act).to(device).contiguous(),
+        time=None if tb.time is None else torch.from_numpy(tb.time).to(device).contiguous(),
+        valid_len=torch.from_numpy(tb.valid_len).to(device).contiguous(), dtype=dtype)
+    cand = torch.from_numpy(tb.cand).to(device=device, dtype=td).contiguous()
+    return tok, cand
+
+
+def oracle_encode_tokens(tb, W, ids=None, causal=True, chunk=4):
+    """oracle.encode on explicit tokens for the candidates in ids (all by
+    default), in parallel chunks; rows outside ids are 0."""
+    ids = np.arange(tb.total) if ids is None else np.asarray(ids, dtype=np.int64)
+    out = np.zeros((tb.total, 2 * W.d_model), dtype=np.float64)
+    time = tb.time if tb.time is not None else np.zeros_like(tb.act)
+
+    def one(part):
+        o = oracle.encode(tb.emb, tb.act, time, tb.valid_len, tb.cand, W, only=part,
+                          chunk=chunk, causal=causal)
+        return part, o[part]
+
+    for part, o in parallel_map(one, chunks(ids, chunk)):
+        out[part] = o
+    return out

@@ -190,8 +190,8 @@ def test_encode_argument_errors(case, status):
     elif case == "null_layer_ptr":
         w.layers[1].W_2 = None
     elif case == "T_too_big":
-        tok.T = 2000
-        w.max_pos = 2000
+        tok.T = 3000
+        w.max_pos = 3000
     elif case == "f32_too_big":
         tok.dtype = T.F32
         w.dtype = T.F32
@@ -220,6 +220,38 @@ def test_encode_argument_errors(case, status):
         w.packed, w.packed_bytes = FAKE + 16, 1 << 40
     st = lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), flags, out, ws, wsb, None)
     assert st == status
+
+
+def test_small_encoder_queries():
+    """d_model 64 (bf16): weights used as given (nothing to pack); a workspace of
+    per-workgroup K / V caches past one 64-position block (layers x 2 x T padded
+    to 64 x d_model bf16 per workgroup, one workgroup per candidate up to 256);
+    the shapes whose weights outgrow the on-chip memory are unsupported."""
+    lib = T.load_library()
+    w = fake_weights(d=32, dm=64, heads=1, ffn=32, layers=2, max_pos=2048)
+    assert lib.tav2_pack_weights_bytes(ctypes.byref(w)) == 0
+    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
+                   d=32, dtype=T.BF16, reserved=0)
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == 0
+    tok.T = 192
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == 10 * 2 * 2 * 192 * 64 * 2
+    tok.T, tok.total = 2000, 1000
+    assert (lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w))
+            == 256 * 2 * 2 * 2048 * 64 * 2)
+    # the unmasked mode: one block of 64 positions (then the missing output is reported)
+    tok.T, tok.total = 64, 10
+    assert lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), T.MASK_NONE, None, FAKE,
+                           1 << 40, None) == -1
+    tok.T = 65
+    assert lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), T.MASK_NONE, FAKE, FAKE,
+                           1 << 40, None) == -4
+    for bad in (dict(layers=3), dict(ffn=64), dict(d=128), dict(ffn=48)):
+        kw = dict(d=32, dm=64, heads=1, ffn=32, layers=2, max_pos=2048)
+        kw.update(bad)
+        wb = fake_weights(**kw)
+        tok.T, tok.d = 64, kw["d"]
+        assert lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(wb), T.MASK_CAUSAL, FAKE,
+                               FAKE, 1 << 40, None) == -4, bad
 
 
 def test_unmasked_encoder_accepted_within_one_block():
