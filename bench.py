@@ -57,6 +57,7 @@ def site_work(w, total, valid_tokens, pairs, launches_per_step, rows_total, k):
     # the fused encoder: input projection (token half per token, candidate half per
     # candidate), all layers (causal attention over valid positions) and the head
     per["encoder_fused"] = ("flop", encoder_flop(w, total, valid_tokens), None)
+    per["encoder_small"] = ("flop", encoder_flop(w, total, valid_tokens), None)
     per["encode_f32"] = ("flop", encoder_flop(w, total, valid_tokens), None)
     scores_bytes = 4.0 * pairs
     per["score_bf16"] = ("flop", 2.0 * pairs * d, scores_bytes)
@@ -72,20 +73,35 @@ def site_work(w, total, valid_tokens, pairs, launches_per_step, rows_total, k):
     return out
 
 
-def encoder_flop(w, total, valid_tokens):
-    """Algorithmic FLOP of the encoder over all candidates (valid tokens only)."""
+def encoder_flop(w, total, valid_tokens, causal=True):
+    """Algorithmic FLOP of the encoder over all candidates (valid tokens only;
+    every candidate taken at the mean valid length)."""
     dm, ff, d, H = w.d_model, w.d_ffn, w.d, w.n_heads
     dh = dm // H
     M = valid_tokens
     Tv = valid_tokens / max(total, 1)
+    pairs = Tv * (Tv + 1) / 2.0 if causal else Tv * Tv
     return (2.0 * M * d * dm + 2.0 * total * d * dm
             + w.n_layers * (2.0 * M * (3 * dm * dm + dm * dm + 2 * ff * dm)
-                            + 4.0 * H * dh * total * Tv * (Tv + 1) / 2.0)
+                            + 4.0 * H * dh * total * pairs)
             + 2.0 * M * dm * dm)
 
 
 TRAFFIC_FILES = {"encoder_fused": "encoder_fused_{workload}_traffic.md"}
-KERNEL_SOURCES = {"encoder_fused": "paper_2506_02267_amd/csrc/encoder_fused.hip"}
+KERNEL_SOURCES = {"encoder_fused": ("paper_2506_02267_amd/csrc/encoder_fused_device.h",
+                                    "paper_2506_02267_amd/csrc/encoder_fused.hip")}
+
+
+def kernel_sha256(site):
+    """SHA-256 over the source files of a kernel site (None if one is missing)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[site]:
+        path = os.path.join(ROOT, f)
+        if not os.path.exists(path):
+            return None
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
 
 
 def measured_traffic(site, workload):
@@ -95,15 +111,13 @@ def measured_traffic(site, workload):
     a plain copy of known size, and the SHA-256 of the kernel source it was taken
     on; a different source (the kernel changed since) gives None.
     """
-    import hashlib
     name = TRAFFIC_FILES.get(site)
     if name is None:
         return None
     path = os.path.join(ROOT, "profiles", name.format(workload=workload))
-    src = os.path.join(ROOT, KERNEL_SOURCES[site])
-    if not (os.path.exists(path) and os.path.exists(src)):
+    sha = kernel_sha256(site)
+    if not os.path.exists(path) or sha is None:
         return None
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
     fields = {}
     for line in open(path):
         if line.startswith("<!-- ") and ":" in line:
@@ -203,6 +217,74 @@ def cpu_baseline_eq2(inp, W, budget_s):
                        f"candidates ({t:.2f} s), float64 numpy")}
 
 
+SWEEP_SEQ = (64, 128, 192, 256, 512, 1024, 2048)          # at batch 256
+SWEEP_BATCH = (16, 32, 64, 128, 256, 512, 1024, 2048)     # at 192 positions
+
+
+def sweep(args):
+    """The encoder alone (tav2_encode on explicit tokens) at the paper's production
+    shape (d 32, d_model 64, one head, FFN 32, two layers, causal), over positions
+    at batch 256 and over batch at 192 positions: one JSON line per point with the
+    forward latency, its MFMA roofline fraction and the oracle on a sample."""
+    import torch
+    import oracle
+    import synth
+    from paper_2506_02267_amd import tav2 as T
+
+    points = [(t, 256) for t in SWEEP_SEQ] + [(192, b) for b in SWEEP_BATCH if b != 256]
+    budget = args.cpu_budget / len(points)
+    for T_, B in points:
+        w = synth.scaled(synth.PAPER, k=T_, rt_len=0, N=B)
+        W = synth.make_weights(w)
+        tb = synth.make_tokens(B, T_, w.d, seed=T_ * 4099 + B)
+        tok = T.DeviceTokens(emb=torch.from_numpy(tb.emb).to("cuda", torch.bfloat16),
+                             act=torch.from_numpy(tb.act).cuda(),
+                             time=torch.from_numpy(tb.time).cuda(),
+                             valid_len=torch.from_numpy(tb.valid_len).cuda(), dtype=T.BF16)
+        cand = torch.from_numpy(tb.cand).to("cuda", torch.bfloat16)
+        dw = T.DeviceWeights(W)
+        out = torch.empty((B, 2 * w.d_model), dtype=torch.float32, device="cuda")
+        ws = T.Workspace(torch.device("cuda"))
+        for _ in range(args.warmup):
+            T.encode(tok, cand, dw, out=out, ws=ws)
+        stream = torch.cuda.current_stream()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            T.encode(tok, cand, dw, out=out, ws=ws)
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / args.steps
+        flop = encoder_flop(w, B, B * T_)
+        ach = flop / (ms / 1000.0) / 1e12
+        cpu = None
+        if not args.no_cpu_baseline:
+            n, t = 0, 0.0
+            while n < B and (t < budget or n == 0):
+                ids = np.arange(n, min(B, n + 4))
+                t0 = time.perf_counter()
+                oracle.encode(tb.emb, tb.act, tb.time, tb.valid_len, tb.cand, W, only=ids)
+                t += time.perf_counter() - t0
+                n += ids.size
+            cpu = {"value": round(n / t, 2), "unit": "candidates/s", "cores": _threads(),
+                   "kind": "oracle", "sample": f"encoder of {n} of {B} candidates ({t:.2f} s)"}
+        line = {"metric": "encoder forward latency, paper shape (d_model 64, 1 head, FFN 32, "
+                          "2 layers, causal)",
+                "value": round(ms, 4), "unit": "ms", "higher_is_better": False,
+                "candidates_per_s": round(B / (ms / 1000.0), 1), "dtype": "bf16",
+                "config": {"workload": "paper_encoder", "T": T_, "batch": B, "d": w.d,
+                           "d_model": w.d_model, "heads": w.n_heads, "d_ffn": w.d_ffn,
+                           "layers": w.n_layers},
+                "roofline": {"bound": "mfma", "achieved": round(ach, 2),
+                             "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                             "frac": round(ach / PEAK_BF16_TFLOPS, 4)},
+                "workspace_bytes": ws.buf.numel() if ws.buf is not None else 0,
+                "cpu_baseline": cpu}
+        print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,13 +293,17 @@ def main():
     ap.add_argument("--workload", default="single_bf16",
                     help="tiny_f32 | single_bf16 | ragged_bf16 | mixed_bf16 | stress_bf16 | "
                          "select_i8 (the NN search alone over int8 codes) | eq2_bf16 (all four "
-                         "parts of Eq. 2)")
+                         "parts of Eq. 2) | paper_bf16 (the paper's production encoder)")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="time replays of one step captured as a HIP graph (the roofline "
                          "figure still comes from an eager pass)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="the encoder alone at the paper's production shape over 64-2048 "
+                         "positions (batch 256) and batch 16-2048 (192 positions): one JSON "
+                         "line per point")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 256 MiB device to device three times "
                          "(a plain copy of known size for scaling memory counters)")
@@ -227,6 +313,9 @@ def main():
               "multi-GPU mode (candidates would shard across GPUs with no exchange).",
               file=sys.stderr)
         sys.exit(2)
+    if args.sweep:
+        sweep(args)
+        return
 
     import torch
     import synth

@@ -155,7 +155,8 @@ typedef struct tav2_weights {
   const tav2_layer* layers;                  /* HOST array of n_layers layer records */
   const void*  W_pool; const float* b_pool;  /* device [dm, dm]; [dm] */
   const void*  packed;         /* device: these weights as tav2_pack_weights wrote them, or
-                                  NULL (then every call packs them into its workspace) */
+                                  NULL (then every call packs them into its workspace;
+                                  dm 64: every call reads them as given) */
   uint64_t     packed_bytes;   /* size of `packed` (ignored when it is NULL) */
 } tav2_weights;
 
@@ -229,7 +230,9 @@ tav2_status tav2_gather(const tav2_seq* seq, const tav2_seq* rt, const tav2_cand
 
 /*
  * Packed encoder weights: the bf16 encoder reads its matrices and side tables in
- * its own fragment order.  tav2_pack_weights writes that form once into a
+ * its own fragment order (dm 64: the image of every layer weight, W_in's token
+ * half and W_pool as the kernel holds them in LDS, which it then loads with one
+ * contiguous copy).  tav2_pack_weights writes that form once into a
  * caller-owned device buffer of tav2_pack_weights_bytes(w) bytes (256-byte
  * aligned); a tav2_weights whose `packed` points at it skips the packing step
  * of every later call (the paper's serving engine likewise keeps its model in
@@ -255,7 +258,8 @@ tav2_status tav2_pack_weights(const tav2_weights* w, void* packed, size_t bytes,
  * layers; bf16 with dm == 64 (the paper's production encoder, Sec. 3.2.2),
  * dm / n_heads in {32, 64}, d_ffn a multiple of 32 up to 256, d a multiple of
  * 32 up to 256, at most 4 layers, all layer weights fitting the 160 KiB of LDS
- * next to the activations (2 layers of FFN 32 do); float32 with dm <= 128,
+ * next to the activations (2 layers of FFN 32 with d <= 64 do), its matrices
+ * 16-byte and its tables 8-byte aligned (else TAV2_ERR_SHAPE); float32 with dm <= 128,
  * d_ffn <= 512, T <= 64 and d <= 256.  Other valid shapes return
  * TAV2_ERR_UNSUPPORTED.  TAV2_MASK_NONE: T <= 128 for dm 256, T <= 64 for dm 64.
  * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_DTYPE, TAV2_ERR_UNSUPPORTED,

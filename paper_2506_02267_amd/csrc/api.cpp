@@ -82,11 +82,12 @@ tav2_status check_weights(const tav2_weights* w, int d, int dtype, int T, bool h
     }
   }
   if (dtype == TAV2_BF16) {
-    if (encode_small_supported(d, *w)) return TAV2_OK;   // d_model 64: weights used as given
-    if (!encode_fused_supported(d, *w) || w->d_ffn > 4096) return TAV2_ERR_UNSUPPORTED;
+    const bool small = encode_small_supported(d, *w);   // d_model 64
+    if (small && !encode_small_aligned(*w)) return TAV2_ERR_SHAPE;
+    if (!small && (!encode_fused_supported(d, *w) || w->d_ffn > 4096)) return TAV2_ERR_UNSUPPORTED;
     if (w->packed) {   // packed by tav2_pack_weights
-      if (!aligned(w->packed, WS_ALIGN) || w->packed_bytes < encode_fused_packed_bytes(*w))
-        return TAV2_ERR_WORKSPACE;
+      const size_t need = small ? encode_small_packed_bytes(*w) : encode_fused_packed_bytes(*w);
+      if (!aligned(w->packed, WS_ALIGN) || w->packed_bytes < need) return TAV2_ERR_WORKSPACE;
     }
   } else {
     if (!encode_f32_fits(T, *w) || d > 256) return TAV2_ERR_UNSUPPORTED;
@@ -376,8 +377,10 @@ size_t tav2_encode_workspace(const tav2_tokens* tok, const tav2_weights* w) {
 }
 
 size_t tav2_pack_weights_bytes(const tav2_weights* w) {
-  if (!w || w->dtype != TAV2_BF16 || encode_small_supported(w->d_in, *w)) return 0;
+  if (!w || w->dtype != TAV2_BF16) return 0;
   if (check_weights(w, w->d_in, TAV2_BF16, 1, w->E_time != nullptr)) return 0;
+  if (encode_small_supported(w->d_in, *w))
+    return align_up(encode_small_packed_bytes(*w), WS_ALIGN);
   return align_up(encode_fused_packed_bytes(*w), WS_ALIGN);
 }
 
@@ -387,10 +390,13 @@ tav2_status tav2_pack_weights(const tav2_weights* w, void* packed, size_t bytes,
   if ((st = check_dtype(w->dtype))) return st;
   if (w->d_in < 16 || w->d_in > 512 || w->d_in % 16) return TAV2_ERR_SHAPE;
   if ((st = check_weights(w, w->d_in, w->dtype, 1, w->E_time != nullptr))) return st;
-  if (w->dtype == TAV2_F32 || encode_small_supported(w->d_in, *w)) return TAV2_OK;
-  if (!packed || !aligned(packed, WS_ALIGN) || bytes < encode_fused_packed_bytes(*w))
-    return TAV2_ERR_WORKSPACE;
-  return hip_status(launch_encode_fused_pack(*w, packed, static_cast<hipStream_t>(stream)));
+  if (w->dtype == TAV2_F32) return TAV2_OK;
+  const bool small = encode_small_supported(w->d_in, *w);
+  const size_t need = small ? encode_small_packed_bytes(*w) : encode_fused_packed_bytes(*w);
+  if (!packed || !aligned(packed, WS_ALIGN) || bytes < need) return TAV2_ERR_WORKSPACE;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  return hip_status(small ? launch_encode_small_pack(*w, packed, hs)
+                          : launch_encode_fused_pack(*w, packed, hs));
 }
 
 tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2_weights* w,

@@ -37,6 +37,7 @@ constexpr int BT = 64;          // tokens per block
 constexpr int NT = 256;         // threads (4 waves, 16 tokens each)
 constexpr int RLD = DM + 8;     // row stride (bf16) of [*][64] activations and weights
 constexpr int MAX_LAYERS = 4;
+constexpr int MAX_DK = 8;       // token width d <= 256: at most 8 k-steps of 32 (kernels for 1, 2, 4, 8)
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ f32x4 mma(const bf16x8& a, const bf16x8& b, const f32x4& c) {
@@ -70,19 +71,19 @@ struct Args {
   const bf16_t* W_pool;      // [DM, DM]
   const float* b_pool;
   tav2_layer layers[MAX_LAYERS];
+  const uint8_t* packed;     // the weights' LDS image (tav2_pack_weights), or null
   int n_layers, d, dh, ffn;
   int64_t total;
   int tpad;                  // cache stride in positions (T rounded up to BT)
   bf16_t* kcache;            // [grid][layers][tpad][DM]
   bf16_t* vcache;            // [grid][layers][DM][tpad]
   float* out;                // [total, 2 DM]
-  // LDS layout (bytes)
+  // LDS layout (bytes): the weights' image [0, wbytes), then the activations
   LayerW lw[MAX_LAYERS];
-  int win, wpool, xb, q, k, vt, h, cvec, pool, tinfo, rowp, lds_bytes;
+  int win, wpool, wbytes, xb, q, k, vt, h, cvec, pool, lds_bytes;
   int unmasked;
 };
 
-// LDS layout: weights first (loaded once), then the block's activations.
 __host__ __device__ inline void plan_lds(Args& a) {
   int off = 0;
   auto take = [&](int bytes) {
@@ -100,22 +101,21 @@ __host__ __device__ inline void plan_lds(Args& a) {
   }
   a.win = take(DM * (a.d + 8) * 2);
   a.wpool = take(DM * RLD * 2);
+  a.wbytes = off;
   a.xb = take(BT * RLD * 2);
   a.q = take(BT * RLD * 2);    // Q, then the attention output O
   a.k = take(BT * RLD * 2);
   a.vt = take(DM * RLD * 2);   // V^T [dim][key]
   a.h = take(BT * fld * 2);
   a.cvec = take(DM * 4);
-  a.pool = take(5 * DM * 4);   // running maxima, then one partial per wave
-  a.tinfo = take(BT * 4);
-  a.rowp = take(BT * 8);
+  a.pool = take(4 * DM * 4);   // one row of pooled maxima per wave
   a.lds_bytes = off;
 }
 // Offsets of the layer vectors inside lw.vec (floats).
 constexpr int V_BQKV = 0, V_BO = 3 * DM, V_LN1G = 4 * DM, V_LN1B = 5 * DM, V_B1 = 6 * DM;
-__device__ __forceinline__ int v_b2(int ffn) { return 6 * DM + ffn; }
-__device__ __forceinline__ int v_ln2g(int ffn) { return 7 * DM + ffn; }
-__device__ __forceinline__ int v_ln2b(int ffn) { return 8 * DM + ffn; }
+__host__ __device__ constexpr int v_b2(int ffn) { return 6 * DM + ffn; }
+__host__ __device__ constexpr int v_ln2g(int ffn) { return 7 * DM + ffn; }
+__host__ __device__ constexpr int v_ln2b(int ffn) { return 8 * DM + ffn; }
 
 // Orders a wave's LDS writes before its later LDS reads of rows other lanes wrote
 // (the wave's own token rows: no workgroup barrier is needed for them).
@@ -127,21 +127,64 @@ __device__ __forceinline__ void wave_lds_sync() {
 
 // Copy a row-major [rows][cols] bf16 matrix into LDS rows of stride ld.
 __device__ __forceinline__ void copy_matrix(bf16_t* dst, int ld, const bf16_t* src, int rows,
-                                            int cols) {
+                                            int cols, int src_ld) {
   const int per = cols / 8;
   for (int e = threadIdx.x; e < rows * per; e += NT) {
     const int r = e / per, c = e % per;
     *reinterpret_cast<uint4*>(dst + r * ld + c * 8) =
-        *reinterpret_cast<const uint4*>(src + int64_t(r) * cols + c * 8);
+        *reinterpret_cast<const uint4*>(src + int64_t(r) * src_ld + c * 8);
   }
 }
 __device__ __forceinline__ void copy_floats(float* dst, const float* src, int n) {
   for (int e = threadIdx.x; e < n; e += NT) dst[e] = src[e];
 }
 
+// The weights into LDS: the packed image with 8 loads in flight per thread, or
+// matrix by matrix from the caller's layout.
+__device__ __forceinline__ void load_weights(const Args& A, uint8_t* smem) {
+  if (A.packed) {
+    const int units = A.wbytes / 16;
+    const uint4* src = reinterpret_cast<const uint4*>(A.packed);
+    uint4* dst = reinterpret_cast<uint4*>(smem);
+    for (int u0 = threadIdx.x; u0 < units; u0 += 8 * NT) {
+      uint4 v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = src[min(u0 + j * NT, units - 1)];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (u0 + j * NT < units) dst[u0 + j * NT] = v[j];
+    }
+    return;
+  }
+  const int ffn = A.ffn;
+  for (int l = 0; l < A.n_layers; ++l) {
+    const tav2_layer& L = A.layers[l];
+    copy_matrix(reinterpret_cast<bf16_t*>(smem + A.lw[l].qkv), RLD,
+                static_cast<const bf16_t*>(L.W_qkv), 3 * DM, DM, DM);
+    copy_matrix(reinterpret_cast<bf16_t*>(smem + A.lw[l].o), RLD, static_cast<const bf16_t*>(L.W_o),
+                DM, DM, DM);
+    copy_matrix(reinterpret_cast<bf16_t*>(smem + A.lw[l].w1), RLD,
+                static_cast<const bf16_t*>(L.W_1), ffn, DM, DM);
+    copy_matrix(reinterpret_cast<bf16_t*>(smem + A.lw[l].w2), ffn + 8,
+                static_cast<const bf16_t*>(L.W_2), DM, ffn, ffn);
+    float* v = reinterpret_cast<float*>(smem + A.lw[l].vec);
+    copy_floats(v + V_BQKV, L.b_qkv, 3 * DM);
+    copy_floats(v + V_BO, L.b_o, DM);
+    copy_floats(v + V_LN1G, L.ln1_g, DM);
+    copy_floats(v + V_LN1B, L.ln1_b, DM);
+    copy_floats(v + V_B1, L.b_1, ffn);
+    copy_floats(v + v_b2(ffn), L.b_2, DM);
+    copy_floats(v + v_ln2g(ffn), L.ln2_g, DM);
+    copy_floats(v + v_ln2b(ffn), L.ln2_b, DM);
+  }
+  // token half of W_in: columns 0 .. d - 1 of [DM][2 d]
+  copy_matrix(reinterpret_cast<bf16_t*>(smem + A.win), A.d + 8, A.W_in, DM, A.d, 2 * A.d);
+  copy_matrix(reinterpret_cast<bf16_t*>(smem + A.wpool), RLD, A.W_pool, DM, DM, DM);
+}
+
 // ---------------------------------------------------------------- LayerNorm
-// acc[f] (f = feature tile) holds X^T of the lane's token: features 16 f + 4 g + i.
-// Normalises over the 64 features (two passes: mean, then the centred squares).
+// x[f] holds X^T of the lane's token: features 16 f + 4 g + i.  Normalises over
+// the 64 features (two passes: mean, then the centred squares).
 __device__ __forceinline__ void layer_norm(f32x4 (&x)[4], const float* g, const float* b) {
   const int lane = threadIdx.x % WAVE, grp = lane / 16;
   float s = 0.f;
@@ -179,28 +222,55 @@ __device__ __forceinline__ void store_xb(bf16_t* Xb, const f32x4 (&x)[4]) {
   for (int f = 0; f < 4; ++f) put4(row + 16 * f, x[f][0], x[f][1], x[f][2], x[f][3]);
   wave_lds_sync();
 }
-// The 4 bf16 at p (8-byte aligned) added to v.
-__device__ __forceinline__ void add4(float (&v)[4], const bf16_t* p) {
-  const uint2 r = *reinterpret_cast<const uint2*>(p);
+// The 4 bf16 of r added to v.
+__device__ __forceinline__ void add4(float (&v)[4], uint2 r) {
   v[0] += __uint_as_float(r.x << 16);
   v[1] += __uint_as_float(r.x & 0xFFFF0000u);
   v[2] += __uint_as_float(r.y << 16);
   v[3] += __uint_as_float(r.y & 0xFFFF0000u);
 }
-
-// acc[f] += W[16 f + .., :K] X^T for the wave's tokens: A = W rows (LDS, stride
-// wld), B = the tokens' rows of ACT (LDS, stride ald), K a multiple of 32.
-template <int NF>
-__device__ __forceinline__ void wt_product(f32x4 (&acc)[NF], const bf16_t* W, int wld,
-                                           const bf16_t* ACT, int ald, int K) {
+// Operand fragments of the wave's own 16 token rows of a [BT][RLD] buffer over
+// 64 features (identical for the A and the B operand: row / column l % 16, k = 8 (l / 16)).
+__device__ __forceinline__ void own_rows(bf16x8 (&xf)[2], const bf16_t* buf) {
   const int lane = threadIdx.x % WAVE, w = threadIdx.x / WAVE;
-  const int c16 = lane % 16, g = lane / 16;
-  const bf16_t* arow = W + c16 * wld + 8 * g;
-  const bf16_t* brow = ACT + (16 * w + c16) * ald + 8 * g;
-  for (int k0 = 0; k0 < K; k0 += 32) {
-    const bf16x8 b = frag(brow + k0);
+  const bf16_t* row = buf + (16 * w + lane % 16) * RLD + 8 * (lane / 16);
+  xf[0] = frag(row);
+  xf[1] = frag(row + 32);
+}
+
+// ------------------------------------------------------------ token inputs
+// One lane's token for Eq. 4: its embedding fragments (k-steps of 32) and the 4
+// side-table values of each feature tile; zeros for a padding position.
+template <int NK>
+struct TokLoad {
+  bf16x8 e[NK];
+  uint2 ea[4], ep[4], et[4];
+};
+__device__ __forceinline__ TokenRef lane_token(const Args& A, int64_t n, int p, int Tv) {
+  TokenRef t{nullptr, 0, 0};
+  if (p < Tv) t = resolve_token(A.s, n, p, A.d * 2);
+  return t;
+}
+template <int NK>
+__device__ __forceinline__ void load_token(TokLoad<NK>& L, const TokenRef& t, int p, bool valid,
+                                           const Args& A, int nk) {
+  const int g = (threadIdx.x % WAVE) / 16;
+  const bf16_t* row = reinterpret_cast<const bf16_t*>(t.emb);
+  const bool have = valid && row != nullptr;
 #pragma unroll
-    for (int f = 0; f < NF; ++f) acc[f] = mma(frag(arow + 16 * f * wld + k0), b, acc[f]);
+  for (int k = 0; k < NK; ++k) {
+    L.e[k] = bf16x8{};
+    if (have && k < nk) L.e[k] = frag(row + 32 * k + 8 * g);
+  }
+#pragma unroll
+  for (int f = 0; f < 4; ++f) {
+    const int feat = 16 * f + 4 * g;
+    L.ea[f] = L.ep[f] = L.et[f] = make_uint2(0u, 0u);
+    if (valid) {
+      L.ea[f] = *reinterpret_cast<const uint2*>(A.E_act + t.act * DM + feat);
+      L.ep[f] = *reinterpret_cast<const uint2*>(A.E_pos + int64_t(p) * DM + feat);
+      if (A.E_time) L.et[f] = *reinterpret_cast<const uint2*>(A.E_time + t.time * DM + feat);
+    }
   }
 }
 
@@ -212,24 +282,41 @@ struct Att {
   f32x4 o[DH / 16];     // O^T accumulators
   float m, l;           // running max (log2 units), this lane's partial row sum
 };
-
-// One 32-key pair: keys from K rows (A operand rows: key, k = dims) and V^T
-// columns (A operand of O^T += V^T P^T: rows dims, k = keys in vpos order).  Key
-// j of the pair is visible to the lane's query iff j < lim (32: all).  Before the
-// first visible key the running max is -inf: the exponents then use 0 as
-// reference, which gives zero weights and a zero rescale of the (zero) sums.
+// Operands of one 32-key pair: K rows (A operand of S^T = K Q^T: rows keys,
+// k = dims) and V^T rows (A operand of O^T += V^T P^T: rows dims, k = keys in
+// vpos order).
 template <int DH>
-__device__ __forceinline__ void att_pair(Att<DH>& st, const bf16_t* K, int kld, const bf16_t* Vt,
-                                         int vld, int col0, int lim, float scale_l2) {
+struct Pair {
+  bf16x8 k[2][DH / 32];
+  bf16x8 v[DH / 16];
+};
+template <int DH>
+__device__ __forceinline__ void load_pair(Pair<DH>& f, const bf16_t* K, int kld, const bf16_t* Vt,
+                                          int vld, int col0) {
   const int lane = threadIdx.x % WAVE;
   const int c16 = lane % 16, g = lane / 16;
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int kb = 0; kb < DH / 32; ++kb)
+      f.k[t][kb] = frag(K + (16 * t + c16) * kld + col0 + 32 * kb + 8 * g);
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) f.v[dt] = frag(Vt + (col0 + 16 * dt + c16) * vld + 8 * g);
+}
+
+// One 32-key pair.  Key j of the pair is visible to the lane's query iff j < lim
+// (32: all).  Before the first visible key the running max is -inf: the
+// exponents then use 0 as reference, which gives zero weights and a zero rescale
+// of the (zero) sums.
+template <int DH>
+__device__ __forceinline__ void att_pair(Att<DH>& st, const Pair<DH>& f, int lim, float scale_l2) {
+  const int g = (threadIdx.x % WAVE) / 16;
   f32x4 s[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
     f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < DH / 32; ++kb)
-      a = mma(frag(K + (16 * t + c16) * kld + col0 + 32 * kb + 8 * g), st.qf[kb], a);
+    for (int kb = 0; kb < DH / 32; ++kb) a = mma(f.k[t][kb], st.qf[kb], a);
     s[t] = a;
   }
   // key 16 t + 4 g + i of the pair
@@ -261,13 +348,13 @@ __device__ __forceinline__ void att_pair(Att<DH>& st, const bf16_t* K, int kld, 
       pb[4 * t + i] = static_cast<__bf16>(p);
     }
 #pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt)
-    st.o[dt] = mma(frag(Vt + (col0 + 16 * dt + c16) * vld + 8 * g), pb, st.o[dt]);
+  for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = mma(f.v[dt], pb, st.o[dt]);
 }
 
 // Attention of the wave's 16 queries (block positions 16 w ..) for one head: the
-// block's own keys 0 .. 16 w + 15 (causal; unmasked: 0 .. nkv - 1), then earlier
-// blocks' keys from the cache.  Leaves O = softmax(S) V in the Q rows.
+// block's own keys 0 .. 16 w + 15 (causal; unmasked: 0 .. nkv - 1) from LDS, then
+// the p0 keys of earlier blocks from the cache, each pair's operands loaded while
+// the previous pair is computed.  Leaves O = softmax(S) V in the Q rows.
 template <int DH>
 __device__ __forceinline__ void attend(bf16_t* Qs, const bf16_t* Ks, const bf16_t* Vts,
                                        const bf16_t* kc, const bf16_t* vc, int tpad, int p0,
@@ -275,22 +362,35 @@ __device__ __forceinline__ void attend(bf16_t* Qs, const bf16_t* Ks, const bf16_
   const int lane = threadIdx.x % WAVE, w = threadIdx.x / WAVE;
   const int c16 = lane % 16, g = lane / 16;
   constexpr float scale_l2 = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
+  const int npair = p0 / 32;
+  Pair<DH> ca, cb;
+  if (npair > 0) load_pair<DH>(ca, kc, DM, vc, tpad, col0);
   Att<DH> st;
 #pragma unroll
-  for (int kb = 0; kb < DH / 32; ++kb) st.qf[kb] = frag(Qs + (16 * w + c16) * RLD + col0 + 32 * kb + 8 * g);
+  for (int kb = 0; kb < DH / 32; ++kb)
+    st.qf[kb] = frag(Qs + (16 * w + c16) * RLD + col0 + 32 * kb + 8 * g);
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   st.m = -__builtin_inff();
   st.l = 0.f;
-  // earlier blocks: every key visible
-  for (int c0 = 0; c0 < p0; c0 += 32)
-    att_pair<DH>(st, kc + int64_t(c0) * DM, DM, vc + c0, tpad, col0, 32, scale_l2);
   // own block: query 16 w + c16 sees keys <= itself (causal) or < nkv (unmasked)
   const int q = 16 * w + c16;
   const int kend = unmasked ? nkv : 16 * (w + 1);
   for (int k0 = 0; k0 < kend; k0 += 32) {
-    const int lim = unmasked ? nkv - k0 : q + 1 - k0;   // keys k0 + j visible iff j < lim
-    att_pair<DH>(st, Ks + k0 * RLD, RLD, Vts + k0, RLD, col0, lim, scale_l2);
+    Pair<DH> f;
+    load_pair<DH>(f, Ks + k0 * RLD, RLD, Vts + k0, RLD, col0);
+    att_pair<DH>(st, f, unmasked ? nkv - k0 : q + 1 - k0, scale_l2);
+  }
+  // earlier blocks: every key visible; two pairs per trip (operands double-buffered)
+  for (int c = 0; c < npair; c += 2) {
+    if (c + 1 < npair)
+      load_pair<DH>(cb, kc + int64_t(c + 1) * 32 * DM, DM, vc + (c + 1) * 32, tpad, col0);
+    att_pair<DH>(st, ca, 32, scale_l2);
+    if (c + 1 < npair) {
+      if (c + 2 < npair)
+        load_pair<DH>(ca, kc + int64_t(c + 2) * 32 * DM, DM, vc + (c + 2) * 32, tpad, col0);
+      att_pair<DH>(st, cb, 32, scale_l2);
+    }
   }
   float l = st.l;
   l += __shfl_xor(l, 16, WAVE);
@@ -305,42 +405,14 @@ __device__ __forceinline__ void attend(bf16_t* Qs, const bf16_t* Ks, const bf16_
 }
 
 // ---------------------------------------------------------------- the kernel
+// NK: k-steps of 32 token features the kernel is built for (d / 32 <= NK).
+template <int NK>
 __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int tid = threadIdx.x, lane = tid % WAVE, w = tid / WAVE;
   const int c16 = lane % 16, g = lane / 16;
-  const int d = A.d, ffn = A.ffn, fld = ffn + 8;
-  // ---- weights into LDS, once
-  for (int l = 0; l < A.n_layers; ++l) {
-    const tav2_layer& L = A.layers[l];
-    copy_matrix(reinterpret_cast<bf16_t*>(smem + A.lw[l].qkv), RLD,
-                static_cast<const bf16_t*>(L.W_qkv), 3 * DM, DM);
-    copy_matrix(reinterpret_cast<bf16_t*>(smem + A.lw[l].o), RLD, static_cast<const bf16_t*>(L.W_o),
-                DM, DM);
-    copy_matrix(reinterpret_cast<bf16_t*>(smem + A.lw[l].w1), RLD,
-                static_cast<const bf16_t*>(L.W_1), ffn, DM);
-    copy_matrix(reinterpret_cast<bf16_t*>(smem + A.lw[l].w2), fld,
-                static_cast<const bf16_t*>(L.W_2), DM, ffn);
-    float* v = reinterpret_cast<float*>(smem + A.lw[l].vec);
-    copy_floats(v + V_BQKV, L.b_qkv, 3 * DM);
-    copy_floats(v + V_BO, L.b_o, DM);
-    copy_floats(v + V_LN1G, L.ln1_g, DM);
-    copy_floats(v + V_LN1B, L.ln1_b, DM);
-    copy_floats(v + V_B1, L.b_1, ffn);
-    copy_floats(v + v_b2(ffn), L.b_2, DM);
-    copy_floats(v + v_ln2g(ffn), L.ln2_g, DM);
-    copy_floats(v + v_ln2b(ffn), L.ln2_b, DM);
-  }
-  {   // token half of W_in: columns 0 .. d - 1 of [DM][2 d]
-    bf16_t* dst = reinterpret_cast<bf16_t*>(smem + A.win);
-    const int per = d / 8;
-    for (int e = tid; e < DM * per; e += NT) {
-      const int r = e / per, c = e % per;
-      *reinterpret_cast<uint4*>(dst + r * (d + 8) + c * 8) =
-          *reinterpret_cast<const uint4*>(A.W_in + int64_t(r) * 2 * d + c * 8);
-    }
-  }
-  copy_matrix(reinterpret_cast<bf16_t*>(smem + A.wpool), RLD, A.W_pool, DM, DM);
+  const int d = A.d, ffn = A.ffn, fld = ffn + 8, nk = d / 32;
+  load_weights(A, smem);
   bf16_t* Xb = reinterpret_cast<bf16_t*>(smem + A.xb);
   bf16_t* Qs = reinterpret_cast<bf16_t*>(smem + A.q);
   bf16_t* Ks = reinterpret_cast<bf16_t*>(smem + A.k);
@@ -348,8 +420,6 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
   bf16_t* Hs = reinterpret_cast<bf16_t*>(smem + A.h);
   float* cvec = reinterpret_cast<float*>(smem + A.cvec);
   float* pool = reinterpret_cast<float*>(smem + A.pool);
-  int* tinfo = reinterpret_cast<int*>(smem + A.tinfo);
-  const uint8_t** rowp = reinterpret_cast<const uint8_t**>(smem + A.rowp);
   const bf16_t* Win = reinterpret_cast<const bf16_t*>(smem + A.win);
   const bf16_t* Wpool = reinterpret_cast<const bf16_t*>(smem + A.wpool);
   bf16_t* kc_wg = A.kcache ? A.kcache + int64_t(blockIdx.x) * A.n_layers * A.tpad * DM : nullptr;
@@ -363,8 +433,13 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
       for (int c = tid; c < 2 * DM; c += NT) out[c] = 0.f;
       continue;
     }
-    // candidate half of the input projection and the pooled maxima
-    if (tid < DM) {   // W_in[:, d:] c + b_in, 8 columns per load
+    // this lane's token of the first block (B operand column c16 of wave w)
+    TokLoad<NK> tl;
+    {
+      const int p = 16 * w + c16;
+      load_token(tl, lane_token(A, n, p, Tv), p, p < Tv, A, nk);
+    }
+    if (tid < DM) {   // candidate half of the input projection: W_in[:, d:] c + b_in
       const uint4* wr = reinterpret_cast<const uint4*>(A.W_in + int64_t(tid) * 2 * d + d);
       const uint4* cr = reinterpret_cast<const uint4*>(A.cand + n * d);
       float acc = A.b_in[tid];
@@ -375,61 +450,43 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
         for (int u = 0; u < 8; ++u) acc = fmaf(float(a[u]), float(b[u]), acc);
       }
       cvec[tid] = acc;
-    } else if (tid < 2 * DM) {
-      pool[tid - DM] = -__builtin_inff();
     }
+    __syncthreads();
+    // running max of X W_pool^T over the wave's valid tokens: lane holds features 16 f + c16
+    float pmax[4] = {-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
     const int nblk = (Tv + BT - 1) / BT;
     for (int blk = 0; blk < nblk; ++blk) {
       const int p0 = blk * BT;
       const int nv = Tv - p0 < BT ? Tv - p0 : BT;   // valid positions of the block
-      // ---- resolve the block's tokens
-      if (tid < BT) {
-        const int p = p0 + tid;
-        const uint8_t* rp = nullptr;
-        int info = 0;
-        if (p < Tv) {
-          const TokenRef t = resolve_token(A.s, n, p, d * 2);
-          rp = t.emb;
-          info = t.act | (t.time << 8);
-        }
-        rowp[tid] = rp;
-        tinfo[tid] = info;
-      }
-      __syncthreads();
+      const int p = p0 + 16 * w + c16;              // this lane's token (B operand column)
       // ---- Eq. 4: X0^T = W_in[:, :d] E^T + cvec + E_act + E_time + E_pos
       f32x4 x[4];
-      {
-        const int tok = 16 * w + c16;          // this lane's token (B operand column)
-        const uint8_t* rp = rowp[tok];
 #pragma unroll
-        for (int f = 0; f < 4; ++f) x[f] = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int k0 = 0; k0 < d; k0 += 32) {
-          bf16x8 b{};
-          if (rp) b = frag(reinterpret_cast<const bf16_t*>(rp) + k0 + 8 * g);
+      for (int f = 0; f < 4; ++f) x[f] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < NK; ++k) {
+        if (k < nk) {
 #pragma unroll
           for (int f = 0; f < 4; ++f)
-            x[f] = mma(frag(Win + (16 * f + c16) * (d + 8) + k0 + 8 * g), b, x[f]);
+            x[f] = mma(frag(Win + (16 * f + c16) * (d + 8) + 32 * k + 8 * g), tl.e[k], x[f]);
         }
-        // D of the transposed product: lane holds token c16 (of the wave's tile),
-        // features 16 f + 4 g + i
-        const int info = tinfo[16 * w + c16];
-        const int act = info & 0xFF, tim = (info >> 8) & 0xFF;
-        const int p = p0 + 16 * w + c16;
-        const bool valid = p < Tv;
-#pragma unroll
-        for (int f = 0; f < 4; ++f) {
-          const int feat = 16 * f + 4 * g;
-          float v[4] = {0.f, 0.f, 0.f, 0.f};
-          if (valid) {
-            add4(v, A.E_act + act * DM + feat);
-            add4(v, A.E_pos + int64_t(p) * DM + feat);
-            if (A.E_time) add4(v, A.E_time + tim * DM + feat);
-          }
-#pragma unroll
-          for (int i = 0; i < 4; ++i) x[f][i] += cvec[feat + i] + v[i];
-        }
-        store_xb(Xb, x);
       }
+      // D of the transposed product: lane holds token c16 of the wave's tile,
+      // features 16 f + 4 g + i
+#pragma unroll
+      for (int f = 0; f < 4; ++f) {
+        const int feat = 16 * f + 4 * g;
+        float v[4] = {cvec[feat], cvec[feat + 1], cvec[feat + 2], cvec[feat + 3]};
+        add4(v, tl.ea[f]);
+        add4(v, tl.ep[f]);
+        add4(v, tl.et[f]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[f][i] += v[i];
+      }
+      store_xb(Xb, x);
+      // the next block's token: its row resolved now, its operands loaded after the
+      // last layer's attention
+      const TokenRef next = blk + 1 < nblk ? lane_token(A, n, p + BT, Tv) : TokenRef{nullptr, 0, 0};
       // ---- layers
       for (int li = 0; li < A.n_layers; ++li) {
         const bf16_t* Wqkv = reinterpret_cast<const bf16_t*>(smem + A.lw[li].qkv);
@@ -440,21 +497,21 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
         bf16_t* kc = kc_wg ? kc_wg + int64_t(li) * A.tpad * DM : nullptr;
         bf16_t* vc = vc_wg ? vc_wg + int64_t(li) * DM * A.tpad : nullptr;
         // Q and K transposed (rows of Wq / Wk as A), V untransposed (X as A)
-        f32x4 qk[8];
+        bf16x8 xf[2];
+        own_rows(xf, Xb);
+        f32x4 qk[8], vv[4];
 #pragma unroll
         for (int f = 0; f < 8; ++f) qk[f] = f32x4{0.f, 0.f, 0.f, 0.f};
-        wt_product<8>(qk, Wqkv, RLD, Xb, RLD, DM);
-        f32x4 vv[4];
 #pragma unroll
         for (int f = 0; f < 4; ++f) vv[f] = f32x4{0.f, 0.f, 0.f, 0.f};
-        {
-          const bf16_t* arow = Xb + (16 * w + c16) * RLD + 8 * g;   // A: the wave's tokens
-          const bf16_t* brow = Wqkv + (2 * DM + c16) * RLD + 8 * g;  // B: W_v rows (columns of V)
-          for (int k0 = 0; k0 < DM; k0 += 32) {
-            const bf16x8 a = frag(arow + k0);
 #pragma unroll
-            for (int f = 0; f < 4; ++f) vv[f] = mma(a, frag(brow + 16 * f * RLD + k0), vv[f]);
-          }
+        for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+          for (int f = 0; f < 8; ++f)
+            qk[f] = mma(frag(Wqkv + (16 * f + c16) * RLD + 32 * kb + 8 * g), xf[kb], qk[f]);
+#pragma unroll
+          for (int f = 0; f < 4; ++f)
+            vv[f] = mma(xf[kb], frag(Wqkv + (2 * DM + 16 * f + c16) * RLD + 32 * kb + 8 * g), vv[f]);
         }
         __syncthreads();   // every wave is past the previous layer's attention (K, V^T reads)
         {
@@ -498,12 +555,20 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
           attend<32>(Qs, Ks, Vts, kc, vc, A.tpad, p0, 0, nv, nm);
           attend<32>(Qs, Ks, Vts, kc, vc, A.tpad, p0, 32, nv, nm);
         }
+        if (li == A.n_layers - 1 && blk + 1 < nblk)
+          load_token(tl, next, p + BT, p + BT < Tv, A, nk);
         // ---- x += O W_o^T + b_o; LayerNorm 1 (the wave's own O rows: no barrier)
         {
+          bf16x8 of[2];
+          own_rows(of, Qs);
           f32x4 o[4];
 #pragma unroll
           for (int f = 0; f < 4; ++f) o[f] = f32x4{0.f, 0.f, 0.f, 0.f};
-          wt_product<4>(o, Wo, RLD, Qs, RLD, DM);
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int f = 0; f < 4; ++f)
+              o[f] = mma(frag(Wo + (16 * f + c16) * RLD + 32 * kb + 8 * g), of[kb], o[f]);
 #pragma unroll
           for (int f = 0; f < 4; ++f)
 #pragma unroll
@@ -513,19 +578,27 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
         }
         // ---- FFN: H = ReLU(x W_1^T + b_1); x += H W_2^T + b_2; LayerNorm 2
         {
+          bf16x8 hf[2];
+          own_rows(hf, Xb);
           for (int f0 = 0; f0 < ffn; f0 += 16) {
-            f32x4 hh[1] = {f32x4{0.f, 0.f, 0.f, 0.f}};
-            wt_product<1>(hh, W1 + f0 * RLD, RLD, Xb, RLD, DM);
+            f32x4 hh = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+              hh = mma(frag(W1 + (f0 + c16) * RLD + 32 * kb + 8 * g), hf[kb], hh);
             const float* b1 = vec + V_B1 + f0 + 4 * g;
-            put4(Hs + (16 * w + c16) * fld + f0 + 4 * g, fmaxf(hh[0][0] + b1[0], 0.f),
-                 fmaxf(hh[0][1] + b1[1], 0.f), fmaxf(hh[0][2] + b1[2], 0.f),
-                 fmaxf(hh[0][3] + b1[3], 0.f));
+            put4(Hs + (16 * w + c16) * fld + f0 + 4 * g, fmaxf(hh[0] + b1[0], 0.f),
+                 fmaxf(hh[1] + b1[1], 0.f), fmaxf(hh[2] + b1[2], 0.f), fmaxf(hh[3] + b1[3], 0.f));
           }
           wave_lds_sync();
           f32x4 o[4];
 #pragma unroll
           for (int f = 0; f < 4; ++f) o[f] = f32x4{0.f, 0.f, 0.f, 0.f};
-          wt_product<4>(o, W2, fld, Hs, fld, ffn);
+          const bf16_t* hrow = Hs + (16 * w + c16) * fld + 8 * g;
+          for (int k0 = 0; k0 < ffn; k0 += 32) {
+            const bf16x8 b = frag(hrow + k0);
+#pragma unroll
+            for (int f = 0; f < 4; ++f) o[f] = mma(frag(W2 + (16 * f + c16) * fld + k0 + 8 * g), b, o[f]);
+          }
 #pragma unroll
           for (int f = 0; f < 4; ++f)
 #pragma unroll
@@ -534,46 +607,66 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
           store_xb(Xb, x);
         }
       }
-      // ---- head: last token's X, running max of X W_pool^T over valid tokens
-      {
-        const int p = p0 + 16 * w + c16;
-        if (p == Tv - 1) {
+      // ---- head: the last token's X; the running max of X W_pool^T over valid tokens
+      if (p == Tv - 1) {
 #pragma unroll
-          for (int f = 0; f < 4; ++f)
-            *reinterpret_cast<float4*>(out + DM + 16 * f + 4 * g) =
-                make_float4(x[f][0], x[f][1], x[f][2], x[f][3]);
-        }
+        for (int f = 0; f < 4; ++f)
+          *reinterpret_cast<float4*>(out + DM + 16 * f + 4 * g) =
+              make_float4(x[f][0], x[f][1], x[f][2], x[f][3]);
+      }
+      {
+        bf16x8 xf[2];
+        own_rows(xf, Xb);
         f32x4 y[4];
 #pragma unroll
         for (int f = 0; f < 4; ++f) y[f] = f32x4{0.f, 0.f, 0.f, 0.f};
-        wt_product<4>(y, Wpool, RLD, Xb, RLD, DM);
-        const bool valid = p < Tv;
 #pragma unroll
-        for (int f = 0; f < 4; ++f)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float m = valid ? y[f][i] : -__builtin_inff();
-#pragma unroll
-            for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, WAVE));
-            y[f][i] = m;   // max over the wave's 16 tokens of feature 16 f + 4 g + i
-          }
-        if (c16 == 0) {
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int f = 0; f < 4; ++f)
+            y[f] = mma(xf[kb], frag(Wpool + (16 * f + c16) * RLD + 32 * kb + 8 * g), y[f]);
+        // D[token][feature]: lane holds feature 16 f + c16 of tokens 16 w + 4 g + i
+        const int t0 = p0 + 16 * w + 4 * g;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) pool[DM + w * DM + 16 * f + 4 * g + i] = y[f][i];
+        for (int f = 0; f < 4; ++f) {
+          float m = -__builtin_inff();
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (t0 + i < Tv) m = fmaxf(m, y[f][i]);
+          m = fmaxf(m, __shfl_xor(m, 16, WAVE));
+          m = fmaxf(m, __shfl_xor(m, 32, WAVE));
+          pmax[f] = fmaxf(pmax[f], m);
         }
       }
-      __syncthreads();
-      if (tid < DM) {
-        float m = pool[tid];
+    }
+    if (g == 0) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) m = fmaxf(m, pool[DM + v * DM + tid]);
-        pool[tid] = m;
-      }
+      for (int f = 0; f < 4; ++f) pool[w * DM + 16 * f + c16] = pmax[f];
     }
     __syncthreads();
-    if (tid < DM) out[tid] = pool[tid] + A.b_pool[tid];
+    if (tid < DM)
+      out[tid] = fmaxf(fmaxf(pool[tid], pool[DM + tid]), fmaxf(pool[2 * DM + tid], pool[3 * DM + tid])) +
+                 A.b_pool[tid];
+  }
+}
+
+// The weights' LDS image: one workgroup per piece (a matrix or a vector).
+struct Seg {
+  const uint8_t* src;
+  int dst, rows, units, src_ld, dst_ld;   // bytes; units of 16 bytes per row
+};
+constexpr int MAX_SEGS = 12 * MAX_LAYERS + 2;
+struct PackArgs {
+  Seg seg[MAX_SEGS];
+  uint8_t* blob;
+};
+__global__ __launch_bounds__(256) void small_pack_kernel(PackArgs P) {
+  const Seg s = P.seg[blockIdx.x];
+  const int n = s.rows * s.units;
+  for (int e = threadIdx.x; e < n; e += 256) {
+    const int r = e / s.units, c = e % s.units;
+    *reinterpret_cast<uint4*>(P.blob + s.dst + int64_t(r) * s.dst_ld + c * 16) =
+        *reinterpret_cast<const uint4*>(s.src + int64_t(r) * s.src_ld + c * 16);
   }
 }
 
@@ -615,14 +708,72 @@ int small_grid(int64_t total, int T, const tav2_weights& w) {
   }
   return int(g > 0 ? g : 1);
 }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// The pieces of the weights' LDS image: every layer matrix and vector, the token
+// half of W_in and W_pool.
+int small_segments(const tav2_weights& w, int d, const sm::Args& a, sm::Seg* seg) {
+  int n = 0;
+  auto add = [&](const void* src, int dst, int rows, int row_bytes, int src_ld, int dst_ld) {
+    seg[n++] = sm::Seg{static_cast<const uint8_t*>(src), dst, rows, row_bytes / 16, src_ld,
+                       dst_ld};
+  };
+  constexpr int DM = sm::DM, RB = sm::RLD * 2;
+  const int ffn = w.d_ffn, fb = (ffn + 8) * 2;
+  for (int l = 0; l < w.n_layers; ++l) {
+    const tav2_layer& L = w.layers[l];
+    const int v = a.lw[l].vec;
+    add(L.W_qkv, a.lw[l].qkv, 3 * DM, DM * 2, DM * 2, RB);
+    add(L.W_o, a.lw[l].o, DM, DM * 2, DM * 2, RB);
+    add(L.W_1, a.lw[l].w1, ffn, DM * 2, DM * 2, RB);
+    add(L.W_2, a.lw[l].w2, DM, ffn * 2, ffn * 2, fb);
+    add(L.b_qkv, v + sm::V_BQKV * 4, 1, 3 * DM * 4, 0, 0);
+    add(L.b_o, v + sm::V_BO * 4, 1, DM * 4, 0, 0);
+    add(L.ln1_g, v + sm::V_LN1G * 4, 1, DM * 4, 0, 0);
+    add(L.ln1_b, v + sm::V_LN1B * 4, 1, DM * 4, 0, 0);
+    add(L.b_1, v + sm::V_B1 * 4, 1, ffn * 4, 0, 0);
+    add(L.b_2, v + sm::v_b2(ffn) * 4, 1, DM * 4, 0, 0);
+    add(L.ln2_g, v + sm::v_ln2g(ffn) * 4, 1, DM * 4, 0, 0);
+    add(L.ln2_b, v + sm::v_ln2b(ffn) * 4, 1, DM * 4, 0, 0);
+  }
+  add(w.W_in, a.win, DM, d * 2, 2 * d * 2, (d + 8) * 2);
+  add(w.W_pool, a.wpool, DM, DM * 2, DM * 2, RB);
+  return n;
+}
 }  // namespace
 
 bool encode_small_supported(int d, const tav2_weights& w) {
   if (w.d_model != sm::DM || w.n_layers > sm::MAX_LAYERS) return false;
   const int dh = w.d_model / w.n_heads;
   if (dh != 32 && dh != 64) return false;
-  if (w.d_ffn % 32 || w.d_ffn > 256 || d % 32 || d > 256) return false;
+  if (w.d_ffn % 32 || w.d_ffn > 256 || d % 32 || d > 32 * sm::MAX_DK) return false;
   return small_args(w, d).lds_bytes <= SM_LDS_MAX;
+}
+
+bool encode_small_aligned(const tav2_weights& w) {
+  if (!aligned16(w.W_in) || !aligned16(w.W_pool) || (reinterpret_cast<uintptr_t>(w.E_act) & 7) ||
+      (reinterpret_cast<uintptr_t>(w.E_pos) & 7) || (reinterpret_cast<uintptr_t>(w.E_time) & 7))
+    return false;
+  for (int l = 0; l < w.n_layers; ++l) {
+    const tav2_layer& L = w.layers[l];
+    if (!aligned16(L.W_qkv) || !aligned16(L.W_o) || !aligned16(L.W_1) || !aligned16(L.W_2))
+      return false;
+  }
+  return true;
+}
+
+size_t encode_small_packed_bytes(const tav2_weights& w) {
+  return size_t(small_args(w, w.d_in).wbytes);
+}
+
+hipError_t launch_encode_small_pack(const tav2_weights& w, void* packed, hipStream_t st) {
+  const sm::Args a = small_args(w, w.d_in);
+  sm::PackArgs P{};
+  const int n = small_segments(w, w.d_in, a, P.seg);
+  P.blob = static_cast<uint8_t*>(packed);
+  ProfScope prof("pack_weights", st);
+  sm::small_pack_kernel<<<unsigned(n), 256, 0, st>>>(P);
+  return hipGetLastError();
 }
 
 size_t encode_small_workspace(int64_t total, int T, const tav2_weights& w) {
@@ -644,6 +795,7 @@ hipError_t launch_encode_small(const TokenSource& src, const void* cand_emb, int
   a.W_pool = static_cast<const bf16_t*>(w.W_pool);
   a.b_pool = w.b_pool;
   for (int i = 0; i < w.n_layers; ++i) a.layers[i] = w.layers[i];
+  a.packed = static_cast<const uint8_t*>(w.packed);
   a.total = total;
   a.tpad = int(small_tpad(src.T));
   a.out = out;
@@ -654,18 +806,22 @@ hipError_t launch_encode_small(const TokenSource& src, const void* cand_emb, int
     a.kcache = static_cast<bf16_t*>(ws);
     a.vcache = reinterpret_cast<bf16_t*>(static_cast<uint8_t*>(ws) + per / 2 * size_t(grid));
   }
-  static std::atomic<bool> done[64] = {};
+  const int nk = src.d / 32;
+  const int which = nk <= 1 ? 0 : nk <= 2 ? 1 : nk <= 4 ? 2 : 3;
+  void (*const kernels[4])(sm::Args) = {sm::encoder_small_kernel<1>, sm::encoder_small_kernel<2>,
+                                         sm::encoder_small_kernel<4>, sm::encoder_small_kernel<8>};
+  static std::atomic<bool> done[64][4] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if (dev >= 0 && dev < 64 && !done[dev].load(std::memory_order_acquire)) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(sm::encoder_small_kernel),
+  if (dev >= 0 && dev < 64 && !done[dev][which].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernels[which]),
                             hipFuncAttributeMaxDynamicSharedMemorySize, SM_LDS_MAX);
     if (e != hipSuccess) return e;
-    done[dev].store(true, std::memory_order_release);
+    done[dev][which].store(true, std::memory_order_release);
   }
   ProfScope prof("encoder_small", st);
-  sm::encoder_small_kernel<<<unsigned(grid), sm::NT, size_t(a.lds_bytes), st>>>(a);
+  hipLaunchKernelGGL(kernels[which], dim3(unsigned(grid)), dim3(sm::NT), size_t(a.lds_bytes), st, a);
   return hipGetLastError();
 }
 

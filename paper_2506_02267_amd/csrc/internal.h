@@ -111,6 +111,9 @@ hipError_t launch_encode_fused(const TokenSource& src, const void* cand_emb, int
 // ---- encoder_small.hip: bf16 encoder for d_model 64 (all layer weights in LDS)
 constexpr int SMALL_UNMASKED_MAX_T = 64;   // the unmasked mode: one 64-position block
 bool encode_small_supported(int d, const tav2_weights& w);
+bool encode_small_aligned(const tav2_weights& w);   // matrices 16-byte, tables 8-byte aligned
+size_t encode_small_packed_bytes(const tav2_weights& w);
+hipError_t launch_encode_small_pack(const tav2_weights& w, void* packed, hipStream_t st);
 size_t encode_small_workspace(int64_t total, int T, const tav2_weights& w);
 hipError_t launch_encode_small(const TokenSource& src, const void* cand_emb, int64_t total,
                                const tav2_weights& w, float* out, void* ws, bool unmasked,

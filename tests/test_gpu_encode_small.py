@@ -111,6 +111,20 @@ def test_paper_workload_select_encode():
     check_workload(synth.PAPER)
 
 
+@pytest.mark.parametrize("kw", [dict(), dict(n_heads=2, d=64)])
+def test_packed_weights_equal_unpacked(kw):
+    """Weights packed once (the kernel's LDS image, loaded by one contiguous copy)
+    give the outputs of the weights read as given, bit for bit."""
+    d = kw.get("d", 32)
+    tb = synth.make_tokens(64, 192, d, seed=4, valid_len=np.random.default_rng(4).integers(0, 193, 64))
+    tok, cand = upload_tokens(tb)
+    W = weights_for(192, **kw)
+    a = T.encode(tok, cand, T.DeviceWeights(W))
+    b = T.encode(tok, cand, T.DeviceWeights(W, pack=True))
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
 def test_repeated_runs_bitwise_identical():
     tb = synth.make_tokens(300, 192, 32, seed=2)
     tok, cand = upload_tokens(tb)
