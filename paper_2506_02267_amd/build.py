@@ -36,7 +36,7 @@ def compile_flags():
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
-# Per-source extra flags.  The fused encoder's and the fused NN search's MFMA
+# Per-source extra flags.  The encoders' and the fused NN search's MFMA
 # results are read by VALU code (softmax, epilogues, LayerNorm, the survivor
 # filter): results kept in VGPRs save one accumulator move per element (and keep
 # the filter's 128 accumulators from being copied out of AGPRs all at once).
@@ -44,6 +44,7 @@ def compile_flags():
 # compiler's default for HIP, stated explicitly).
 EXTRA_FLAGS = {"encoder_fused.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
                "encoder_fused_unmasked.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+               "encoder_small.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
                "select.hip": ["-fhip-fp32-correctly-rounded-divide-sqrt"],
                "select_fused.hip": ["-fhip-fp32-correctly-rounded-divide-sqrt", "-mllvm",
                                     "-amdgpu-mfma-vgpr-form"]}

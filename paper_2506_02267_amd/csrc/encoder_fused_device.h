@@ -112,34 +112,6 @@ __device__ __forceinline__ bf16x8 bias_ones() {
   return __builtin_bit_cast(bf16x8, u32x4{v, 0u, 0u, 0u});
 }
 
-// Partner values across lane halves without LDS: the gfx950 permlane swaps of a
-// register with itself leave {v[l], v[l ^ 32]} (or {v[l], v[l ^ 16]}) in the pair.
-// Maximum without NaN quieting (gfx950 v_maximum3_f32): fmaxf's IEEE semantics
-// make the compiler canonicalize every operand that is not the result of an
-// arithmetic instruction (MFMA results, lane swaps), one extra instruction each.
-// The operands here are finite or -inf.
-__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
-__device__ __forceinline__ float xmax32(float v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
-                                                  false);
-  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float xmax16(float v) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
-                                                  false);
-  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float xsum32(float v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
-                                                  false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-__device__ __forceinline__ float xsum16(float v) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
-                                                  false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 struct LayerPk {        // first fragment of each packed matrix (last k-block: bias)
   int qkv;              // [768 rows][16 + 1 kb]
   int o;                // [256][16 + 1]

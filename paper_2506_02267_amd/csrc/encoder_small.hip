@@ -3,10 +3,11 @@
 // Encoder'; the fused transformer of Sec. 3.4.2 keeps every transformer weight
 // on chip next to the activations).  One workgroup runs Eq. 4's feature
 // encoding, every causal post-LN layer and the linear + max-pool head for one
-// candidate at a time, with all layer weights resident in LDS.
+// candidate at a time, with all layer weights resident in LDS (W_pool in
+// registers).
 //
 // Layout of the work:
-//  * The workgroup is persistent: it loads every weight into LDS once and then
+//  * The workgroup is persistent: it loads every weight on chip once and then
 //    takes candidates blockIdx.x, blockIdx.x + gridDim.x, ...
 //  * A candidate's positions are processed in blocks of 64; under the causal
 //    mask a block depends on earlier blocks only through their keys and values,
@@ -21,8 +22,10 @@
 //    bf16 of one row; V is computed untransposed to give V^T [dim][key], with
 //    each 32-key pair's keys in the order of the P^T fragment.
 //  * Attention: S^T = K Q^T (one query per lane column), online softmax over
-//    32-key pairs in registers, O^T += V^T P^T; keys of earlier blocks are read
-//    from the cache straight into MFMA operands.
+//    32-key pairs in registers, O^T += V^T P^T; keys of earlier blocks come
+//    from the cache through a one-pair LDS stage filled by the whole workgroup.
+//  * The next block's token rows are resolved during the current block and
+//    loaded after its last attention, so Eq. 4 finds them in registers.
 #include <atomic>
 
 #include "common.h"
@@ -36,6 +39,7 @@ constexpr int DM = 64;          // d_model
 constexpr int BT = 64;          // tokens per block
 constexpr int NT = 256;         // threads (4 waves, 16 tokens each)
 constexpr int RLD = DM + 8;     // row stride (bf16) of [*][64] activations and weights
+constexpr int SLD = 32 + 8;     // row stride (bf16) of a staged V^T pair
 constexpr int MAX_LAYERS = 4;
 constexpr int MAX_DK = 8;       // token width d <= 256: at most 8 k-steps of 32 (kernels for 1, 2, 4, 8)
 
@@ -80,7 +84,7 @@ struct Args {
   float* out;                // [total, 2 DM]
   // LDS layout (bytes): the weights' image [0, wbytes), then the activations
   LayerW lw[MAX_LAYERS];
-  int win, wpool, wbytes, xb, q, k, vt, h, cvec, pool, lds_bytes;
+  int win, wbytes, xb, q, k, vt, h, kst, vst, cvec, pool, lds_bytes;
   int unmasked;
 };
 
@@ -100,13 +104,14 @@ __host__ __device__ inline void plan_lds(Args& a) {
     a.lw[l].vec = take((3 * DM + DM + 2 * DM + a.ffn + DM + 2 * DM) * 4);
   }
   a.win = take(DM * (a.d + 8) * 2);
-  a.wpool = take(DM * RLD * 2);
   a.wbytes = off;
   a.xb = take(BT * RLD * 2);
   a.q = take(BT * RLD * 2);    // Q, then the attention output O
   a.k = take(BT * RLD * 2);
   a.vt = take(DM * RLD * 2);   // V^T [dim][key]
   a.h = take(BT * fld * 2);
+  a.kst = take(32 * RLD * 2);  // one 32-key pair of an earlier block: K rows
+  a.vst = take(DM * SLD * 2);  //   and V^T rows
   a.cvec = take(DM * 4);
   a.pool = take(4 * DM * 4);   // one row of pooled maxima per wave
   a.lds_bytes = off;
@@ -139,8 +144,8 @@ __device__ __forceinline__ void copy_floats(float* dst, const float* src, int n)
   for (int e = threadIdx.x; e < n; e += NT) dst[e] = src[e];
 }
 
-// The weights into LDS: the packed image with 8 loads in flight per thread, or
-// matrix by matrix from the caller's layout.
+// The layer weights and W_in's token half into LDS: the packed image with 8
+// loads in flight per thread, or matrix by matrix from the caller's layout.
 __device__ __forceinline__ void load_weights(const Args& A, uint8_t* smem) {
   if (A.packed) {
     const int units = A.wbytes / 16;
@@ -179,7 +184,6 @@ __device__ __forceinline__ void load_weights(const Args& A, uint8_t* smem) {
   }
   // token half of W_in: columns 0 .. d - 1 of [DM][2 d]
   copy_matrix(reinterpret_cast<bf16_t*>(smem + A.win), A.d + 8, A.W_in, DM, A.d, 2 * A.d);
-  copy_matrix(reinterpret_cast<bf16_t*>(smem + A.wpool), RLD, A.W_pool, DM, DM, DM);
 }
 
 // ---------------------------------------------------------------- LayerNorm
@@ -190,8 +194,7 @@ __device__ __forceinline__ void layer_norm(f32x4 (&x)[4], const float* g, const 
   float s = 0.f;
 #pragma unroll
   for (int f = 0; f < 4; ++f) s += (x[f][0] + x[f][1]) + (x[f][2] + x[f][3]);
-  s += __shfl_xor(s, 16, WAVE);
-  s += __shfl_xor(s, 32, WAVE);
+  s = xsum32(xsum16(s));
   const float mean = s * (1.f / DM);
   float v = 0.f;
 #pragma unroll
@@ -201,8 +204,7 @@ __device__ __forceinline__ void layer_norm(f32x4 (&x)[4], const float* g, const 
       const float c = x[f][i] - mean;
       v = fmaf(c, c, v);
     }
-  v += __shfl_xor(v, 16, WAVE);
-  v += __shfl_xor(v, 32, WAVE);
+  v = xsum32(xsum16(v));
   const float rstd = rsqrtf(v * (1.f / DM) + 1e-5f);
 #pragma unroll
   for (int f = 0; f < 4; ++f) {
@@ -307,7 +309,8 @@ __device__ __forceinline__ void load_pair(Pair<DH>& f, const bf16_t* K, int kld,
 // One 32-key pair.  Key j of the pair is visible to the lane's query iff j < lim
 // (32: all).  Before the first visible key the running max is -inf: the
 // exponents then use 0 as reference, which gives zero weights and a zero rescale
-// of the (zero) sums.
+// of the (zero) sums.  exp2 is the hardware instruction (results below 2^-126
+// flush to zero, far under the bf16 resolution of P).
 template <int DH>
 __device__ __forceinline__ void att_pair(Att<DH>& st, const Pair<DH>& f, int lim, float scale_l2) {
   const int g = (threadIdx.x % WAVE) / 16;
@@ -325,15 +328,12 @@ __device__ __forceinline__ void att_pair(Att<DH>& st, const Pair<DH>& f, int lim
     if (4 * g + i >= lim) s[0][i] = -__builtin_inff();
     if (16 + 4 * g + i >= lim) s[1][i] = -__builtin_inff();
   }
-  float mx = -__builtin_inff();
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-    mx = fmaxf(mx, fmaxf(fmaxf(s[t][0], s[t][1]), fmaxf(s[t][2], s[t][3])));
-  mx = fmaxf(mx, __shfl_xor(mx, 16, WAVE));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, WAVE));
-  const float mnew = fmaxf(st.m, mx * scale_l2);
+  float mx = vmax(vmax(vmax(s[0][0], s[0][1]), vmax(s[0][2], s[0][3])),
+                  vmax(vmax(s[1][0], s[1][1]), vmax(s[1][2], s[1][3])));
+  mx = xmax32(xmax16(mx));
+  const float mnew = vmax(st.m, mx * scale_l2);
   const float mref = mnew == -__builtin_inff() ? 0.f : mnew;
-  const float alpha = exp2f(st.m - mref);
+  const float alpha = __builtin_amdgcn_exp2f(st.m - mref);
   st.l *= alpha;
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] *= alpha;
@@ -343,7 +343,7 @@ __device__ __forceinline__ void att_pair(Att<DH>& st, const Pair<DH>& f, int lim
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float p = exp2f(fmaf(s[t][i], scale_l2, -mref));
+      const float p = __builtin_amdgcn_exp2f(fmaf(s[t][i], scale_l2, -mref));
       st.l += p;
       pb[4 * t + i] = static_cast<__bf16>(p);
     }
@@ -351,56 +351,83 @@ __device__ __forceinline__ void att_pair(Att<DH>& st, const Pair<DH>& f, int lim
   for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = mma(f.v[dt], pb, st.o[dt]);
 }
 
-// Attention of the wave's 16 queries (block positions 16 w ..) for one head: the
-// block's own keys 0 .. 16 w + 15 (causal; unmasked: 0 .. nkv - 1) from LDS, then
-// the p0 keys of earlier blocks from the cache, each pair's operands loaded while
-// the previous pair is computed.  Leaves O = softmax(S) V in the Q rows.
+// Attention of the wave's 16 queries (block positions 16 w ..) for every head:
+// the block's own keys 0 .. 16 w + 15 (causal; unmasked: 0 .. nkv - 1) from LDS,
+// then the p0 keys of earlier blocks from the cache, one 32-key pair at a time
+// staged in LDS by the whole workgroup (each key is read from the cache once per
+// workgroup, not once per wave); the loads of the next two pairs are in flight
+// while a pair is computed.  Leaves O = softmax(S) V in the Q rows.
 template <int DH>
 __device__ __forceinline__ void attend(bf16_t* Qs, const bf16_t* Ks, const bf16_t* Vts,
                                        const bf16_t* kc, const bf16_t* vc, int tpad, int p0,
-                                       int col0, int nkv, bool unmasked) {
-  const int lane = threadIdx.x % WAVE, w = threadIdx.x / WAVE;
+                                       int nkv, bool unmasked, bf16_t* Kst, bf16_t* Vst) {
+  constexpr int NH = DM / DH;
+  const int tid = threadIdx.x, lane = tid % WAVE, w = tid / WAVE;
   const int c16 = lane % 16, g = lane / 16;
   constexpr float scale_l2 = (DH == 64 ? 0.125f : 0.17677669529663688f) * 1.4426950408889634f;
   const int npair = p0 / 32;
-  Pair<DH> ca, cb;
-  if (npair > 0) load_pair<DH>(ca, kc, DM, vc, tpad, col0);
-  Att<DH> st;
+  // staging: thread t moves 16 bytes of K (key t / 8) and of V^T (dim t / 4)
+  const int kkey = tid / 8, kcol = 8 * (tid % 8), vdim = tid / 4, vcol = 8 * (tid % 4);
+  auto fetch = [&](uint4& kr, uint4& vr, int c) {
+    if (c < npair) {
+      kr = *reinterpret_cast<const uint4*>(kc + int64_t(c * 32 + kkey) * DM + kcol);
+      vr = *reinterpret_cast<const uint4*>(vc + int64_t(vdim) * tpad + c * 32 + vcol);
+    }
+  };
+  uint4 k0 = make_uint4(0u, 0u, 0u, 0u), v0 = k0, k1 = k0, v1 = k0, k2 = k0, v2 = k0;
+  fetch(k0, v0, 0);
+  fetch(k1, v1, 1);
+  Att<DH> st[NH];
 #pragma unroll
-  for (int kb = 0; kb < DH / 32; ++kb)
-    st.qf[kb] = frag(Qs + (16 * w + c16) * RLD + col0 + 32 * kb + 8 * g);
+  for (int h = 0; h < NH; ++h) {
 #pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  st.m = -__builtin_inff();
-  st.l = 0.f;
+    for (int kb = 0; kb < DH / 32; ++kb)
+      st[h].qf[kb] = frag(Qs + (16 * w + c16) * RLD + h * DH + 32 * kb + 8 * g);
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt) st[h].o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    st[h].m = -__builtin_inff();
+    st[h].l = 0.f;
+  }
   // own block: query 16 w + c16 sees keys <= itself (causal) or < nkv (unmasked)
   const int q = 16 * w + c16;
   const int kend = unmasked ? nkv : 16 * (w + 1);
-  for (int k0 = 0; k0 < kend; k0 += 32) {
-    Pair<DH> f;
-    load_pair<DH>(f, Ks + k0 * RLD, RLD, Vts + k0, RLD, col0);
-    att_pair<DH>(st, f, unmasked ? nkv - k0 : q + 1 - k0, scale_l2);
-  }
-  // earlier blocks: every key visible; two pairs per trip (operands double-buffered)
-  for (int c = 0; c < npair; c += 2) {
-    if (c + 1 < npair)
-      load_pair<DH>(cb, kc + int64_t(c + 1) * 32 * DM, DM, vc + (c + 1) * 32, tpad, col0);
-    att_pair<DH>(st, ca, 32, scale_l2);
-    if (c + 1 < npair) {
-      if (c + 2 < npair)
-        load_pair<DH>(ca, kc + int64_t(c + 2) * 32 * DM, DM, vc + (c + 2) * 32, tpad, col0);
-      att_pair<DH>(st, cb, 32, scale_l2);
+  for (int k0p = 0; k0p < kend; k0p += 32) {
+    const int lim = unmasked ? nkv - k0p : q + 1 - k0p;
+#pragma unroll
+    for (int h = 0; h < NH; ++h) {
+      Pair<DH> f;
+      load_pair<DH>(f, Ks + k0p * RLD, RLD, Vts + k0p, RLD, h * DH);
+      att_pair<DH>(st[h], f, lim, scale_l2);
     }
   }
-  float l = st.l;
-  l += __shfl_xor(l, 16, WAVE);
-  l += __shfl_xor(l, 32, WAVE);
-  const float inv = 1.f / l;
-  // O^T tile dt: lane holds query c16, dims 16 dt + 4 g + i
+  // earlier blocks: every key visible
+  auto step = [&](const uint4& kr, const uint4& vr, uint4& kn, uint4& vn, int c) {
+    __syncthreads();   // every wave is done with the previous pair
+    *reinterpret_cast<uint4*>(Kst + kkey * RLD + kcol) = kr;
+    *reinterpret_cast<uint4*>(Vst + vdim * SLD + vcol) = vr;
+    __syncthreads();
+    fetch(kn, vn, c + 2);
 #pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt)
-    put4(Qs + (16 * w + c16) * RLD + col0 + 16 * dt + 4 * g, st.o[dt][0] * inv,
-         st.o[dt][1] * inv, st.o[dt][2] * inv, st.o[dt][3] * inv);
+    for (int h = 0; h < NH; ++h) {
+      Pair<DH> f;
+      load_pair<DH>(f, Kst, RLD, Vst, SLD, h * DH);
+      att_pair<DH>(st[h], f, 32, scale_l2);
+    }
+  };
+  for (int c = 0; c < npair; c += 3) {
+    step(k0, v0, k2, v2, c);
+    if (c + 1 < npair) step(k1, v1, k0, v0, c + 1);
+    if (c + 2 < npair) step(k2, v2, k1, v1, c + 2);
+  }
+#pragma unroll
+  for (int h = 0; h < NH; ++h) {
+    const float inv = 1.f / xsum32(xsum16(st[h].l));
+    // O^T tile dt: lane holds query c16, dims 16 dt + 4 g + i
+#pragma unroll
+    for (int dt = 0; dt < DH / 16; ++dt)
+      put4(Qs + (16 * w + c16) * RLD + h * DH + 16 * dt + 4 * g, st[h].o[dt][0] * inv,
+           st[h].o[dt][1] * inv, st[h].o[dt][2] * inv, st[h].o[dt][3] * inv);
+  }
   wave_lds_sync();
 }
 
@@ -421,7 +448,15 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
   float* cvec = reinterpret_cast<float*>(smem + A.cvec);
   float* pool = reinterpret_cast<float*>(smem + A.pool);
   const bf16_t* Win = reinterpret_cast<const bf16_t*>(smem + A.win);
-  const bf16_t* Wpool = reinterpret_cast<const bf16_t*>(smem + A.wpool);
+  bf16_t* Kst = reinterpret_cast<bf16_t*>(smem + A.kst);
+  bf16_t* Vst = reinterpret_cast<bf16_t*>(smem + A.vst);
+  // W_pool as B operand fragments (rows 16 f + c16, k = 32 kb + 8 g), held in
+  // registers for the workgroup's lifetime
+  bf16x8 wpf[2][4];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int f = 0; f < 4; ++f) wpf[kb][f] = frag(A.W_pool + (16 * f + c16) * DM + 32 * kb + 8 * g);
   bf16_t* kc_wg = A.kcache ? A.kcache + int64_t(blockIdx.x) * A.n_layers * A.tpad * DM : nullptr;
   bf16_t* vc_wg = A.vcache ? A.vcache + int64_t(blockIdx.x) * A.n_layers * DM * A.tpad : nullptr;
 
@@ -549,12 +584,10 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
         }
         // ---- attention (per head), O into the Q rows of the wave's tokens
         const bool nm = A.unmasked != 0;
-        if (A.dh == 64) {
-          attend<64>(Qs, Ks, Vts, kc, vc, A.tpad, p0, 0, nv, nm);
-        } else {
-          attend<32>(Qs, Ks, Vts, kc, vc, A.tpad, p0, 0, nv, nm);
-          attend<32>(Qs, Ks, Vts, kc, vc, A.tpad, p0, 32, nv, nm);
-        }
+        if (A.dh == 64)
+          attend<64>(Qs, Ks, Vts, kc, vc, A.tpad, p0, nv, nm, Kst, Vst);
+        else
+          attend<32>(Qs, Ks, Vts, kc, vc, A.tpad, p0, nv, nm, Kst, Vst);
         if (li == A.n_layers - 1 && blk + 1 < nblk)
           load_token(tl, next, p + BT, p + BT < Tv, A, nk);
         // ---- x += O W_o^T + b_o; LayerNorm 1 (the wave's own O rows: no barrier)
@@ -624,7 +657,7 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int f = 0; f < 4; ++f)
-            y[f] = mma(xf[kb], frag(Wpool + (16 * f + c16) * RLD + 32 * kb + 8 * g), y[f]);
+            y[f] = mma(xf[kb], wpf[kb][f], y[f]);
         // D[token][feature]: lane holds feature 16 f + c16 of tokens 16 w + 4 g + i
         const int t0 = p0 + 16 * w + 4 * g;
 #pragma unroll
@@ -632,10 +665,8 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
           float m = -__builtin_inff();
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            if (t0 + i < Tv) m = fmaxf(m, y[f][i]);
-          m = fmaxf(m, __shfl_xor(m, 16, WAVE));
-          m = fmaxf(m, __shfl_xor(m, 32, WAVE));
-          pmax[f] = fmaxf(pmax[f], m);
+            if (t0 + i < Tv) m = vmax(m, y[f][i]);
+          pmax[f] = vmax(pmax[f], xmax32(xmax16(m)));
         }
       }
     }
@@ -645,7 +676,7 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
     }
     __syncthreads();
     if (tid < DM)
-      out[tid] = fmaxf(fmaxf(pool[tid], pool[DM + tid]), fmaxf(pool[2 * DM + tid], pool[3 * DM + tid])) +
+      out[tid] = vmax(vmax(pool[tid], pool[DM + tid]), vmax(pool[2 * DM + tid], pool[3 * DM + tid])) +
                  A.b_pool[tid];
   }
 }
@@ -655,7 +686,7 @@ struct Seg {
   const uint8_t* src;
   int dst, rows, units, src_ld, dst_ld;   // bytes; units of 16 bytes per row
 };
-constexpr int MAX_SEGS = 12 * MAX_LAYERS + 2;
+constexpr int MAX_SEGS = 12 * MAX_LAYERS + 1;
 struct PackArgs {
   Seg seg[MAX_SEGS];
   uint8_t* blob;
@@ -710,8 +741,8 @@ int small_grid(int64_t total, int T, const tav2_weights& w) {
 }
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
-// The pieces of the weights' LDS image: every layer matrix and vector, the token
-// half of W_in and W_pool.
+// The pieces of the weights' LDS image: every layer matrix and vector and the
+// token half of W_in.
 int small_segments(const tav2_weights& w, int d, const sm::Args& a, sm::Seg* seg) {
   int n = 0;
   auto add = [&](const void* src, int dst, int rows, int row_bytes, int src_ld, int dst_ld) {
@@ -737,7 +768,6 @@ int small_segments(const tav2_weights& w, int d, const sm::Args& a, sm::Seg* seg
     add(L.ln2_b, v + sm::v_ln2b(ffn) * 4, 1, DM * 4, 0, 0);
   }
   add(w.W_in, a.win, DM, d * 2, 2 * d * 2, (d + 8) * 2);
-  add(w.W_pool, a.wpool, DM, DM * 2, DM * 2, RB);
   return n;
 }
 }  // namespace

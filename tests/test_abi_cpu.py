@@ -225,17 +225,17 @@ def test_encode_argument_errors(case, status):
 def test_small_encoder_queries():
     """d_model 64 (bf16): the packed form is the kernel's LDS image of the weights
     (per layer: W_qkv, W_o and W_1 in rows of 72 bf16, W_2 in rows of FFN + 8, the
-    eight vectors in fp32; then W_in's token half in rows of d + 8 and W_pool); a workspace of
+    eight vectors in fp32; then W_in's token half in rows of d + 8); a workspace of
     per-workgroup K / V caches past one 64-position block (layers x 2 x T padded
     to 64 x d_model bf16 per workgroup, one workgroup per candidate up to 256);
     the shapes whose weights outgrow the on-chip memory are unsupported."""
     lib = T.load_library()
     w = fake_weights(d=32, dm=64, heads=1, ffn=32, layers=2, max_pos=2048)
     per_layer = (3 * 64 * 72 + 64 * 72 + 32 * 72 + 64 * 40) * 2 + (9 * 64 + 32) * 4
-    image = 2 * per_layer + 64 * 40 * 2 + 64 * 72 * 2
+    image = 2 * per_layer + 64 * 40 * 2
     assert lib.tav2_pack_weights_bytes(ctypes.byref(w)) == -(-image // 256) * 256
-    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10, T=64,
-                   d=32, dtype=T.BF16, reserved=0)
+    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10,
+                   T=64, d=32, dtype=T.BF16, reserved=0)
     assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == 0
     tok.T = 192
     assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(w)) == 10 * 2 * 2 * 192 * 64 * 2

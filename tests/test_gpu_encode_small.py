@@ -24,8 +24,9 @@ def weights_for(T_, d=32, n_heads=1, d_ffn=32, n_layers=2, has_time=True, seed=N
 
 
 def ragged_lengths(total, T_, rng):
-    """Valid lengths over [0, T_] with the block edges (63, 64, 65, ...) and the
-    extremes (0, 1, T_) present."""
+    """Valid lengths over [0, T_] with the edges of 64-position steps (63, 64, 65,
+    127, 128, 129, ...: the encoder's blocks are 64 positions, its key pairs 32)
+    and the extremes (0, 1, T_) present."""
     edges = [0, 1, T_]
     for e in range(64, T_ + 1, 64):
         edges += [e - 1, e, e + 1]
@@ -59,12 +60,14 @@ def test_paper_shape_ragged(T_, total):
     run_and_check(tb, weights_for(T_))
 
 
-@pytest.mark.parametrize("case", ["two_heads", "one_layer_ffn128_d64", "no_time_d64",
+@pytest.mark.parametrize("case", ["two_heads", "one_layer_ffn96", "no_time_d64",
                                   "two_heads_one_layer_d256"])
 def test_other_shapes(case):
-    T_ = 160
+    """Two heads of 32; an FFN wider than 64 (its hidden rows in a region of their
+    own); d 64 without the time feature; d 256."""
+    T_ = 300
     kw = {"two_heads": dict(n_heads=2),
-          "one_layer_ffn128_d64": dict(n_layers=1, d_ffn=128, d=64),
+          "one_layer_ffn96": dict(n_layers=1, d_ffn=96),
           "no_time_d64": dict(d=64, has_time=False),
           "two_heads_one_layer_d256": dict(n_heads=2, n_layers=1, d=256)}[case]
     print(f"encode_small {case}", flush=True)
