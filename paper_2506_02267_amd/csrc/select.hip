@@ -272,7 +272,7 @@ __global__ __launch_bounds__(TK_THREADS) void topk_kernel(
     float* __restrict__ out_score, int out_ld, int32_t* __restrict__ cand_req) {
   __shared__ int red[2][TK_THREADS / WAVE];
   __shared__ uint64_t scan_w[(TK_THREADS / WAVE) * 5];
-  __shared__ uint64_t sel[TAV2_K_MAX];
+  __shared__ __attribute__((aligned(16))) uint64_t sel[TAV2_K_MAX];
 
   const int r = blockIdx.y;
   const int64_t n = cand_off[r] + blockIdx.x;
@@ -445,7 +445,7 @@ __global__ __launch_bounds__(TS_THREADS) void topk_stream_kernel(
     float* __restrict__ out_score, int out_ld, int32_t* __restrict__ cand_req) {
   __shared__ int red[2][TS_NW];
   __shared__ uint64_t scan_w[TS_NW];
-  __shared__ uint64_t sel[TAV2_K_MAX];
+  __shared__ __attribute__((aligned(16))) uint64_t sel[TAV2_K_MAX];
   __shared__ uint64_t cand[TK_CAP];
   __shared__ uint32_t hist[256];
   __shared__ int misc[4];   // radix digit, rest, selected count, appended count

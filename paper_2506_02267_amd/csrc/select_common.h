@@ -122,19 +122,24 @@ __device__ __forceinline__ uint64_t radix_select48(const uint64_t* v, int cnt, i
   return pre;
 }
 
-// The kk distinct selection values sel[] (LDS, any order) to their ranks in the
-// order: out_idx[rank] = row, out_score[rank] = score.  The rank of a value is the
-// number of larger values (each thread's LDS reads are the same address across
-// the wave: broadcasts).
+// The kk distinct selection values sel[] (LDS, any order, 16-byte aligned) to
+// their ranks in the order: out_idx[rank] = row, out_score[rank] = score.  The
+// rank of a value is the number of larger values (each thread reads the list
+// two values per 16-byte LDS read, the same address across the wave: broadcasts).
 template <int NT>
 __device__ __forceinline__ void place_by_rank(const uint64_t* sel, int kk, int32_t* oi, float* os) {
+  const uint4* s2 = reinterpret_cast<const uint4*>(sel);
   for (int s = threadIdx.x; s < kk; s += NT) {
     const uint64_t me = sel[s];
     int rank = 0;
     int t = 0;
     for (; t + 8 <= kk; t += 8) {
 #pragma unroll
-      for (int u = 0; u < 8; ++u) rank += sel[t + u] > me ? 1 : 0;
+      for (int u = 0; u < 4; ++u) {
+        const uint4 v = s2[t / 2 + u];
+        rank += (uint64_t(v.y) << 32 | v.x) > me ? 1 : 0;
+        rank += (uint64_t(v.w) << 32 | v.z) > me ? 1 : 0;
+      }
     }
     for (; t < kk; ++t) rank += sel[t] > me ? 1 : 0;
     oi[rank] = sel_row(me);

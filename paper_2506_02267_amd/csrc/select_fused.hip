@@ -381,12 +381,14 @@ __host__ __device__ __forceinline__ int filter_region(int nc, int d) {
 // bf16: workgroup = 128 candidates x 256 rows, wave w rows 64 w .. +63.  A lane
 // holds candidates l % 32 + 32 a (a = 0..3) for 32 of the wave's rows (half
 // l / 32 of every 8-row group), so its survivors go to its own LDS segments, one
-// per (candidate, wave, half), each with a lane-private counter: the hot loop
-// has one compare per score and no cross-lane step.  A segment keeps FS_LSEG
-// survivors (the expected count is about one); more go straight to the
-// candidate's list in memory.  Scores are compared as floats with the
-// threshold's value (keys and floats are ordered alike), and staged as raw bits
-// with their row.
+// per (candidate, wave, half), each with a lane-private counter.  The hot loop is
+// branch-free: every score is written, to the segment's next slot when it
+// survives and to the segment's last slot (never read) when it does not, and the
+// counter advances by the compare's result.  A segment keeps FS_LSEG - 1
+// survivors (the expected count is about one); a lane with more goes through
+// its scores again and sends the rest straight to the candidate's list in
+// memory.  Scores are compared as floats with the threshold's value (keys and
+// floats are ordered alike), and staged as raw bits with their row.
 constexpr int FS_LSEG = 8;
 constexpr int FS_NSEG = FB_CANDS * 4 * 2;   // (candidate, wave, half)
 __host__ __device__ __forceinline__ int filter_bf16_lds(int d) {
@@ -439,55 +441,80 @@ __global__ __launch_bounds__(256) void fsel_filter_bf16(FusedArgs A) {
   if (active)
     bf16_products<4, FS_FILTER_D>(ctile + l32 * cld + 8 * hf, cld, brow0, brow1, d / 16, bq, acc);
   __syncthreads();   // the candidate tile's region now stages survivors
+  // segment of (candidate 32 a + l32, wave w, half hf): lane-consecutive, and the
+  // stage slot-major, so that a wave's 64 slot writes are one contiguous 512 bytes
+  constexpr uint32_t KEEP = FS_LSEG - 1;   // survivors a segment keeps
+  auto seg_of = [](int a, int wv, int l, int h) { return ((a * 4 + wv) * 32 + l) * 2 + h; };
   uint32_t cnt[4] = {0u, 0u, 0u, 0u};
   if (active) {
+    // register 4 j + i of row tile b holds row row0 + 32 b + 8 j + 4 hf + i
+    uint32_t rowok[2] = {0u, 0u};
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int reg = 0; reg < 16; ++reg)
+        rowok[b] |= uint32_t(row0 + 32 * b + 8 * (reg / 4) + 4 * hf + (reg % 4) < L) << reg;
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
       const int c = 32 * a + l32;
       const float t = thr_f[c];
-      uint2* seg = stage + ((c * 4 + w) * 2 + hf) * FS_LSEG;
+      uint2* seg = stage + seg_of(a, w, l32, hf);
+      uint32_t m = 0;
 #pragma unroll
       for (int b = 0; b < 2; ++b)
 #pragma unroll
         for (int reg = 0; reg < 16; ++reg) {
           const float sc = acc[a][b][reg];
+          const bool keep = sc >= t && ((rowok[b] >> reg) & 1u);
           const int row = row0 + 32 * b + 8 * (reg / 4) + 4 * hf + (reg % 4);
-          if (sc >= t && row < L) {
-            if (cnt[a] < uint32_t(FS_LSEG)) {
-              seg[cnt[a]] = make_uint2(uint32_t(row), __float_as_uint(sc));
-            } else {
-              const int64_t n = n0 + c;
-              const uint32_t gp = atomicAdd(&A.cnt[n], 1u);
-              if (gp < uint32_t(A.cap)) A.surv[n * A.cap + gp] = sel_value(score_key(sc), row);
-            }
-            ++cnt[a];
-          }
+          seg[(keep ? min(m, KEEP) : KEEP) * FS_NSEG] = make_uint2(uint32_t(row), __float_as_uint(sc));
+          m += keep ? 1u : 0u;
         }
+      cnt[a] = m;
+      if (m > KEEP) {   // rare: the survivors past the segment's slots go to memory
+        uint32_t q = 0;
+        const int64_t n = n0 + c;
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int reg = 0; reg < 16; ++reg) {
+            const float sc = acc[a][b][reg];
+            if (sc >= t && ((rowok[b] >> reg) & 1u)) {
+              if (q >= KEEP) {
+                const int row = row0 + 32 * b + 8 * (reg / 4) + 4 * hf + (reg % 4);
+                const uint32_t gp = atomicAdd(&A.cnt[n], 1u);
+                if (gp < uint32_t(A.cap)) A.surv[n * A.cap + gp] = sel_value(score_key(sc), row);
+              }
+              ++q;
+            }
+          }
+      }
     }
   }
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
-    scnt[((32 * a + l32) * 4 + w) * 2 + hf] = min(cnt[a], uint32_t(FS_LSEG));
+  for (int a = 0; a < 4; ++a) scnt[seg_of(a, w, l32, hf)] = min(cnt[a], KEEP);
   __syncthreads();
-  if (tid < FB_CANDS) {   // one counter update per candidate; segment offsets
+  if (tid < FB_CANDS) {   // one counter update per candidate; its segments' offsets
+    const int a = tid / 32, l = tid % 32;
     uint32_t m = 0;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      soff[tid * 8 + q] = m;
-      m += scnt[tid * 8 + q];
+      const int sg = seg_of(a, q / 2, l, q % 2);
+      soff[sg] = m;
+      m += scnt[sg];
     }
     const uint32_t base = m ? atomicAdd(&A.cnt[n0 + tid], m) : 0u;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) soff[tid * 8 + q] += base;
+    for (int q = 0; q < 8; ++q) soff[seg_of(a, q / 2, l, q % 2)] += base;
   }
   __syncthreads();
 #pragma unroll
-  for (int q = 0; q < FS_NSEG / 256; ++q) {   // segment tid + 256 q: candidate seg / 8
+  for (int q = 0; q < FS_NSEG / 256; ++q) {   // segment sg = tid + 256 q
     const int sg = tid + 256 * q;
     const uint32_t m = scnt[sg], base = soff[sg];
-    const int64_t n = n0 + sg / 8;
+    const int64_t n = n0 + 32 * (sg / 256) + (sg / 2) % 32;
     for (uint32_t i = 0; i < m; ++i) {
-      const uint2 e = stage[sg * FS_LSEG + i];
+      const uint2 e = stage[i * FS_NSEG + sg];
       if (base + i < uint32_t(A.cap))
         A.surv[n * A.cap + base + i] = sel_value(score_key(__uint_as_float(e.y)), int(e.x));
     }
@@ -568,7 +595,7 @@ __global__ __launch_bounds__(FT_THREADS) void fsel_select(FusedArgs A, int32_t* 
                                                           float* __restrict__ out_score,
                                                           int32_t* __restrict__ cand_req) {
   __shared__ uint64_t vals[FS_CAP_MAX];
-  __shared__ uint64_t sel[TAV2_K_MAX];
+  __shared__ __attribute__((aligned(16))) uint64_t sel[TAV2_K_MAX];
   __shared__ uint32_t hist[256];
   __shared__ int misc[4];
   __shared__ unsigned long long common[2];
