@@ -293,7 +293,8 @@ def main():
     ap.add_argument("--workload", default="single_bf16",
                     help="tiny_f32 | single_bf16 | ragged_bf16 | mixed_bf16 | stress_bf16 | "
                          "select_i8 (the NN search alone over int8 codes) | eq2_bf16 (all four "
-                         "parts of Eq. 2) | paper_bf16 (the paper's production encoder)")
+                         "parts of Eq. 2) | paper_bf16 (the paper's production encoder) | "
+                         "paper_i8 (the same on int8 code storage)")
     ap.add_argument("--cpu-budget", type=float, default=20.0,
                     help="seconds of oracle work in the CPU baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -323,7 +324,7 @@ def main():
 
     w = synth.BY_NAME[args.workload]
     inp = synth.make_inputs(w)
-    select_only = w.dtype == "i8"
+    select_only = not w.encode
     eq2 = w.k_rt > 0 or w.k_imp > 0 or w.rt_keep >= 0
     W = None if select_only else synth.make_weights(w)
     dt = {"bf16": T.BF16, "i8": T.I8}.get(w.dtype, T.F32)
@@ -494,9 +495,11 @@ def main():
             "unit": "candidates/s", "n_gpus": 1,
             "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-            "dtype": {"bf16": "bf16", "i8": "i8"}.get(w.dtype, "f32"),
+            "dtype": "i8" if select_only else ("f32" if w.dtype == "f32" else "bf16"),
             "data": ("synthetic (seeded int8 codes of random unit rows, 1/8-grid candidates)"
                      if select_only else
+                     "synthetic (seeded int8 codes of random unit rows, 1/8-grid candidates, "
+                     "N(0,0.02) weights)" if w.dtype == "i8" else
                      "synthetic (seeded 1/8-grid embeddings, N(0,0.02) weights)"),
             "config": config, "roofline": roof, "e2e_frac": round(e2e_frac, 4),
             "e2e_roofline_us": round(roof_s * 1e6, 2), "stages": stages, "cpu_baseline": cpu}

@@ -135,7 +135,7 @@ def select_encode(inputs, W, k, only=None, chunk=32, causal=True):
 
     Returns idx, score (as nn_select_batch) and out [total, 2 d_model] float64.
     """
-    from .nn_select import nn_select_batch, gather_tokens
+    from .nn_select import nn_select_batch, gather_tokens, dequantise
     idx, score = nn_select_batch(inputs.seq, inputs.cand, inputs.cand_offset, k, only=only)
     T = k + (0 if inputs.rt is None else int(inputs.rt.length.max()))
     creq = np.empty(inputs.cand.shape[0], dtype=np.int32)
@@ -144,6 +144,8 @@ def select_encode(inputs, W, k, only=None, chunk=32, causal=True):
     ids = np.arange(inputs.cand.shape[0]) if only is None else np.asarray(only, dtype=np.int64)
     tok_emb, tok_act, tok_time, valid = gather_tokens(inputs.seq, inputs.rt, creq[ids],
                                                       idx[ids], T)
+    if inputs.seq.emb.dtype == np.int8:   # int8 storage: the encoder takes the values
+        tok_emb = dequantise(tok_emb)
     out_ids = encode(tok_emb, tok_act, tok_time, valid, inputs.cand[ids], W, chunk=chunk,
                      causal=causal)
     out = np.zeros((inputs.cand.shape[0], 2 * W.d_model), dtype=np.float64)
@@ -161,7 +163,7 @@ def select_encode_eq2(inputs, W, only=None, chunk=32, causal=True):
     then S_imp rows; -1 padded), score of the same shape (float32, -inf padded)
     and out [total, 2 d_model] float64.
     """
-    from .nn_select import nn_select_batch, eq2_tokens
+    from .nn_select import nn_select_batch, eq2_tokens, dequantise
     w = inputs.w
     k, r = w.k, w.r
     k_rt = w.k_rt if inputs.rt is not None else 0
@@ -183,6 +185,8 @@ def select_encode_eq2(inputs, W, only=None, chunk=32, causal=True):
     tok_emb, tok_act, tok_time, valid, _ = eq2_tokens(
         inputs.seq, inputs.rt, inputs.imp, creq[ids], idx_ll[ids], r, pick(idx_rt),
         pick(idx_imp), w.T)
+    if inputs.seq.emb.dtype == np.int8:
+        tok_emb = dequantise(tok_emb)
     out = np.zeros((total, 2 * W.d_model), dtype=np.float64)
     out[ids] = encode(tok_emb, tok_act, tok_time, valid, inputs.cand[ids], W, chunk=chunk,
                       causal=causal)

@@ -61,6 +61,14 @@ def rank_order(s: np.ndarray) -> np.ndarray:
     return np.argsort(-s, axis=1, kind="stable")
 
 
+def dequantise(Q: np.ndarray) -> np.ndarray:
+    """Embedding values of int8 codes (Sec. 3.2.1): the affine quantisation maps e
+    to round(e / 0.65 * 127) clamped to [-127, 127], so a code q stands for
+    q * 0.65 / 127.  float64.  (The paper dequantises into fp16; the encoder
+    here takes the value in exact arithmetic.)"""
+    return np.asarray(Q, dtype=np.float64) * (0.65 / 127.0)
+
+
 def normalised_scores(Q: np.ndarray, C: np.ndarray) -> np.ndarray:
     """Scores over the int8 sequence storage with dequantisation and L2
     normalisation (Sec. 3.4.2, fused sequence dequantisation; codes of Sec. 3.2.1).

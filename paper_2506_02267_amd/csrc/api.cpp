@@ -195,7 +195,10 @@ tav2_status check_select_encode(const tav2_seq* seq, const Sources& src, const t
                                 int k, const tav2_weights* w, uint32_t flags, int* T_out) {
   tav2_status st;
   if ((st = check_seq(seq, true)) || (st = check_cands(cands, seq)) || (st = check_k(k))) return st;
-  if (seq->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;
+  // int8 codes feed the d_model-64 encoder (bf16 weights) only
+  const bool codes = seq->dtype == TAV2_I8;
+  if (codes && (!w || w->dtype != TAV2_BF16)) return w ? TAV2_ERR_DTYPE : TAV2_ERR_NULL;
+  if (codes && !encode_small_supported(seq->d, *w)) return TAV2_ERR_UNSUPPORTED;
   if (src.r < 0 || src.k_rt < 0 || src.k_imp < 0) return TAV2_ERR_SHAPE;
   if (src.k_rt > TAV2_K_MAX || src.k_imp > TAV2_K_MAX) return TAV2_ERR_SHAPE;
   if ((src.k_rt > 0 || src.r > 0) && !src.rt) return TAV2_ERR_NULL;
@@ -205,7 +208,9 @@ tav2_status check_select_encode(const tav2_seq* seq, const Sources& src, const t
   const int64_t T = int64_t(k) + (src.rt ? std::min(src.r, src.rt->max_len) : 0) + src.k_rt +
                     src.k_imp;
   if (T > TAV2_T_MAX) return TAV2_ERR_SHAPE;
-  if ((st = check_weights(w, seq->d, seq->dtype, int(T), seq->time_bucket != nullptr))) return st;
+  if ((st = check_weights(w, seq->d, codes ? TAV2_BF16 : seq->dtype, int(T),
+                          seq->time_bucket != nullptr)))
+    return st;
   if ((st = check_flags(flags, w, int(T)))) return st;
   *T_out = int(T);
   return TAV2_OK;
@@ -282,6 +287,7 @@ tav2_status select_encode(const tav2_seq* seq, const Sources& src, const tav2_ca
     return TAV2_ERR_HIP;
   TokenSource ts{};
   ts.explicit_tokens = false;
+  ts.codes = seq->dtype == TAV2_I8;
   ts.seq_emb = seq->emb;
   ts.seq_act = seq->action_type;
   ts.seq_time = seq->time_bucket;
@@ -372,7 +378,8 @@ tav2_status tav2_gather(const tav2_seq* seq, const tav2_seq* rt, const tav2_cand
 
 size_t tav2_encode_workspace(const tav2_tokens* tok, const tav2_weights* w) {
   if (!tok || !w) return 0;
-  if (check_weights(w, tok->d, tok->dtype, tok->T, tok->time_bucket != nullptr)) return 0;
+  const int dt = tok->dtype == TAV2_I8 ? TAV2_BF16 : tok->dtype;   // codes: bf16 weights
+  if (check_weights(w, tok->d, dt, tok->T, tok->time_bucket != nullptr)) return 0;
   return encode_ws_bytes(tok->total, tok->T, w);
 }
 
@@ -403,11 +410,16 @@ tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2
                         uint32_t flags, float* out, void* ws, size_t ws_bytes, void* stream) {
   if (!tok || !w) return TAV2_ERR_NULL;
   tav2_status st;
-  if (tok->dtype == TAV2_I8) return TAV2_ERR_UNSUPPORTED;   // codes are for the NN search
-  if ((st = check_dtype(tok->dtype))) return st;
+  // int8 codes feed the d_model-64 encoder (bf16 weights) only
+  const bool codes = tok->dtype == TAV2_I8;
+  if (codes && w->dtype != TAV2_BF16) return TAV2_ERR_DTYPE;
+  if (!codes && (st = check_dtype(tok->dtype))) return st;
   if (tok->total < 0 || tok->d < 16 || tok->d > 512 || tok->d % 16) return TAV2_ERR_SHAPE;
   if (tok->total > (int64_t(1) << 31) - 1) return TAV2_ERR_UNSUPPORTED;
-  if ((st = check_weights(w, tok->d, tok->dtype, tok->T, tok->time_bucket != nullptr))) return st;
+  if (codes && !encode_small_supported(tok->d, *w)) return TAV2_ERR_UNSUPPORTED;
+  if ((st = check_weights(w, tok->d, codes ? TAV2_BF16 : tok->dtype, tok->T,
+                          tok->time_bucket != nullptr)))
+    return st;
   if ((st = check_flags(flags, w, tok->T))) return st;
   if (tok->total == 0) return TAV2_OK;
   if (!tok->emb || !tok->action_type || !tok->valid_len || !cand_emb || !out) return TAV2_ERR_NULL;
@@ -415,6 +427,7 @@ tav2_status tav2_encode(const tav2_tokens* tok, const void* cand_emb, const tav2
   if ((st = check_ws(ws, ws_bytes, encode_ws_bytes(tok->total, tok->T, w)))) return st;
   TokenSource src{};
   src.explicit_tokens = true;
+  src.codes = codes;
   src.tok_emb = tok->emb;
   src.tok_act = tok->action_type;
   src.tok_time = tok->time_bucket;

@@ -250,19 +250,31 @@ struct TokLoad {
 };
 __device__ __forceinline__ TokenRef lane_token(const Args& A, int64_t n, int p, int Tv) {
   TokenRef t{nullptr, 0, 0};
-  if (p < Tv) t = resolve_token(A.s, n, p, A.d * 2);
+  if (p < Tv) t = resolve_token(A.s, n, p, A.s.codes ? A.d : A.d * 2);
   return t;
+}
+// 8 int8 codes as bf16 (exact: |q| <= 127).
+__device__ __forceinline__ bf16x8 codes8(uint2 raw) {
+  bf16x8 v;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    v[j] = static_cast<__bf16>(float(int8_t(((j < 4 ? raw.x : raw.y) >> (8 * (j & 3))) & 0xFF)));
+  return v;
 }
 template <int NK>
 __device__ __forceinline__ void load_token(TokLoad<NK>& L, const TokenRef& t, int p, bool valid,
                                            const Args& A, int nk) {
   const int g = (threadIdx.x % WAVE) / 16;
-  const bf16_t* row = reinterpret_cast<const bf16_t*>(t.emb);
-  const bool have = valid && row != nullptr;
+  const bool have = valid && t.emb != nullptr;
 #pragma unroll
   for (int k = 0; k < NK; ++k) {
     L.e[k] = bf16x8{};
-    if (have && k < nk) L.e[k] = frag(row + 32 * k + 8 * g);
+    if (have && k < nk) {
+      if (A.s.codes)   // int8 codes: dequantised after the product (Eq. 4 in the kernel)
+        L.e[k] = codes8(*reinterpret_cast<const uint2*>(t.emb + 32 * k + 8 * g));
+      else
+        L.e[k] = frag(reinterpret_cast<const bf16_t*>(t.emb) + 32 * k + 8 * g);
+    }
   }
 #pragma unroll
   for (int f = 0; f < 4; ++f) {
@@ -507,7 +519,12 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
         }
       }
       // D of the transposed product: lane holds token c16 of the wave's tile,
-      // features 16 f + 4 g + i
+      // features 16 f + 4 g + i.  int8 codes: the product of the codes times the
+      // scale 0.65 / 127 of their quantisation (Sec. 3.2.1) is that of the values.
+      if (A.s.codes) {
+#pragma unroll
+        for (int f = 0; f < 4; ++f) x[f] *= 0.65f / 127.f;
+      }
 #pragma unroll
       for (int f = 0; f < 4; ++f) {
         const int feat = 16 * f + 4 * g;

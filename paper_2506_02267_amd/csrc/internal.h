@@ -88,6 +88,7 @@ struct TokenSource {
   int T;
   int d;
   bool explicit_tokens;
+  bool codes;   // rows are int8 codes (d bytes each); the encoder dequantises them
 };
 
 // The view S_RT[r:] of a sequence batch: off_out[q] = off[q] + min(r, len[q]),

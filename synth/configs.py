@@ -40,6 +40,7 @@ class Workload:
     k_rt: int = 0
     imp_len: int = 0
     k_imp: int = 0
+    encode: bool = True           # the encoder follows the NN search
 
     @property
     def r(self) -> int:
@@ -84,7 +85,7 @@ WORKLOADS = {w.cid: w for w in (TINY, SINGLE, RAGGED, MIXED, STRESS)}
 # one request of the single workload's size.  The encoder fields are unused.
 SELECT_I8 = Workload(6, "select_i8", "i8", R=1, L=16384, L_range=None, d=32, N=1000, k=256,
                      d_model=256, n_heads=4, d_ffn=1024, n_layers=2, has_time=True,
-                     tie_frac=0.01)
+                     tie_frac=0.01, encode=False)
 # The whole of Eq. 2 (Sec. 3.2.2): NN(S_LL, c) + S_RT[:r] + NN(S_RT[r:], c) +
 # NN(S_imp, c), with real-time and impression sequences of O(10^2) actions; the
 # single workload's lifelong sequence, candidates and encoder.
@@ -97,7 +98,13 @@ EQ2 = Workload(7, "eq2_bf16", "bf16", R=1, L=16384, L_range=None, d=256, N=1000,
 # positions are the top-128 NN tokens and 64 real-time actions.
 PAPER = Workload(8, "paper_bf16", "bf16", R=1, L=16384, L_range=None, d=32, N=256, k=128,
                  d_model=64, n_heads=1, d_ffn=32, n_layers=2, has_time=True, rt_len=64)
-BY_NAME = {w.name: w for w in list(WORKLOADS.values()) + [SELECT_I8, EQ2, PAPER]}
+# The paper's production path end to end: the lifelong and real-time sequences
+# stored as 32-d int8 codes (Sec. 3.2.1), the NN search with fused dequantisation
+# and L2 normalisation (Sec. 3.4.2), and the production encoder on the
+# dequantised rows.
+PAPER_I8 = Workload(9, "paper_i8", "i8", R=1, L=16384, L_range=None, d=32, N=256, k=128,
+                    d_model=64, n_heads=1, d_ffn=32, n_layers=2, has_time=True, rt_len=64)
+BY_NAME = {w.name: w for w in list(WORKLOADS.values()) + [SELECT_I8, EQ2, PAPER, PAPER_I8]}
 
 
 def scaled(w: Workload, **changes) -> Workload:

@@ -14,9 +14,11 @@ Recipe (every draw from one numpy PCG64 stream):
     (row 0 is the most recent action, so its age bucket is the smallest);
   * tie injection: a fraction of rows per request is overwritten by a copy of
     another uniformly chosen row, so the pair ties for every candidate;
+  * int8 workloads: every sequence (lifelong, real-time, impression) holds the
+    int8 codes of random unit rows (int8_codes); candidates stay on the grid;
   * weights: N(0, 0.02) for every matrix, table and bias; LayerNorm gains
-    1 + N(0, 0.02) and offsets N(0, 0.02).  For bf16 workloads matrices and
-    embedding tables are rounded to bf16 (round to nearest even); biases and
+    1 + N(0, 0.02) and offsets N(0, 0.02).  For bf16 and int8 workloads matrices
+    and embedding tables are rounded to bf16 (round to nearest even); biases and
     LayerNorm parameters stay fp32.
 
 Matrices use the [out_features, in_features] layout: y = x W^T + b.
@@ -178,17 +180,19 @@ def make_inputs(w: Workload, seed: Optional[int] = None) -> Inputs:
     cand_offset = np.arange(w.R + 1, dtype=np.int64) * w.N
     rt = None
     if w.rt_len > 0:
-        rt = _draw_seq(rng, [w.rt_len] * w.R, w.d, w.has_time, 0.0)
+        rt = _draw_seq(rng, [w.rt_len] * w.R, w.d, w.has_time, 0.0, codes=(w.dtype == "i8"))
     imp = None
     if w.imp_len > 0:
-        imp = _draw_seq(rng, [w.imp_len] * w.R, w.d, w.has_time, 0.0)
+        imp = _draw_seq(rng, [w.imp_len] * w.R, w.d, w.has_time, 0.0, codes=(w.dtype == "i8"))
     return Inputs(w=w, seq=seq, cand=cand, cand_offset=cand_offset, rt=rt, imp=imp)
 
 
 def make_weights(w: Workload, seed: Optional[int] = None, scale: float = 0.02) -> Weights:
     rng = np.random.Generator(np.random.PCG64(w.weight_seed if seed is None else seed))
     dm, ff = w.d_model, w.d_ffn
-    mat = (lambda a: round_to_bf16(a)) if w.dtype == "bf16" else (lambda a: a)
+    # int8 sequences feed a bf16 encoder
+    wdtype = "bf16" if w.dtype in ("bf16", "i8") else w.dtype
+    mat = (lambda a: round_to_bf16(a)) if wdtype == "bf16" else (lambda a: a)
 
     def n(*shape):
         return (rng.standard_normal(shape) * scale).astype(np.float32)
@@ -217,7 +221,7 @@ def make_weights(w: Workload, seed: Optional[int] = None, scale: float = 0.02) -
     W_pool = mat(n(dm, dm))
     b_pool = n(dm)
     return Weights(d_in=w.d, d_model=dm, n_heads=w.n_heads, d_ffn=ff, max_pos=w.T,
-                   dtype=w.dtype, W_in=W_in, b_in=b_in, E_act=E_act, E_time=E_time,
+                   dtype=wdtype, W_in=W_in, b_in=b_in, E_act=E_act, E_time=E_time,
                    E_pos=E_pos, layers=layers, W_pool=W_pool, b_pool=b_pool)
 
 
@@ -226,7 +230,7 @@ class TokenBatch:
     """Explicit encoder inputs (the encoder run on its own): per candidate T token
     rows with their action types, time buckets and valid length, and the
     candidate's embedding.  Rows at or past a valid length hold grid values too."""
-    emb: np.ndarray                 # [total, T, d] float32 on the 1/8 grid
+    emb: np.ndarray                 # [total, T, d] float32 on the 1/8 grid, or int8 codes
     act: np.ndarray                 # [total, T] uint8
     time: Optional[np.ndarray]      # [total, T] uint8 or None
     valid_len: np.ndarray           # [total] int32
@@ -238,11 +242,12 @@ class TokenBatch:
 
 
 def make_tokens(total: int, T: int, d: int, has_time: bool = True, seed: int = 0,
-                valid_len=None) -> TokenBatch:
-    """Seeded explicit tokens: grid rows, uniform action types, sorted time buckets;
-    valid_len defaults to T for every candidate."""
+                valid_len=None, codes: bool = False) -> TokenBatch:
+    """Seeded explicit tokens: grid rows (codes: int8 codes of random unit rows),
+    uniform action types, sorted time buckets; valid_len defaults to T for every
+    candidate."""
     rng = np.random.Generator(np.random.PCG64(seed))
-    emb = grid_values(rng, (total, T, d))
+    emb = int8_codes(rng, (total, T, d)) if codes else grid_values(rng, (total, T, d))
     act = rng.integers(0, N_ACT, size=(total, T)).astype(np.uint8)
     time = np.sort(rng.integers(0, N_TIME, size=(total, T)), axis=1).astype(np.uint8) \
         if has_time else None

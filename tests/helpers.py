@@ -136,14 +136,17 @@ def oracle_select_encode_eq2(inp, W, ids=None, chunk=16, causal=True):
 
 
 def upload_tokens(tb, dtype=T.BF16, device="cuda"):
-    """A synth.TokenBatch as explicit device tokens and candidate embeddings."""
+    """A synth.TokenBatch as explicit device tokens and candidate embeddings (int8
+    codes stay codes, with bf16 candidates)."""
+    if tb.emb.dtype == np.int8:
+        dtype = T.I8
     td = T.torch_dtype(dtype)
     tok = T.DeviceTokens(
         emb=torch.from_numpy(tb.emb).to(device=device, dtype=td).contiguous(),
         act=torch.from_numpy(tb.act).to(device).contiguous(),
         time=None if tb.time is None else torch.from_numpy(tb.time).to(device).contiguous(),
         valid_len=torch.from_numpy(tb.valid_len).to(device).contiguous(), dtype=dtype)
-    cand = torch.from_numpy(tb.cand).to(device=device, dtype=td).contiguous()
+    cand = torch.from_numpy(tb.cand).to(device=device, dtype=T.cand_dtype(dtype)).contiguous()
     return tok, cand
 
 
@@ -153,9 +156,10 @@ def oracle_encode_tokens(tb, W, ids=None, causal=True, chunk=4):
     ids = np.arange(tb.total) if ids is None else np.asarray(ids, dtype=np.int64)
     out = np.zeros((tb.total, 2 * W.d_model), dtype=np.float64)
     time = tb.time if tb.time is not None else np.zeros_like(tb.act)
+    emb = oracle.dequantise(tb.emb) if tb.emb.dtype == np.int8 else tb.emb
 
     def one(part):
-        o = oracle.encode(tb.emb, tb.act, time, tb.valid_len, tb.cand, W, only=part,
+        o = oracle.encode(emb, tb.act, time, tb.valid_len, tb.cand, W, only=part,
                           chunk=chunk, causal=causal)
         return part, o[part]
 

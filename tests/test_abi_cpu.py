@@ -258,6 +258,36 @@ def test_small_encoder_queries():
                                FAKE, 1 << 40, None) == -4, bad
 
 
+def test_int8_codes_feed_only_the_small_encoder():
+    """int8 sequences (and int8 explicit tokens) go to the d_model-64 encoder with
+    bf16 weights; d_model 256 reports unsupported, float32 weights a dtype error."""
+    lib = T.load_library()
+    s = fake_seq(R=1, d=32, dtype=T.I8, max_len=16384)
+    c = fake_cands(total=10, max_count=10)
+    small = fake_weights(d=32, dm=64, heads=1, ffn=32, layers=2, max_pos=128)
+    assert lib.tav2_select_encode_workspace(ctypes.byref(s), None, ctypes.byref(c), 128,
+                                            ctypes.byref(small)) > 0
+    big = fake_weights(d=32, dm=256, heads=4, ffn=512, layers=2, max_pos=128)
+    assert lib.tav2_select_encode_workspace(ctypes.byref(s), None, ctypes.byref(c), 128,
+                                            ctypes.byref(big)) == 0
+    call = lambda w: lib.tav2_select_encode(ctypes.byref(s), None, ctypes.byref(c), 128,
+                                            ctypes.byref(w), T.MASK_CAUSAL, FAKE, FAKE, FAKE,
+                                            FAKE, 1 << 40, None)
+    assert call(big) == -4
+    f32 = fake_weights(d=32, dm=64, heads=1, ffn=32, layers=2, max_pos=128, dtype=T.F32)
+    assert call(f32) == -3
+    tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10,
+                   T=64, d=32, dtype=T.I8, reserved=0)
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(small)) == 0   # one block
+    tok.T = 65
+    assert lib.tav2_encode_workspace(ctypes.byref(tok), ctypes.byref(small)) > 0
+    tok.T = 64
+    enc = lambda w: lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), T.MASK_CAUSAL,
+                                    FAKE, FAKE, 1 << 40, None)
+    assert enc(big) == -4
+    assert enc(f32) == -3
+
+
 def test_unmasked_encoder_accepted_within_one_block():
     """TAV2_MASK_NONE passes the checks at T = 128 (the error then comes from the
     missing output), and for float32 at any supported T."""

@@ -128,6 +128,21 @@ def test_packed_weights_equal_unpacked(kw):
     assert torch.equal(a, b)
 
 
+def test_int8_code_tokens():
+    """Explicit tokens stored as int8 codes (Sec. 3.2.1): the encoder takes their
+    dequantised values (the oracle: codes x 0.65 / 127 in float64)."""
+    rng = np.random.default_rng(8)
+    tb = synth.make_tokens(48, 192, 32, seed=8, valid_len=ragged_lengths(48, 192, rng), codes=True)
+    run_and_check(tb, weights_for(192))
+
+
+def test_paper_int8_workload_select_encode():
+    """The paper's production path on its int8 storage: NN top-128 with fused
+    dequantisation and L2 normalisation over 16k codes, the 64 real-time code
+    rows kept, the encoder on the dequantised rows; every candidate checked."""
+    check_workload(synth.PAPER_I8)
+
+
 def test_repeated_runs_bitwise_identical():
     tb = synth.make_tokens(300, 192, 32, seed=2)
     tok, cand = upload_tokens(tb)
