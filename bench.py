@@ -65,6 +65,13 @@ def site_work(w, total, valid_tokens, pairs, launches_per_step, rows_total, k):
     # int8 storage: the codes and the candidates are what the method reads
     per["score_i8"] = ("byte", 1.0 * rows_total * d + 2.0 * total * d, scores_bytes)
     per["topk"] = ("byte", 8.0 * total * k, scores_bytes)
+    # the fused search (rows > 4096): the full products keep only survivors; over
+    # int8 codes it reads the codes and the candidates once
+    if w.dtype == "i8":
+        per["nn_filter"] = ("byte", 1.0 * rows_total * d + 2.0 * total * d, None)
+    else:
+        per["nn_filter"] = ("flop", 2.0 * pairs * d, None)
+        per["nn_sample"] = ("flop", 2.0 * 1024 * d * total, None)
     out = {}
     for site, (kind, amount, mat) in per.items():
         n = launches_per_step.get(site)
