@@ -62,7 +62,8 @@ typedef int32_t tav2_status;
 #define TAV2_F32  0   /* float32 storage and arithmetic */
 #define TAV2_BF16 1   /* bfloat16 storage, fp32 accumulation */
 #define TAV2_I8   2   /* int8 codes of the quantised sequence storage (Sec. 3.2.1): a
-                         sequence dtype for tav2_nn_select only, with bf16 candidates */
+                         sequence dtype for the NN search (with bf16 candidates) and for
+                         the d_model-64 encoder, which takes the dequantised values */
 
 /* Attention mask of the encoder: the flags argument of tav2_encode and
  * tav2_select_encode. */
@@ -339,6 +340,67 @@ tav2_status tav2_select_encode_eq2(const tav2_seq* seq, const tav2_eq2* eq2,
  */
 int32_t tav2_profile_enable(int32_t on, const char* only_site);
 int64_t tav2_profile_report(char* buf, size_t buf_bytes);
+
+/*
+ * Serving-side batching (Sec. 3.4.2, 'Pinned Memory Arena' and 'Request Level
+ * De-duplication').  A batcher owns a pinned host arena and a device mirror of
+ * one mini-batch in the de-duplicated layout of tav2_seq / tav2_cands, both
+ * allocated once by tav2_batcher_create and freed by tav2_batcher_destroy (the
+ * only calls of this library that allocate; the arena is reset, never freed,
+ * between mini-batches).  Requests are collated straight into the pinned arena
+ * (no pageable staging copy), each request's sequences once whatever its number
+ * of candidates; tav2_batcher_upload moves the whole mini-batch to the device
+ * with one host-to-device copy on the caller's stream; tav2_batcher_views gives
+ * the tav2_seq / tav2_cands that tav2_select_encode then takes.
+ *
+ * Dynamic batching: tav2_batcher_add returns TAV2_ERR_TOO_LARGE when the request
+ * does not fit the capacities; the caller uploads and runs the mini-batch and
+ * starts the next one with tav2_batcher_reset.  After an upload the mini-batch
+ * is sealed: add returns TAV2_ERR_SHAPE until reset, and a second upload copies
+ * the same bytes again.  The copy is asynchronous: the caller synchronises the
+ * stream before it resets the batcher or reuses the views' memory for the next
+ * mini-batch.  A batcher is not thread-safe; use one per serving thread (the
+ * paper's arena is thread-local).
+ */
+typedef struct tav2_batcher tav2_batcher;
+typedef struct tav2_batcher_config {
+  int32_t dtype;          /* sequence dtype: TAV2_F32, TAV2_BF16 or TAV2_I8 (candidates: fp32
+                             with fp32 sequences, else bf16) */
+  int32_t d;              /* embedding width, multiple of 16, 16..512 */
+  int32_t has_time;       /* 1: time buckets present, 0: absent */
+  int32_t max_requests;   /* requests of one mini-batch, 1..65535 */
+  int64_t max_rows;       /* lifelong rows of one mini-batch, summed over its requests */
+  int64_t max_rt_rows;    /* real-time rows of one mini-batch (0: none) */
+  int64_t max_cands;      /* candidates of one mini-batch, >= 1 */
+} tav2_batcher_config;
+typedef struct tav2_request {   /* HOST pointers, read during tav2_batcher_add only */
+  const void*    emb;             /* [len, d]: the lifelong sequence, most recent first */
+  const uint8_t* action_type;     /* [len] */
+  const uint8_t* time_bucket;     /* [len], or NULL without the time feature */
+  int32_t        len;
+  int32_t        rt_len;          /* real-time rows (0: none) */
+  const void*    rt_emb;          /* [rt_len, d], most recent first */
+  const uint8_t* rt_action_type;  /* [rt_len] */
+  const uint8_t* rt_time_bucket;  /* [rt_len], or NULL */
+  const void*    cand_emb;        /* [n_cands, d] */
+  int32_t        n_cands;
+  int32_t        reserved;        /* set to 0 */
+} tav2_request;
+/* Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_DTYPE (bad configuration, checked
+ * before anything is allocated), TAV2_ERR_HIP (allocation failed). */
+tav2_status tav2_batcher_create(const tav2_batcher_config* cfg, tav2_batcher** out);
+void tav2_batcher_destroy(tav2_batcher* b);
+size_t tav2_batcher_arena_bytes(const tav2_batcher* b);   /* pinned bytes (= device bytes) */
+tav2_status tav2_batcher_reset(tav2_batcher* b);
+/* Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_TOO_LARGE (does not fit: nothing added). */
+tav2_status tav2_batcher_add(tav2_batcher* b, const tav2_request* r);
+/* Errors: TAV2_ERR_NULL, TAV2_ERR_HIP. */
+tav2_status tav2_batcher_upload(tav2_batcher* b, void* stream);
+/* Device views of the uploaded mini-batch (rt may be NULL; its num_requests is the
+ * batch's, with rt_len 0 for requests without real-time rows).  Errors:
+ * TAV2_ERR_NULL, TAV2_ERR_SHAPE (nothing uploaded since the last reset). */
+tav2_status tav2_batcher_views(const tav2_batcher* b, tav2_seq* seq, tav2_seq* rt,
+                               tav2_cands* cands);
 
 #ifdef __cplusplus
 }

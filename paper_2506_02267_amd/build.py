@@ -16,7 +16,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtav2.so")
-SOURCES = ["api.cpp", "profile.cpp", "select.hip", "select_fused.hip", "gather.hip",
+SOURCES = ["api.cpp", "batcher.cpp", "profile.cpp", "select.hip", "select_fused.hip", "gather.hip",
            "encoder_fused.hip", "encoder_fused_unmasked.hip", "encoder_small.hip",
            "encoder_f32.hip"]
 ARCH = "gfx950"

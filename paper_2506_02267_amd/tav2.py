@@ -60,6 +60,19 @@ class Weights(ctypes.Structure):
                 ("b_pool", c_void_p), ("packed", c_void_p), ("packed_bytes", ctypes.c_uint64)]
 
 
+class BatcherConfig(ctypes.Structure):
+    _fields_ = [("dtype", c_int32), ("d", c_int32), ("has_time", c_int32),
+                ("max_requests", c_int32), ("max_rows", ctypes.c_int64),
+                ("max_rt_rows", ctypes.c_int64), ("max_cands", ctypes.c_int64)]
+
+
+class Request(ctypes.Structure):
+    _fields_ = [("emb", c_void_p), ("action_type", c_void_p), ("time_bucket", c_void_p),
+                ("len", c_int32), ("rt_len", c_int32), ("rt_emb", c_void_p),
+                ("rt_action_type", c_void_p), ("rt_time_bucket", c_void_p),
+                ("cand_emb", c_void_p), ("n_cands", c_int32), ("reserved", c_int32)]
+
+
 FUNCTIONS = {
     "tav2_status_string": (ctypes.c_char_p, [c_int32]),
     "tav2_abi_version": (c_int32, []),
@@ -86,6 +99,13 @@ FUNCTIONS = {
     "tav2_select_encode_eq2": (c_int32, [POINTER(Seq), POINTER(Eq2), POINTER(Cands), c_int32,
                                          POINTER(Weights), ctypes.c_uint32, c_void_p, c_void_p,
                                          c_void_p, c_void_p, c_size_t, c_void_p]),
+    "tav2_batcher_create": (c_int32, [POINTER(BatcherConfig), POINTER(c_void_p)]),
+    "tav2_batcher_destroy": (None, [c_void_p]),
+    "tav2_batcher_arena_bytes": (c_size_t, [c_void_p]),
+    "tav2_batcher_reset": (c_int32, [c_void_p]),
+    "tav2_batcher_add": (c_int32, [c_void_p, POINTER(Request)]),
+    "tav2_batcher_upload": (c_int32, [c_void_p, c_void_p]),
+    "tav2_batcher_views": (c_int32, [c_void_p, POINTER(Seq), POINTER(Seq), POINTER(Cands)]),
     "tav2_profile_enable": (c_int32, [c_int32, ctypes.c_char_p]),
     "tav2_profile_report": (ctypes.c_int64, [ctypes.c_char_p, c_size_t]),
 }
@@ -470,3 +490,77 @@ def profile_report() -> dict:
 
 def select_encode(seq, rt, cands, k, w, stream=None, flags: int = MASK_CAUSAL):
     return SelectEncode(seq, rt, cands, k, w, flags)(stream)
+
+
+class Batcher:
+    """A tav2_batcher: pinned host arena + device mirror of one mini-batch.
+
+    add() takes host numpy arrays in the storage layout (bf16 as uint16 bits, int8
+    codes, float32) and returns False when the request does not fit the mini-batch."""
+
+    TOO_LARGE = -7
+
+    def __init__(self, dtype: int, d: int, has_time: bool, max_requests: int, max_rows: int,
+                 max_rt_rows: int, max_cands: int):
+        self.lib = load_library()
+        self.cfg = BatcherConfig(dtype=dtype, d=d, has_time=int(has_time),
+                                 max_requests=max_requests, max_rows=max_rows,
+                                 max_rt_rows=max_rt_rows, max_cands=max_cands)
+        h = c_void_p()
+        _check("tav2_batcher_create", self.lib.tav2_batcher_create(ctypes.byref(self.cfg),
+                                                                   ctypes.byref(h)))
+        self.h = h
+
+    @property
+    def arena_bytes(self) -> int:
+        return int(self.lib.tav2_batcher_arena_bytes(self.h))
+
+    def reset(self):
+        _check("tav2_batcher_reset", self.lib.tav2_batcher_reset(self.h))
+
+    def add(self, emb, act, time=None, rt_emb=None, rt_act=None, rt_time=None, cand=None) -> bool:
+        a = lambda x: None if x is None else x.ctypes.data
+        q = Request(emb=a(emb), action_type=a(act), time_bucket=a(time),
+                    len=0 if emb is None else int(emb.shape[0]),
+                    rt_len=0 if rt_emb is None else int(rt_emb.shape[0]), rt_emb=a(rt_emb),
+                    rt_action_type=a(rt_act), rt_time_bucket=a(rt_time), cand_emb=a(cand),
+                    n_cands=0 if cand is None else int(cand.shape[0]), reserved=0)
+        st = self.lib.tav2_batcher_add(self.h, ctypes.byref(q))
+        if st == self.TOO_LARGE:
+            return False
+        _check("tav2_batcher_add", st)
+        return True
+
+    def upload(self, stream=None):
+        _check("tav2_batcher_upload", self.lib.tav2_batcher_upload(self.h, _stream_handle(stream)))
+
+    def views(self):
+        """(Seq, Seq, Cands) structs of the uploaded mini-batch on the device."""
+        s, r, c = Seq(), Seq(), Cands()
+        _check("tav2_batcher_views", self.lib.tav2_batcher_views(self.h, ctypes.byref(s),
+                                                                 ctypes.byref(r), ctypes.byref(c)))
+        return s, r, c
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.tav2_batcher_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        self.close()
+
+
+def select_encode_structs(s: Seq, r: Optional[Seq], c: Cands, k: int, w: DeviceWeights,
+                          out_idx: torch.Tensor, out_score: torch.Tensor, out: torch.Tensor,
+                          ws: Workspace, stream=None, flags: int = MASK_CAUSAL):
+    """tav2_select_encode on raw structs (e.g. a batcher's views); outputs
+    preallocated by the caller with at least c.total rows."""
+    lib = load_library()
+    rp = ctypes.byref(r) if r is not None else None
+    need = lib.tav2_select_encode_workspace(ctypes.byref(s), rp, ctypes.byref(c), k,
+                                            ctypes.byref(w.s))
+    wp, wb = ws.get(max(need, 1))
+    _check("tav2_select_encode", lib.tav2_select_encode(
+        ctypes.byref(s), rp, ctypes.byref(c), k, ctypes.byref(w.s), flags, _ptr(out_idx),
+        _ptr(out_score), _ptr(out), wp, wb, _stream_handle(stream)))
+    _used_on(stream, ws.buf, out_idx, out_score, out)

@@ -439,3 +439,35 @@ def test_eq2_struct_layout_and_argument_errors(tmp_path):
     plain = lib.tav2_select_encode_workspace(ctypes.byref(s), None, ctypes.byref(c), 64,
                                              ctypes.byref(fake_weights(max_pos=1024)))
     assert need > plain > 0
+
+
+@pytest.mark.parametrize("case,status", [("null_cfg", -1), ("dtype", -3), ("d", -2),
+                                         ("requests", -2), ("cands", -2), ("time", -2)])
+def test_batcher_config_errors(case, status):
+    """A bad configuration is refused before anything is allocated."""
+    lib = T.load_library()
+    cfg = T.BatcherConfig(dtype=T.I8, d=32, has_time=1, max_requests=8, max_rows=1000,
+                          max_rt_rows=0, max_cands=64)
+    if case == "dtype":
+        cfg.dtype = 7
+    elif case == "d":
+        cfg.d = 20
+    elif case == "requests":
+        cfg.max_requests = 0
+    elif case == "cands":
+        cfg.max_cands = 0
+    elif case == "time":
+        cfg.has_time = 2
+    h = ctypes.c_void_p()
+    st = lib.tav2_batcher_create(None if case == "null_cfg" else ctypes.byref(cfg), ctypes.byref(h))
+    assert st == status and not h.value
+
+
+def test_batcher_null_handles():
+    lib = T.load_library()
+    assert lib.tav2_batcher_reset(None) == -1
+    assert lib.tav2_batcher_add(None, None) == -1
+    assert lib.tav2_batcher_upload(None, None) == -1
+    assert lib.tav2_batcher_views(None, None, None, None) == -1
+    assert lib.tav2_batcher_arena_bytes(None) == 0
+    lib.tav2_batcher_destroy(None)
