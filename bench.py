@@ -292,6 +292,149 @@ def sweep(args):
         print(json.dumps(line), flush=True)
 
 
+SERVING_BATCHES = (128, 256, 512)   # items per mini-batch (the paper's copy-time figure)
+SERVING_PER_REQUEST = 16            # candidates per request
+
+
+def serving(args):
+    """Host side of serving (the paper's copy-time and model-run measurements):
+    per mini-batch of B items (requests of 16 candidates, each with a 16384-row
+    lifelong and a 64-row real-time sequence of 32-d int8 codes and time / action
+    features), the time to move it to the GPU for four ways of building it:
+    broadcast (every item carries its request's sequences) or de-duplicated
+    (each request's sequences once), collated in pageable memory and copied into
+    a pinned buffer (PinMem) or collated straight into pinned memory, then the
+    host-to-device copy (PCIe).  The de-duplicated, pinned way is the library's
+    batcher; its model run (upload, select + encode, outputs back to pinned host
+    memory) is timed as well.  One JSON line per B."""
+    import torch
+    import synth
+    from paper_2506_02267_amd import tav2 as T
+
+    reps = max(3, args.steps // 4)
+    for B in SERVING_BATCHES:
+        R = B // SERVING_PER_REQUEST
+        w = synth.scaled(synth.PAPER_I8, R=R, N=SERVING_PER_REQUEST)
+        inp = synth.make_inputs(w)
+        L, d, rt = w.L, w.d, w.rt_len
+        seq, rtq = inp.seq, inp.rt
+        cand_bf16 = torch.from_numpy(inp.cand).to(torch.bfloat16).view(torch.int16).numpy()
+        row_b = d + 2   # code bytes + action type + time bucket per row
+        per_item = (L + rt) * row_b
+        sizes = {"broadcast": B * per_item + B * d * 2,
+                 "dedup": R * per_item + B * d * 2 + R * 24 + (R + 1) * 8}
+        # pageable host sources (what a feature service hands over)
+        src = []
+        for r in range(R):
+            a, b0 = int(seq.offset[r]), int(rtq.offset[r])
+            src.append((seq.emb[a:a + L], seq.act[a:a + L], seq.time[a:a + L],
+                        rtq.emb[b0:b0 + rt], rtq.act[b0:b0 + rt], rtq.time[b0:b0 + rt],
+                        cand_bf16[r * SERVING_PER_REQUEST:(r + 1) * SERVING_PER_REQUEST]))
+
+        def collate(buf, broadcast):
+            """Rows of the mini-batch into buf (uint8 numpy view), in the layout the
+            way uses; returns the bytes written."""
+            o = 0
+            for r in range(R):
+                e, ac, tm, re, ra, rtm, c = src[r]
+                for _ in range(SERVING_PER_REQUEST if broadcast else 1):
+                    for x in (e, re, ac, ra, tm, rtm):
+                        n = x.nbytes
+                        buf[o:o + n] = x.reshape(-1).view(np.uint8)
+                        o += n
+                buf[o:o + c.nbytes] = c.reshape(-1).view(np.uint8)
+                o += c.nbytes
+            return o
+
+        dev = torch.empty(sizes["broadcast"] + 4096, dtype=torch.uint8, device="cuda")
+        pinned = torch.empty(sizes["broadcast"] + 4096, dtype=torch.uint8, pin_memory=True)
+        pageable = np.empty(sizes["broadcast"] + 4096, dtype=np.uint8)
+        pin_np = pinned.numpy()
+
+        def h2d(nbytes):
+            ev0 = torch.cuda.Event(enable_timing=True)
+            ev1 = torch.cuda.Event(enable_timing=True)
+            ev0.record()
+            dev[:nbytes].copy_(pinned[:nbytes], non_blocking=True)
+            ev1.record()
+            torch.cuda.synchronize()
+            return ev0.elapsed_time(ev1)
+
+        res = {}
+        for way, broadcast, in_pinned in (("baseline", True, False), ("pinned_arena", True, True),
+                                          ("dedup", False, False), ("all", False, True)):
+            pin_ms, pcie_ms, coll_ms = [], [], []
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                if in_pinned:
+                    n = collate(pin_np, broadcast)
+                    t1 = time.perf_counter()
+                    pm = 0.0
+                else:
+                    n = collate(pageable, broadcast)
+                    t1 = time.perf_counter()
+                    pin_np[:n] = pageable[:n]
+                    pm = (time.perf_counter() - t1) * 1e3
+                coll_ms.append((t1 - t0) * 1e3)
+                pin_ms.append(pm)
+                pcie_ms.append(h2d(n))
+            res[way] = {"bytes": n, "collate_ms": round(float(np.median(coll_ms)), 3),
+                        "pinmem_ms": round(float(np.median(pin_ms)), 3),
+                        "pcie_ms": round(float(np.median(pcie_ms)), 3)}
+        del dev, pinned, pageable
+        # the library's batcher: collate into its pinned arena, one upload, the model
+        # run (select + encode) and the outputs back to pinned host memory
+        W = synth.make_weights(w)
+        dw = T.DeviceWeights(W, pack=True)
+        bt = T.Batcher(T.I8, d, True, max_requests=R, max_rows=R * L, max_rt_rows=R * rt,
+                       max_cands=B)
+        ws = T.Workspace(torch.device("cuda"))
+        oi = torch.empty((B, w.k), dtype=torch.int32, device="cuda")
+        osc = torch.empty((B, w.k), dtype=torch.float32, device="cuda")
+        oo = torch.empty((B, 2 * w.d_model), dtype=torch.float32, device="cuda")
+        hi = torch.empty_like(oi, device="cpu", pin_memory=True)
+        hs = torch.empty_like(osc, device="cpu", pin_memory=True)
+        ho = torch.empty_like(oo, device="cpu", pin_memory=True)
+        run_ms, add_ms, up_ms = [], [], []
+        for i in range(reps + 2):
+            bt.reset()
+            t0 = time.perf_counter()
+            for r in range(R):
+                e, ac, tm, re, ra, rtm, c = src[r]
+                assert bt.add(e, ac, tm, re, ra, rtm, c)
+            t1 = time.perf_counter()
+            ev0 = torch.cuda.Event(enable_timing=True)
+            ev1 = torch.cuda.Event(enable_timing=True)
+            ev2 = torch.cuda.Event(enable_timing=True)
+            ev0.record()
+            bt.upload()
+            ev1.record()
+            s_, r_, c_ = bt.views()
+            T.select_encode_structs(s_, r_, c_, w.k, dw, oi, osc, oo, ws)
+            hi.copy_(oi, non_blocking=True)
+            hs.copy_(osc, non_blocking=True)
+            ho.copy_(oo, non_blocking=True)
+            ev2.record()
+            torch.cuda.synchronize()
+            if i >= 2:
+                add_ms.append((t1 - t0) * 1e3)
+                up_ms.append(ev0.elapsed_time(ev1))
+                run_ms.append(ev0.elapsed_time(ev2))
+        arena = int(bt.arena_bytes)
+        bt.close()
+        line = {"metric": "mini-batch copy time to the GPU by way of building it (ms)",
+                "unit": "ms", "higher_is_better": False,
+                "config": {"workload": "serving_copy", "items": B, "requests": R, "L": L,
+                           "rt_rows": rt, "d": d, "storage": "int8 codes"},
+                "ways": res,
+                "batcher": {"arena_bytes": arena,
+                            "collate_ms": round(float(np.median(add_ms)), 3),
+                            "upload_ms": round(float(np.median(up_ms)), 3),
+                            "model_run_ms": round(float(np.median(run_ms)), 3)},
+                "reduction_bytes": round(sizes["broadcast"] / sizes["dedup"], 2)}
+        print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -312,6 +455,9 @@ def main():
                     help="the encoder alone at the paper's production shape over 64-2048 "
                          "positions (batch 256) and batch 16-2048 (192 positions): one JSON "
                          "line per point")
+    ap.add_argument("--serving", action="store_true",
+                    help="the host side of serving: copy time of 128 / 256 / 512-item "
+                         "mini-batches built four ways, and the batcher's model run")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy 256 MiB device to device three times "
                          "(a plain copy of known size for scaling memory counters)")
@@ -323,6 +469,9 @@ def main():
         sys.exit(2)
     if args.sweep:
         sweep(args)
+        return
+    if args.serving:
+        serving(args)
         return
 
     import torch
