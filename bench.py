@@ -8,6 +8,10 @@ the causal encoder and the pooled head.  The default workload is one request
 with a 16384-action lifelong sequence (d = 256, bf16), 1000 candidates and
 k = 256, encoded by 2 layers of d_model 256 / 4 heads / FFN 1024.
 
+The encoder weights are packed into the kernels' layout once, before the timed
+region (tav2_pack_weights, as a server does when it loads its model);
+--pack-per-call times the calls that pack them every time instead.
+
 Prints one JSON line: candidates/s (whole job), the dominant kernel's
 roofline position, and the CPU oracle's throughput on a bounded sample.
 """
@@ -249,7 +253,7 @@ def sweep(args):
                              time=torch.from_numpy(tb.time).cuda(),
                              valid_len=torch.from_numpy(tb.valid_len).cuda(), dtype=T.BF16)
         cand = torch.from_numpy(tb.cand).to("cuda", torch.bfloat16)
-        dw = T.DeviceWeights(W)
+        dw = T.DeviceWeights(W, pack=True)
         out = torch.empty((B, 2 * w.d_model), dtype=torch.float32, device="cuda")
         ws = T.Workspace(torch.device("cuda"))
         for _ in range(args.warmup):
@@ -455,6 +459,9 @@ def main():
                     help="the encoder alone at the paper's production shape over 64-2048 "
                          "positions (batch 256) and batch 16-2048 (192 positions): one JSON "
                          "line per point")
+    ap.add_argument("--pack-per-call", action="store_true",
+                    help="let every call pack the encoder weights into its workspace instead "
+                         "of packing them once at load (tav2_pack_weights)")
     ap.add_argument("--serving", action="store_true",
                     help="the host side of serving: copy time of 128 / 256 / 512-item "
                          "mini-batches built four ways, and the batcher's model run")
@@ -499,9 +506,9 @@ def main():
         imp = T.DeviceSeq.from_host(inp.imp, dt) if inp.imp is not None else None
         call = T.SelectEncodeEq2(seq, rt, w.r, w.k_rt if rt is not None else 0, imp,
                                  w.k_imp if imp is not None else 0, cands, w.k,
-                                 T.DeviceWeights(W))
+                                 T.DeviceWeights(W, pack=not args.pack_per_call))
     else:
-        call = T.SelectEncode(seq, rt, cands, w.k, T.DeviceWeights(W))
+        call = T.SelectEncode(seq, rt, cands, w.k, T.DeviceWeights(W, pack=not args.pack_per_call))
     stream = torch.cuda.current_stream()
     total = inp.total
     lengths = inp.seq.length.astype(np.int64)
@@ -642,6 +649,8 @@ def main():
               "d": w.d, "candidates": total, "k": w.k}
     if args.graph:
         config["launch"] = "hip_graph"
+    if not select_only:
+        config["weights"] = "packed per call" if args.pack_per_call else "packed at load"
     if not select_only:
         config.update({"rt_len": w.rt_len, "T": w.T, "d_model": w.d_model, "heads": w.n_heads,
                        "d_ffn": w.d_ffn, "layers": w.n_layers})
