@@ -38,87 +38,139 @@ __device__ __forceinline__ uint64_t sel_value(uint32_t key, int row) {
 __device__ __forceinline__ int sel_row(uint64_t v) { return int(0xFFFFu - uint32_t(v & 0xFFFFu)); }
 __device__ __forceinline__ uint32_t sel_key(uint64_t v) { return uint32_t(v >> 16); }
 
+// Orders a wave's LDS writes before its later LDS reads of words other lanes
+// wrote (no workgroup barrier: the data is the wave's own).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Wave-wide scans and reductions through DPP row shifts and row broadcasts
+// (no LDS round trip): row_shr 1, 2, 4, 8 combine within rows of 16 lanes, then
+// row_bcast 15 and 31 carry row totals upwards.  Lanes a shift leaves without a
+// source take the identity (the `old` operand).
+#define TAV2_DPP_STEPS(OP, ID)                                                          \
+  v = v OP uint32_t(__builtin_amdgcn_update_dpp(ID, int(v), 0x111, 0xf, 0xf, false)); \
+  v = v OP uint32_t(__builtin_amdgcn_update_dpp(ID, int(v), 0x112, 0xf, 0xf, false)); \
+  v = v OP uint32_t(__builtin_amdgcn_update_dpp(ID, int(v), 0x114, 0xf, 0xf, false)); \
+  v = v OP uint32_t(__builtin_amdgcn_update_dpp(ID, int(v), 0x118, 0xf, 0xf, false)); \
+  v = v OP uint32_t(__builtin_amdgcn_update_dpp(ID, int(v), 0x142, 0xa, 0xf, false)); \
+  v = v OP uint32_t(__builtin_amdgcn_update_dpp(ID, int(v), 0x143, 0xc, 0xf, false));
+// Inclusive prefix sum over the lanes.
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t v) {
+  TAV2_DPP_STEPS(+, 0)
+  return v;
+}
+// OR / AND over the lanes, returned to every lane (lane 63 holds the result).
+__device__ __forceinline__ uint64_t wave_or64(uint64_t x) {
+  uint32_t v = uint32_t(x);
+  TAV2_DPP_STEPS(|, 0)
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(v), 63));
+  v = uint32_t(x >> 32);
+  TAV2_DPP_STEPS(|, 0)
+  return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(v), 63))) << 32) | lo;
+}
+__device__ __forceinline__ uint64_t wave_and64(uint64_t x) {
+  uint32_t v = uint32_t(x);
+  TAV2_DPP_STEPS(&, -1)
+  const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(v), 63));
+  v = uint32_t(x >> 32);
+  TAV2_DPP_STEPS(&, -1)
+  return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(v), 63))) << 32) | lo;
+}
+#undef TAV2_DPP_STEPS
+
+// One digit step of a descending radix select, done by a whole wave on a
+// 256-bin histogram h in LDS: the digit whose bin holds the need-th largest
+// value (1 <= need <= the histogram's total) and the rank of that value among
+// the bin's values (rest).  Lane l takes bins 255 - 4l .. 252 - 4l; every lane
+// returns the result.
+__device__ __forceinline__ void radix_digit(const uint32_t* h, uint32_t need, uint32_t& digit,
+                                            uint32_t& rest) {
+  const int lane = threadIdx.x % WAVE;
+  const uint4 q = *reinterpret_cast<const uint4*>(h + 252 - 4 * lane);
+  const uint32_t hb[4] = {q.w, q.z, q.y, q.x};   // bins 255 - 4l - i
+  const uint32_t sum = hb[0] + hb[1] + hb[2] + hb[3];
+  const uint32_t incl = wave_incl_sum(sum);
+  const uint32_t before = incl - sum;
+  uint32_t dg = 0, rs = 0, cum = before;
+  bool hit = false;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if (!hit && cum + hb[i] >= need) {
+      hit = true;
+      dg = uint32_t(255 - 4 * lane - i);
+      rs = need - cum;
+    }
+    cum += hb[i];
+  }
+  // exactly one lane holds the crossing
+  const uint64_t who = __builtin_amdgcn_ballot_w64(before < need && need <= incl);
+  const int src = int(__builtin_ctzll(who));
+  digit = uint32_t(__builtin_amdgcn_readlane(int(dg), src));
+  rest = uint32_t(__builtin_amdgcn_readlane(int(rs), src));
+}
+
 // The need-th largest (1-based) of the cnt distinct 48-bit values v[] in LDS,
 // by an 8-bit radix select, most significant byte first, with NT threads.  The
 // bytes above the highest bit in which the values differ are common to all of
-// them and are skipped (their passes would put every value in one bin).  hist
-// (256 words), misc (2 words) and common (2 words) are LDS scratch.  Ends with
-// a barrier; every thread returns the value.
+// them and are skipped (their passes would put every value in one bin).  Every
+// wave reads each histogram and finds the digit itself, and the histograms
+// rotate over three buffers (a buffer is cleared in the pass after its own, two
+// passes before its next use), so that a pass costs one barrier.  hist (3 x 256
+// words, 16-byte aligned) and red (2 x NT / 64 values) are LDS scratch.  Starts
+// and ends with a barrier; every thread returns the value.
 template <int NT>
 __device__ __forceinline__ uint64_t radix_select48(const uint64_t* v, int cnt, int need,
-                                                   uint32_t* hist, int* misc,
-                                                   unsigned long long* common) {
+                                                   uint32_t* hist, uint64_t* red) {
   static_assert(NT >= 256, "one histogram bin per thread");
+  constexpr int NW = NT / WAVE;
   const int tid = threadIdx.x, lane = tid % WAVE, wid = tid / WAVE;
+  __syncthreads();   // v[] is complete
   uint64_t any = 0, all = ~uint64_t(0);
   for (int i = tid; i < cnt; i += NT) {
     any |= v[i];
     all &= v[i];
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    any |= __shfl_xor(any, o, WAVE);
-    all &= __shfl_xor(all, o, WAVE);
-  }
-  if (tid == 0) {
-    common[0] = 0ull;
-    common[1] = ~0ull;
-  }
-  __syncthreads();
+  any = wave_or64(any);
+  all = wave_and64(all);
   if (lane == 0) {
-    atomicOr(&common[0], (unsigned long long)any);
-    atomicAnd(&common[1], (unsigned long long)all);
+    red[wid] = any;
+    red[NW + wid] = all;
   }
+  if (tid < 256) hist[tid] = hist[256 + tid] = 0u;
   __syncthreads();
-  const uint64_t diff = (uint64_t(common[0]) ^ uint64_t(common[1])) & ((uint64_t(1) << 48) - 1);
+  any = 0;
+  all = ~uint64_t(0);
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    any |= red[w];
+    all &= red[NW + w];
+  }
+  const uint64_t diff = (any ^ all) & ((uint64_t(1) << 48) - 1);
   // first pass: the byte holding the highest differing bit (0 when cnt == 1)
   const int top = diff ? 63 - __builtin_clzll(diff) : 0;
   const int sh0 = top / 8 * 8;
-  uint64_t pre = sh0 + 8 >= 48 ? 0 : uint64_t(common[1]) >> (sh0 + 8);
+  uint64_t pre = sh0 + 8 >= 48 ? 0 : all >> (sh0 + 8);
+  uint32_t nd = uint32_t(need);
+  int buf = 0;
   for (int sh = sh0; sh >= 0; sh -= 8) {
-    if (tid < 256) hist[tid] = 0;
-    __syncthreads();
+    uint32_t* h = hist + 256 * buf;
     for (int i = tid; i < cnt; i += NT) {
       const uint64_t x = v[i];
-      if ((x >> (sh + 8)) == pre) atomicAdd(&hist[(x >> sh) & 255u], 1u);
+      if ((x >> (sh + 8)) == pre) atomicAdd(&h[(x >> sh) & 255u], 1u);
     }
     __syncthreads();
-    if (wid == 0) {   // bins in descending order: lane l holds bins 255 - 4l - q
-      uint32_t h[4], sum = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        h[q] = hist[255 - 4 * lane - q];
-        sum += h[q];
-      }
-      uint32_t incl = sum;
-#pragma unroll
-      for (int o = 1; o < WAVE; o <<= 1) {
-        const uint32_t t = __shfl_up(incl, o, WAVE);
-        if (lane >= o) incl += t;
-      }
-      const uint32_t before = incl - sum;
-      if (before < uint32_t(need) && uint32_t(need) <= incl) {
-        uint32_t cum = before;
-        int digit = 0, rest = 0;
-        bool hit = false;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (!hit && cum + h[q] >= uint32_t(need)) {
-            hit = true;
-            digit = 255 - 4 * lane - q;
-            rest = need - int(cum);
-          }
-          cum += h[q];
-        }
-        misc[0] = digit;
-        misc[1] = rest;
-      }
-    }
-    __syncthreads();
-    pre = (pre << 8) | uint64_t(misc[0]);
-    need = misc[1];
-    __syncthreads();   // misc and hist are rewritten by the next pass
+    const int clr = buf == 0 ? 2 : buf - 1;   // the previous pass's buffer: read by now
+    if (tid < 256) hist[256 * clr + tid] = 0u;
+    uint32_t digit, rest;
+    radix_digit(h, nd, digit, rest);
+    pre = (pre << 8) | uint64_t(digit);
+    nd = rest;
+    buf = buf == 2 ? 0 : buf + 1;
   }
+  __syncthreads();
   return pre;
 }
 

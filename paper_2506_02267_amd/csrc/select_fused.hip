@@ -40,10 +40,8 @@ constexpr int FB_ROWS = 256;                // bf16 filter: rows per workgroup (
 constexpr int FB_SROWS = 64;                // bf16 sample: slots per workgroup (wave w: tile w)
 constexpr int FI_CANDS = 32;                // int8: candidates per tile
 constexpr int FI_ROWS = 256;                // int8: rows (or slots) per workgroup
-constexpr int FT_THREADS = 256;             // select kernel
 constexpr int FF_THREADS = 512;             // fallback kernel
 constexpr int FF_GRID = 64;                 // fallback workgroups (each loops over the queue)
-constexpr int FS_SAMPLE_D = 16;             // bf16 sample: sequence k-blocks in flight
 constexpr int FS_FILTER_D = 8;              // bf16 filter: sequence k-blocks in flight
 
 int64_t fused_cap(int k) { return int64_t(align_up(size_t(2 * k + 1024), 64)); }
@@ -193,53 +191,84 @@ __device__ __forceinline__ void i8_products(const bf16_t* arow, const int8_t* br
 }
 
 // ---------------------------------------------------------------- 1. sample
-// bf16: workgroup = 128 candidates x 64 sample slots; wave w takes candidate
-// tile w.  samp[n][s] = top 16 bits of the key of slot s (0 for slots past the
-// row's end, below every score's).
+// bf16: wave w = candidate tile w (32 candidates) x 64 sample slots, the
+// workgroup's 4 waves over the same slots (their row loads after the first hit
+// L1).  The operands come straight from memory, D k-blocks ahead of their use:
+// each wave is the only reader of its candidates.  The products are the
+// filter's (same operands, same k-block order).  samp[n][s0 .. s0 + 63] gets
+// the top 16 bits of the keys of those slots in some order within each 32-slot
+// tile (0 for slots past the row's end, below every score's key); the
+// threshold takes a candidate's keys as a multiset.
+constexpr int FS_SAMPLE_D = 16;   // k-blocks in flight (all of them at d <= 256)
 __global__ __launch_bounds__(256) void fsel_sample_bf16(FusedArgs A) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t fs_smem[];
-  bf16_t* ctile = reinterpret_cast<bf16_t*>(fs_smem);
   const int r = blockIdx.z;
-  const int64_t c_begin = A.cand_off[r], c_end = A.cand_off[r + 1];
-  const int64_t n0 = c_begin + int64_t(blockIdx.y) * FB_CANDS;
-  if (n0 >= c_end) return;
+  const int w = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
+  const int hf = lane / 32, l32 = lane % 32;
+  const int64_t c_end = A.cand_off[r + 1];
+  const int64_t nt = A.cand_off[r] + int64_t(blockIdx.y) * FB_CANDS + 32 * w;
+  if (nt >= c_end) return;   // wave-uniform
   const int L = min(A.seq_len[r], A.max_len);
   const SampleGeom g = sample_geom(L);
   const int s0 = blockIdx.x * FB_SROWS;
   if (s0 >= g.nsb * FS_BLK) return;
-  const int d = A.d, cld = d + FS_PAD;
-  const int w = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-  const int hf = lane / 32, l32 = lane % 32;
+  const int d = A.d, nkb = d / 16;
   const bf16_t* seq = static_cast<const bf16_t*>(A.emb) + A.seq_off[r] * int64_t(d);
-  int row[2];
-  bool ok[2];
+  const bf16_t* brow[2];
 #pragma unroll
   for (int b = 0; b < 2; ++b) {
-    const int s = s0 + 32 * b + l32;
-    row[b] = sample_row(s, g.q);
-    ok[b] = s < g.nsb * FS_BLK && row[b] < L;
+    const int sl = s0 + 32 * b + l32;
+    const int row = sample_row(sl, g.q);
+    const bool ok = sl < g.nsb * FS_BLK && row < L;
+    brow[b] = seq + int64_t(ok ? row : L - 1) * d + 8 * hf;
   }
-  const bf16_t* brow0 = seq + int64_t(ok[0] ? row[0] : L - 1) * d + 8 * hf;
-  const bf16_t* brow1 = seq + int64_t(ok[1] ? row[1] : L - 1) * d + 8 * hf;
-  bf16x8 bq[FS_SAMPLE_D][2];
-  bf16_prefetch<FS_SAMPLE_D>(bq, brow0, brow1, d / 16);
-  load_cand_tile(ctile, A.cand, n0, c_end, FB_CANDS, d);
-  __syncthreads();
-  f32x16 acc[1][2];
-  bf16_products<1, FS_SAMPLE_D>(ctile + (32 * w + l32) * cld + 8 * hf, cld, brow0, brow1, d / 16,
-                                bq, acc);
-  // lane: candidate 32 w + l32, slots s0 + 32 b + 8 j + 4 hf + i (register 4 j + i)
-  const int64_t n = n0 + 32 * w + l32;
-  if (n < c_end) {
+  const int64_t n = nt + l32;
+  const bf16_t* crow = A.cand + (n < c_end ? n : c_end - 1) * d + 8 * hf;
+  constexpr int D = FS_SAMPLE_D;
+  bf16x8 q0[D], q1[D], qc[D];
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+  for (int u = 0; u < D; ++u)
+    if (u < nkb) {
+      q0[u] = as_bf16x8(*reinterpret_cast<const uint4*>(brow[0] + 16 * u));
+      q1[u] = as_bf16x8(*reinterpret_cast<const uint4*>(brow[1] + 16 * u));
+      qc[u] = as_bf16x8(*reinterpret_cast<const uint4*>(crow + 16 * u));
+    }
+  f32x16 acc[2] = {f32x16{}, f32x16{}};
+  for (int kb0 = 0; kb0 < nkb; kb0 += D) {
 #pragma unroll
-      for (int reg = 0; reg < 16; ++reg) {
-        const int s = s0 + 32 * b + 8 * (reg / 4) + 4 * hf + (reg % 4);
-        const int row = sample_row(s, g.q);
-        const bool valid = s < g.nsb * FS_BLK && row < L;
-        A.samp[n * FS_NS + s] = valid ? uint16_t(score_key(acc[0][b][reg]) >> 16) : 0;
+    for (int u = 0; u < D; ++u) {
+      const int kb = kb0 + u;
+      if (kb < nkb) {   // wave-uniform
+        acc[0] = mfma32(q0[u], qc[u], acc[0]);
+        acc[1] = mfma32(q1[u], qc[u], acc[1]);
+        const int kn = kb + D;
+        if (kn < nkb) {
+          q0[u] = as_bf16x8(*reinterpret_cast<const uint4*>(brow[0] + 16 * kn));
+          q1[u] = as_bf16x8(*reinterpret_cast<const uint4*>(brow[1] + 16 * kn));
+          qc[u] = as_bf16x8(*reinterpret_cast<const uint4*>(crow + 16 * kn));
+        }
       }
+    }
+  }
+  if (n >= c_end) return;
+  // register 4 j + i of tile b: slot s0 + 32 b + 8 j + 4 hf + i; stored at
+  // position 16 hf + 4 j + i of the tile, two 16-byte stores per tile
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    uint32_t wd[8];
+#pragma unroll
+    for (int reg = 0; reg < 16; reg += 2) {
+      uint32_t k2[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int sl = s0 + 32 * b + 8 * ((reg + e) / 4) + 4 * hf + (reg + e) % 4;
+        const bool valid = sl < g.nsb * FS_BLK && sample_row(sl, g.q) < L;
+        k2[e] = valid ? score_key(acc[b][reg + e]) >> 16 : 0u;
+      }
+      wd[reg / 2] = k2[0] | (k2[1] << 16);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(A.samp + n * FS_NS + s0 + 32 * b + 16 * hf);
+    dst[0] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+    dst[1] = make_uint4(wd[4], wd[5], wd[6], wd[7]);
   }
 }
 
@@ -288,11 +317,12 @@ __global__ __launch_bounds__(256) void fsel_sample_i8(FusedArgs A) {
 }
 
 // ---------------------------------------------------------------- 2. threshold
-// One wave per candidate: t = the rr-th largest sampled 16-bit key (a bitwise
-// search: the largest t with at least rr sampled keys >= t), as a 32-bit key
+// One wave per candidate: t = the rr-th largest sampled 16-bit key (two radix
+// digits through a histogram of the wave's own in LDS), as a 32-bit key
 // threshold.  kk = 0: nothing survives; rr beyond the sample: everything does.
 // Also clears the candidate's survivor count and (first wave) the queue count.
 __global__ __launch_bounds__(256) void fsel_threshold(FusedArgs A) {
+  __shared__ __attribute__((aligned(16))) uint32_t th_hist[4][256];
   const int r = blockIdx.y;
   const int w = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
   if (blockIdx.x == 0 && r == 0 && threadIdx.x == 0) *A.nfb = 0u;
@@ -313,22 +343,40 @@ __global__ __launch_bounds__(256) void fsel_threshold(FusedArgs A) {
     if (rr > g.ns) {
       t = 0u;
     } else {
-      const int nslots = g.nsb * FS_BLK;
-      uint32_t kv[FS_NS / WAVE];
+      // the lane's 16 slots: 8 lane + 512 j + 0..7 (slots past the sample: key 0,
+      // below every sampled key that can count)
+      const int nslots = g.nsb * FS_BLK;   // a multiple of 8
+      uint32_t kw[8];
 #pragma unroll
-      for (int j = 0; j < FS_NS / WAVE; ++j) {
-        const int s = lane + WAVE * j;
-        kv[j] = s < nslots ? uint32_t(A.samp[n * FS_NS + s]) : 0u;
+      for (int j = 0; j < 2; ++j) {
+        const int s = 8 * lane + 512 * j;
+        const uint4 q = s < nslots ? *reinterpret_cast<const uint4*>(A.samp + n * FS_NS + s)
+                                   : make_uint4(0u, 0u, 0u, 0u);
+        kw[4 * j] = q.x;
+        kw[4 * j + 1] = q.y;
+        kw[4 * j + 2] = q.z;
+        kw[4 * j + 3] = q.w;
       }
-      uint32_t th = 0;
-      for (int b = 15; b >= 0; --b) {
-        const uint32_t probe = th | (1u << b);
-        int c = 0;
+      uint32_t* h = th_hist[w];
+      *reinterpret_cast<uint4*>(h + 4 * lane) = make_uint4(0u, 0u, 0u, 0u);
+      wave_lds_sync();
 #pragma unroll
-        for (int j = 0; j < FS_NS / WAVE; ++j) c += __popcll(__builtin_amdgcn_ballot_w64(kv[j] >= probe));
-        if (c >= rr) th = probe;
+      for (int i = 0; i < 16; ++i) atomicAdd(&h[(kw[i / 2] >> (16 * (i % 2) + 8)) & 255u], 1u);
+      wave_lds_sync();
+      uint32_t hi, rest;
+      radix_digit(h, uint32_t(rr), hi, rest);
+      wave_lds_sync();
+      *reinterpret_cast<uint4*>(h + 4 * lane) = make_uint4(0u, 0u, 0u, 0u);
+      wave_lds_sync();
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const uint32_t key = (kw[i / 2] >> (16 * (i % 2))) & 0xFFFFu;
+        if ((key >> 8) == hi) atomicAdd(&h[key & 255u], 1u);
       }
-      t = th << 16;
+      wave_lds_sync();
+      uint32_t lo, rest2;
+      radix_digit(h, rest, lo, rest2);
+      t = ((hi << 8) | lo) << 16;
     }
   }
   if (lane == 0) {
@@ -403,7 +451,7 @@ __device__ __forceinline__ float threshold_value(uint32_t t) {
   return key_score(t);
 }
 
-__global__ __launch_bounds__(256) void fsel_filter_bf16(FusedArgs A) {
+__global__ __launch_bounds__(256, 2) void fsel_filter_bf16(FusedArgs A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t fs_smem[];
   const int d = A.d, cld = d + FS_PAD;
   const int tile_b = FB_CANDS * cld * 2, stage_b = FS_NSEG * FS_LSEG * 8;
@@ -590,19 +638,21 @@ __global__ __launch_bounds__(256) void fsel_filter_i8(FusedArgs A) {
 }
 
 // ---------------------------------------------------------------- 4. select
-// One workgroup per candidate: the k best of its survivors, or the queue.
+// One workgroup per candidate: the k best of its survivors (a radix select of
+// the k-th largest, the values at or above it, placed by rank), or the queue.
+constexpr int FT_THREADS = 256;
 __global__ __launch_bounds__(FT_THREADS) void fsel_select(FusedArgs A, int32_t* __restrict__ out_idx,
                                                           float* __restrict__ out_score,
                                                           int32_t* __restrict__ cand_req) {
   __shared__ uint64_t vals[FS_CAP_MAX];
   __shared__ __attribute__((aligned(16))) uint64_t sel[TAV2_K_MAX];
-  __shared__ uint32_t hist[256];
-  __shared__ int misc[4];
-  __shared__ unsigned long long common[2];
+  __shared__ __attribute__((aligned(16))) uint32_t hist[3 * 256];
+  __shared__ uint64_t red[2 * FT_THREADS / WAVE];
+  __shared__ int nsel;
   const int r = blockIdx.y;
   const int64_t n = A.cand_off[r] + blockIdx.x;
   if (n >= A.cand_off[r + 1]) return;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid % WAVE;
   if (cand_req && tid == 0) cand_req[n] = r;   // the candidate's request, for the encoder
   const int L = min(A.seq_len[r], A.max_len);
   const int k = A.k;
@@ -638,13 +688,22 @@ __global__ __launch_bounds__(FT_THREADS) void fsel_select(FusedArgs A, int32_t* 
       if (i < m) vals[i] = v[u];
     }
   }
-  __syncthreads();
-  const uint64_t pre = radix_select48<FT_THREADS>(vals, m, kk, hist, misc, common);
-  if (tid == 0) misc[2] = 0;
-  __syncthreads();
-  for (int i = tid; i < m; i += FT_THREADS) {
-    const uint64_t v = vals[i];
-    if (v >= pre) sel[atomicAdd(&misc[2], 1)] = v;   // exactly kk of them
+  if (tid == 0) nsel = 0;
+  const uint64_t pre = radix_select48<FT_THREADS>(vals, m, kk, hist, red);
+  // the values at or above the kk-th largest: exactly kk of them (one counter
+  // update per wave and round)
+  for (int i0 = 0; i0 < m; i0 += FT_THREADS) {
+    const int i = i0 + tid;
+    const bool take = i < m && vals[i] >= pre;
+    const uint64_t bm = __builtin_amdgcn_ballot_w64(take);
+    if (bm) {   // wave-uniform
+      int base = 0;
+      if (lane == 0) base = atomicAdd(&nsel, __popcll(bm));
+      base = __shfl(base, 0, WAVE);
+      const int pos = base + int(__builtin_amdgcn_mbcnt_hi(uint32_t(bm >> 32),
+                                                           __builtin_amdgcn_mbcnt_lo(uint32_t(bm), 0)));
+      if (take) sel[pos] = vals[i];
+    }
   }
   __syncthreads();
   place_by_rank<FT_THREADS>(sel, kk, oi, os);
@@ -841,16 +900,14 @@ hipError_t launch_select_fused(const tav2_seq& seq, const tav2_cands& c, int k,
   hipError_t e;
   {
     ProfScope prof("nn_sample", st);
-    const size_t lds = size_t(nct) * (d + FS_PAD) * 2;
-    const size_t lds_max = size_t(nct) * (512 + FS_PAD) * 2;
     if (i8) {
+      const size_t lds = size_t(nct) * (d + FS_PAD) * 2;
+      const size_t lds_max = size_t(nct) * (512 + FS_PAD) * 2;
       static std::atomic<bool> done[64] = {};
       if ((e = allow_lds(reinterpret_cast<const void*>(fsel_sample_i8), lds_max, done))) return e;
       fsel_sample_i8<<<dim3(FS_NS / FI_ROWS, ctiles, R), 256, lds, st>>>(A);
     } else {
-      static std::atomic<bool> done[64] = {};
-      if ((e = allow_lds(reinterpret_cast<const void*>(fsel_sample_bf16), lds_max, done))) return e;
-      fsel_sample_bf16<<<dim3(FS_NS / FB_SROWS, ctiles, R), 256, lds, st>>>(A);
+      fsel_sample_bf16<<<dim3(FS_NS / FB_SROWS, ctiles, R), 256, 0, st>>>(A);
     }
     if ((e = hipGetLastError())) return e;
   }
