@@ -124,7 +124,7 @@ hipError_t launch_encode_small(const TokenSource& src, const void* cand_emb, int
 constexpr int F32_MAX_T = 64;
 constexpr int F32_MAX_DM = 128;
 constexpr int F32_MAX_FFN = 512;
-constexpr int F32_LDS_FLOATS = 36 * 1024;
+constexpr int F32_MAX_D = 256;
 bool encode_f32_fits(int T, const tav2_weights& w);
 hipError_t launch_encode_f32(const TokenSource& src, const void* cand_emb, int64_t total,
                              const tav2_weights& w, float* out, bool unmasked, hipStream_t st);

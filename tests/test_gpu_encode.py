@@ -45,6 +45,27 @@ def test_tiny_fp32_all_candidates():
     check_workload(synth.TINY)
 
 
+@pytest.mark.parametrize("shape,flags", [
+    # the whole fp32 envelope: T 64, d_model 128, FFN 512 (four hidden chunks), d 256
+    (dict(d=256, d_model=128, n_heads=4, d_ffn=512, n_layers=2, k=64, has_time=True),
+     T.MASK_CAUSAL),
+    # 3 heads of 32, FFN 200 (a partial hidden chunk), a 48-wide embedding
+    (dict(d=48, d_model=96, n_heads=3, d_ffn=200, n_layers=1, k=40, has_time=False),
+     T.MASK_CAUSAL),
+    # one head of 128, three layers, T = 61 (keys padded to 64 in the P V product)
+    (dict(d=256, d_model=128, n_heads=1, d_ffn=64, n_layers=3, k=61, has_time=True),
+     T.MASK_CAUSAL),
+    (dict(d=256, d_model=128, n_heads=1, d_ffn=64, n_layers=3, k=61, has_time=True),
+     T.MASK_NONE),
+    # eight heads of 4, T = 17
+    (dict(d=16, d_model=32, n_heads=8, d_ffn=36, n_layers=1, k=17, has_time=False),
+     T.MASK_CAUSAL),
+])
+def test_fp32_encoder_shapes(shape, flags):
+    w = synth.scaled(synth.TINY, R=2, L=700, N=10, **shape)
+    check_workload(w, flags=flags)
+
+
 def test_small_bf16_all_candidates():
     w = synth.scaled(synth.SINGLE, R=2, L=3000, N=24, k=64)
     check_workload(w)
