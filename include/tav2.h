@@ -261,7 +261,7 @@ tav2_status tav2_pack_weights(const tav2_weights* w, void* packed, size_t bytes,
  * 32 up to 256, at most 4 layers, all layer weights fitting the 160 KiB of LDS
  * next to the activations (2 layers of FFN 32 with d <= 64 do), its matrices
  * 16-byte and its tables 8-byte aligned (else TAV2_ERR_SHAPE); float32 with dm <= 128,
- * d_ffn <= 512, T <= 64 and d <= 256.  Other valid shapes return
+ * d_ffn <= 512, T <= 64 and d <= 256, dm, dm / n_heads and d_ffn multiples of 4.  Other valid shapes return
  * TAV2_ERR_UNSUPPORTED.  TAV2_MASK_NONE: T <= 128 for dm 256, T <= 64 for dm 64.
  * Errors: TAV2_ERR_NULL, TAV2_ERR_SHAPE, TAV2_ERR_DTYPE, TAV2_ERR_UNSUPPORTED,
  * TAV2_ERR_WORKSPACE, TAV2_ERR_HIP.

@@ -288,6 +288,30 @@ def test_int8_codes_feed_only_the_small_encoder():
     assert enc(f32) == -3
 
 
+def test_fp32_encoder_envelope():
+    """float32 encoder: T <= 64, d_model <= 128, FFN <= 512, d <= 256, with d_model,
+    the head width and the FFN width multiples of 4.  Shapes inside pass every check
+    (the call then reports the missing output); shapes outside are unsupported."""
+    lib = T.load_library()
+
+    def enc(T_, d, dm, heads, ffn):
+        w = fake_weights(d=d, dm=dm, heads=heads, ffn=ffn, layers=2, max_pos=128, dtype=T.F32)
+        tok = T.Tokens(emb=FAKE, action_type=FAKE, time_bucket=FAKE, valid_len=FAKE, total=10,
+                       T=T_, d=d, dtype=T.F32, reserved=0)
+        return lib.tav2_encode(ctypes.byref(tok), FAKE, ctypes.byref(w), T.MASK_CAUSAL, None, FAKE,
+                               1 << 40, None)
+
+    assert enc(64, 256, 128, 4, 512) == -1    # the envelope's corner
+    assert enc(17, 16, 32, 8, 36) == -1       # heads of 4
+    assert enc(40, 48, 96, 3, 200) == -1
+    assert enc(65, 256, 128, 4, 512) == -4    # T
+    assert enc(64, 256, 132, 4, 512) == -4    # d_model
+    assert enc(64, 256, 128, 4, 516) == -4    # FFN
+    assert enc(64, 272, 128, 4, 512) == -4    # d
+    assert enc(64, 64, 24, 4, 64) == -4       # heads of 6
+    assert enc(64, 64, 64, 2, 130) == -4      # FFN not a multiple of 4
+
+
 def test_unmasked_encoder_accepted_within_one_block():
     """TAV2_MASK_NONE passes the checks at T = 128 (the error then comes from the
     missing output), and for float32 at any supported T."""
