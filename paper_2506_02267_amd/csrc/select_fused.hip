@@ -426,8 +426,9 @@ __host__ __device__ __forceinline__ int filter_region(int nc, int d) {
   return tile > stage ? tile : stage;
 }
 
-// bf16: workgroup = 128 candidates x 256 rows, wave w rows 64 w .. +63.  A lane
-// holds candidates l % 32 + 32 a (a = 0..3) for 32 of the wave's rows (half
+// bf16: workgroup = 32 NA candidates (NA = 4, or 2 when that gives too few
+// workgroups to fill the GPU) x 256 rows, wave w rows 64 w .. +63.  A lane
+// holds candidates l % 32 + 32 a (a < NA) for 32 of the wave's rows (half
 // l / 32 of every 8-row group), so its survivors go to its own LDS segments, one
 // per (candidate, wave, half), each with a lane-private counter.  The hot loop is
 // branch-free: every score is written, to the segment's next slot when it
@@ -438,10 +439,13 @@ __host__ __device__ __forceinline__ int filter_region(int nc, int d) {
 // memory.  Scores are compared as floats with the threshold's value (keys and
 // floats are ordered alike), and staged as raw bits with their row.
 constexpr int FS_LSEG = 8;
-constexpr int FS_NSEG = FB_CANDS * 4 * 2;   // (candidate, wave, half)
+template <int NA>
+constexpr int filter_nseg() { return 32 * NA * 4 * 2; }   // (candidate, wave, half)
+template <int NA>
 __host__ __device__ __forceinline__ int filter_bf16_lds(int d) {
-  const int tile = FB_CANDS * (d + FS_PAD) * 2, stage = FS_NSEG * FS_LSEG * 8;
-  return (tile > stage ? tile : stage) + FB_CANDS * 4 + 2 * FS_NSEG * 4;
+  constexpr int NC = 32 * NA, NSEG = filter_nseg<NA>();
+  const int tile = NC * (d + FS_PAD) * 2, stage = NSEG * FS_LSEG * 8;
+  return (tile > stage ? tile : stage) + NC * 4 + 2 * NSEG * 4;
 }
 // Float value a 32-bit threshold key stands for: key 0 lets every score through
 // (-inf), key 0xFFFFFFFF none (NaN compares false).
@@ -451,25 +455,27 @@ __device__ __forceinline__ float threshold_value(uint32_t t) {
   return key_score(t);
 }
 
+template <int NA>
 __global__ __launch_bounds__(256, 2) void fsel_filter_bf16(FusedArgs A) {
+  constexpr int NC = 32 * NA, NSEG = filter_nseg<NA>();
   extern __shared__ __attribute__((aligned(16))) uint8_t fs_smem[];
   const int d = A.d, cld = d + FS_PAD;
-  const int tile_b = FB_CANDS * cld * 2, stage_b = FS_NSEG * FS_LSEG * 8;
+  const int tile_b = NC * cld * 2, stage_b = NSEG * FS_LSEG * 8;
   const int region = tile_b > stage_b ? tile_b : stage_b;
   bf16_t* ctile = reinterpret_cast<bf16_t*>(fs_smem);
   uint2* stage = reinterpret_cast<uint2*>(fs_smem);                 // {row, score bits}
-  float* thr_f = reinterpret_cast<float*>(fs_smem + region);          // [FB_CANDS]
-  uint32_t* scnt = reinterpret_cast<uint32_t*>(thr_f + FB_CANDS);     // [FS_NSEG]
-  uint32_t* soff = scnt + FS_NSEG;                                    // [FS_NSEG]
+  float* thr_f = reinterpret_cast<float*>(fs_smem + region);          // [NC]
+  uint32_t* scnt = reinterpret_cast<uint32_t*>(thr_f + NC);           // [NSEG]
+  uint32_t* soff = scnt + NSEG;                                       // [NSEG]
   const int r = blockIdx.z;
   const int64_t c_begin = A.cand_off[r], c_end = A.cand_off[r + 1];
-  const int64_t n0 = c_begin + int64_t(blockIdx.y) * FB_CANDS;
+  const int64_t n0 = c_begin + int64_t(blockIdx.y) * NC;
   if (n0 >= c_end) return;
   const int L = min(A.seq_len[r], A.max_len);
   const int ib = blockIdx.x * FB_ROWS;
   if (ib >= L) return;
   const int tid = threadIdx.x;
-  if (tid < FB_CANDS) {   // tile columns past the request's candidates keep nothing
+  if (tid < NC) {   // tile columns past the request's candidates keep nothing
     const int64_t n = n0 + tid;
     thr_f[tid] = threshold_value(n < c_end ? A.thr[n] : 0xFFFFFFFFu);
   }
@@ -483,17 +489,17 @@ __global__ __launch_bounds__(256, 2) void fsel_filter_bf16(FusedArgs A) {
   const bf16_t* brow1 = seq + int64_t(i1) * d + 8 * hf;
   bf16x8 bq[FS_FILTER_D][2];
   if (active) bf16_prefetch<FS_FILTER_D>(bq, brow0, brow1, d / 16);
-  load_cand_tile(ctile, A.cand, n0, c_end, FB_CANDS, d);
+  load_cand_tile(ctile, A.cand, n0, c_end, NC, d);
   __syncthreads();
-  f32x16 acc[4][2];
+  f32x16 acc[NA][2];
   if (active)
-    bf16_products<4, FS_FILTER_D>(ctile + l32 * cld + 8 * hf, cld, brow0, brow1, d / 16, bq, acc);
+    bf16_products<NA, FS_FILTER_D>(ctile + l32 * cld + 8 * hf, cld, brow0, brow1, d / 16, bq, acc);
   __syncthreads();   // the candidate tile's region now stages survivors
   // segment of (candidate 32 a + l32, wave w, half hf): lane-consecutive, and the
   // stage slot-major, so that a wave's 64 slot writes are one contiguous 512 bytes
   constexpr uint32_t KEEP = FS_LSEG - 1;   // survivors a segment keeps
   auto seg_of = [](int a, int wv, int l, int h) { return ((a * 4 + wv) * 32 + l) * 2 + h; };
-  uint32_t cnt[4] = {0u, 0u, 0u, 0u};
+  uint32_t cnt[NA] = {};
   if (active) {
     // register 4 j + i of row tile b holds row row0 + 32 b + 8 j + 4 hf + i
     uint32_t rowok[2] = {0u, 0u};
@@ -503,7 +509,7 @@ __global__ __launch_bounds__(256, 2) void fsel_filter_bf16(FusedArgs A) {
       for (int reg = 0; reg < 16; ++reg)
         rowok[b] |= uint32_t(row0 + 32 * b + 8 * (reg / 4) + 4 * hf + (reg % 4) < L) << reg;
 #pragma unroll
-    for (int a = 0; a < 4; ++a) {
+    for (int a = 0; a < NA; ++a) {
       const int c = 32 * a + l32;
       const float t = thr_f[c];
       uint2* seg = stage + seg_of(a, w, l32, hf);
@@ -515,7 +521,7 @@ __global__ __launch_bounds__(256, 2) void fsel_filter_bf16(FusedArgs A) {
           const float sc = acc[a][b][reg];
           const bool keep = sc >= t && ((rowok[b] >> reg) & 1u);
           const int row = row0 + 32 * b + 8 * (reg / 4) + 4 * hf + (reg % 4);
-          seg[(keep ? min(m, KEEP) : KEEP) * FS_NSEG] = make_uint2(uint32_t(row), __float_as_uint(sc));
+          seg[(keep ? min(m, KEEP) : KEEP) * NSEG] = make_uint2(uint32_t(row), __float_as_uint(sc));
           m += keep ? 1u : 0u;
         }
       cnt[a] = m;
@@ -540,9 +546,9 @@ __global__ __launch_bounds__(256, 2) void fsel_filter_bf16(FusedArgs A) {
     }
   }
 #pragma unroll
-  for (int a = 0; a < 4; ++a) scnt[seg_of(a, w, l32, hf)] = min(cnt[a], KEEP);
+  for (int a = 0; a < NA; ++a) scnt[seg_of(a, w, l32, hf)] = min(cnt[a], KEEP);
   __syncthreads();
-  if (tid < FB_CANDS) {   // one counter update per candidate; its segments' offsets
+  if (tid < NC) {   // one counter update per candidate; its segments' offsets
     const int a = tid / 32, l = tid % 32;
     uint32_t m = 0;
 #pragma unroll
@@ -557,12 +563,12 @@ __global__ __launch_bounds__(256, 2) void fsel_filter_bf16(FusedArgs A) {
   }
   __syncthreads();
 #pragma unroll
-  for (int q = 0; q < FS_NSEG / 256; ++q) {   // segment sg = tid + 256 q
+  for (int q = 0; q < NSEG / 256; ++q) {   // segment sg = tid + 256 q
     const int sg = tid + 256 * q;
     const uint32_t m = scnt[sg], base = soff[sg];
     const int64_t n = n0 + 32 * (sg / 256) + (sg / 2) % 32;
     for (uint32_t i = 0; i < m; ++i) {
-      const uint2 e = stage[i * FS_NSEG + sg];
+      const uint2 e = stage[i * NSEG + sg];
       if (base + i < uint32_t(A.cap))
         A.surv[n * A.cap + base + i] = sel_value(score_key(__uint_as_float(e.y)), int(e.x));
     }
@@ -897,6 +903,11 @@ hipError_t launch_select_fused(const tav2_seq& seq, const tav2_cands& c, int k,
   const int d = seq.d;
   const int nct = i8 ? FI_CANDS : FB_CANDS;
   const unsigned ctiles = unsigned(cdiv(c.max_count, nct));
+  // bf16 filter: 128-candidate tiles, unless that leaves fewer workgroups than two
+  // per CU (few candidates): then 64
+  const unsigned rblocks = unsigned(cdiv(seq.max_len, FB_ROWS));
+  const bool narrow = !i8 && int64_t(R) * int64_t(ctiles) * rblocks < 512;
+  const unsigned ftiles = narrow ? unsigned(cdiv(c.max_count, FB_CANDS / 2)) : ctiles;
   hipError_t e;
   {
     ProfScope prof("nn_sample", st);
@@ -918,19 +929,24 @@ hipError_t launch_select_fused(const tav2_seq& seq, const tav2_cands& c, int k,
   }
   {
     ProfScope prof("nn_filter", st);
-    const unsigned rblocks = unsigned(cdiv(seq.max_len, FB_ROWS));
-    const size_t lds = i8 ? size_t(filter_region(nct, d)) + 3 * size_t(nct) * 4
-                          : size_t(filter_bf16_lds(d));
-    const size_t lds_max = i8 ? size_t(filter_region(nct, 512)) + 3 * size_t(nct) * 4
-                              : size_t(filter_bf16_lds(512));
     if (i8) {
+      const size_t lds = size_t(filter_region(nct, d)) + 3 * size_t(nct) * 4;
+      const size_t lds_max = size_t(filter_region(nct, 512)) + 3 * size_t(nct) * 4;
       static std::atomic<bool> done[64] = {};
       if ((e = allow_lds(reinterpret_cast<const void*>(fsel_filter_i8), lds_max, done))) return e;
       fsel_filter_i8<<<dim3(rblocks, ctiles, R), 256, lds, st>>>(A);
+    } else if (narrow) {
+      static std::atomic<bool> done[64] = {};
+      if ((e = allow_lds(reinterpret_cast<const void*>(fsel_filter_bf16<2>),
+                         size_t(filter_bf16_lds<2>(512)), done)))
+        return e;
+      fsel_filter_bf16<2><<<dim3(rblocks, ftiles, R), 256, size_t(filter_bf16_lds<2>(d)), st>>>(A);
     } else {
       static std::atomic<bool> done[64] = {};
-      if ((e = allow_lds(reinterpret_cast<const void*>(fsel_filter_bf16), lds_max, done))) return e;
-      fsel_filter_bf16<<<dim3(rblocks, ctiles, R), 256, lds, st>>>(A);
+      if ((e = allow_lds(reinterpret_cast<const void*>(fsel_filter_bf16<4>),
+                         size_t(filter_bf16_lds<4>(512)), done)))
+        return e;
+      fsel_filter_bf16<4><<<dim3(rblocks, ftiles, R), 256, size_t(filter_bf16_lds<4>(d)), st>>>(A);
     }
     if ((e = hipGetLastError())) return e;
   }
