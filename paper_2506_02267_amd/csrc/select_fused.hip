@@ -33,7 +33,6 @@ namespace tav2 {
 constexpr int FS_BLK = 32;                  // rows per sampled block
 constexpr int FS_MAXBLK = 32;               // sampled blocks per request at most
 constexpr int FS_NS = FS_BLK * FS_MAXBLK;   // sampled rows at most
-constexpr int FS_LCAP = 64;                 // LDS survivor slots per candidate and workgroup
 constexpr int FS_PAD = 8;                   // LDS row padding (bf16) of candidate tiles
 constexpr int FB_CANDS = 128;               // bf16: candidates per tile
 constexpr int FB_ROWS = 256;                // bf16 filter: rows per workgroup (4 waves x 64)
@@ -386,46 +385,6 @@ __global__ __launch_bounds__(256) void fsel_threshold(FusedArgs A) {
 }
 
 // ---------------------------------------------------------------- 3. filter
-// Survivor epilogue of a wave: value of (candidate c, row) appended when its key
-// is >= thr_s[c]; LDS slots first, then straight to the candidate's list.
-__device__ __forceinline__ void append_survivor(const FusedArgs& A, uint32_t* lcnt,
-                                                uint64_t* stage, int c, int64_t n, uint64_t v) {
-  const uint32_t p = atomicAdd(&lcnt[c], 1u);
-  if (p < uint32_t(FS_LCAP)) {
-    stage[c * FS_LCAP + p] = v;
-  } else {
-    const uint32_t gp = atomicAdd(&A.cnt[n], 1u);
-    if (gp < uint32_t(A.cap)) A.surv[n * A.cap + gp] = v;
-  }
-}
-// The workgroup's staged survivors (nc candidates) to their lists: one counter
-// update per candidate with survivors, then the copies (wave w: candidates w,
-// w + 4, ...).  Starts with a barrier.
-__device__ __forceinline__ void flush_survivors(const FusedArgs& A, const uint32_t* lcnt,
-                                                uint32_t* lbase, const uint64_t* stage, int nc,
-                                                int64_t n0) {
-  __syncthreads();
-  const int tid = threadIdx.x, w = tid / WAVE, lane = tid % WAVE;
-  if (tid < nc) {
-    const uint32_t m = min(lcnt[tid], uint32_t(FS_LCAP));
-    lbase[tid] = m ? atomicAdd(&A.cnt[n0 + tid], m) : 0u;
-  }
-  __syncthreads();
-  for (int c = w; c < nc; c += 4) {
-    const uint32_t m = min(lcnt[c], uint32_t(FS_LCAP));
-    const uint32_t base = lbase[c];
-    for (uint32_t i = lane; i < m; i += WAVE)
-      if (base + i < uint32_t(A.cap)) A.surv[(n0 + c) * A.cap + base + i] = stage[c * FS_LCAP + i];
-  }
-}
-
-// LDS layout of the filter kernels: [max(candidate tile, staged survivors)]
-// [thresholds nc][counts nc][bases nc].
-__host__ __device__ __forceinline__ int filter_region(int nc, int d) {
-  const int tile = nc * (d + FS_PAD) * 2, stage = nc * FS_LCAP * 8;
-  return tile > stage ? tile : stage;
-}
-
 // bf16: workgroup = 32 NA candidates (NA = 4, or 2 when that gives too few
 // workgroups to fill the GPU) x 256 rows, wave w rows 64 w .. +63.  A lane
 // holds candidates l % 32 + 32 a (a < NA) for 32 of the wave's rows (half
@@ -575,16 +534,37 @@ __global__ __launch_bounds__(256, 2) void fsel_filter_bf16(FusedArgs A) {
   }
 }
 
-// int8: workgroup = 32 candidates x 256 rows, wave w rows 64 w .. +63.
+// int8: workgroup = 32 candidates x 256 rows, wave w rows 64 w .. +63.  D
+// register 4 j + i of row tile b of a lane holds candidate 8 j + 4 hf + i and
+// the lane's row 32 b + l32, so for one register and lane half every lane has
+// the same candidate: the lanes whose score may survive are compacted with a
+// ballot into that (candidate, wave, row tile) segment of LDS, no atomics.  The
+// estimate (the hardware reciprocal square root) keeps every score within 64
+// units in the last place of the threshold (estimate and score have the same sign
+// and differ by a few units in the last place, relative error below 2^-21, and
+// keys of same-signed scores are ordered like their ulp counts); the staged ones
+// then get the exact score (a correctly rounded square root and division) and
+// those below the threshold are dropped before the counts are published.
+constexpr int FI_SLOTS = 8;                           // staged entries per segment
+constexpr int FI_NSEG = FI_CANDS * 4 * 2;             // (candidate, wave, row tile)
+__host__ __device__ __forceinline__ int filter_i8_lds(int d) {
+  const int tile = FI_CANDS * (d + FS_PAD) * 2, stage = FI_NSEG * FI_SLOTS * 8;
+  return (tile > stage ? tile : stage) + 2 * FI_CANDS * 4 + 2 * FI_NSEG * 4 + FI_ROWS * 4 +
+         FI_CANDS * 4;
+}
 __global__ __launch_bounds__(256) void fsel_filter_i8(FusedArgs A) {
   extern __shared__ __attribute__((aligned(16))) uint8_t fs_smem[];
   const int d = A.d, cld = d + FS_PAD;
-  const int region = filter_region(FI_CANDS, d);
+  const int tile_b = FI_CANDS * cld * 2, stage_b = FI_NSEG * FI_SLOTS * 8;
+  const int region = tile_b > stage_b ? tile_b : stage_b;
   bf16_t* ctile = reinterpret_cast<bf16_t*>(fs_smem);
-  uint64_t* stage = reinterpret_cast<uint64_t*>(fs_smem);
-  uint32_t* thr_s = reinterpret_cast<uint32_t*>(fs_smem + region);
-  uint32_t* lcnt = thr_s + FI_CANDS;
-  uint32_t* lbase = lcnt + FI_CANDS;
+  uint2* stage = reinterpret_cast<uint2*>(fs_smem);                   // {row, dot bits | key}
+  uint32_t* thr_s = reinterpret_cast<uint32_t*>(fs_smem + region);    // [FI_CANDS] keys
+  float* thr_e = reinterpret_cast<float*>(thr_s + FI_CANDS);          // [FI_CANDS]
+  uint32_t* scnt = reinterpret_cast<uint32_t*>(thr_e + FI_CANDS);     // [FI_NSEG]
+  uint32_t* soff = scnt + FI_NSEG;                                    // [FI_NSEG]
+  float* ssr = reinterpret_cast<float*>(soff + FI_NSEG);              // [FI_ROWS] row sums of squares
+  uint32_t* cbase = reinterpret_cast<uint32_t*>(ssr + FI_ROWS);       // [FI_CANDS]
   const int r = blockIdx.z;
   const int64_t c_begin = A.cand_off[r], c_end = A.cand_off[r + 1];
   const int64_t n0 = c_begin + int64_t(blockIdx.y) * FI_CANDS;
@@ -594,9 +574,12 @@ __global__ __launch_bounds__(256) void fsel_filter_i8(FusedArgs A) {
   if (ib >= L) return;
   const int tid = threadIdx.x;
   if (tid < FI_CANDS) {
+    // the key threshold t, and the float an estimate must reach to come within
+    // 64 units in the last place of it (keys and floats are ordered alike)
     const int64_t n = n0 + tid;
-    thr_s[tid] = n < c_end ? A.thr[n] : 0xFFFFFFFFu;
-    lcnt[tid] = 0u;
+    const uint32_t t = n < c_end ? A.thr[n] : 0xFFFFFFFFu;
+    thr_s[tid] = t;
+    thr_e[tid] = threshold_value(t < 64u ? 0u : t - 64u);
   }
   load_cand_tile(ctile, A.cand, n0, c_end, FI_CANDS, d);
   __syncthreads();
@@ -606,41 +589,97 @@ __global__ __launch_bounds__(256) void fsel_filter_i8(FusedArgs A) {
   const bool active = row0 < L;
   const int8_t* seq = static_cast<const int8_t*>(A.emb) + A.seq_off[r] * int64_t(d);
   f32x16 acc[2];
-  float sq[2];
+  float sq[2] = {0.f, 0.f};
   if (active) {
     const int i0 = min(row0 + l32, L - 1), i1 = min(row0 + 32 + l32, L - 1);
     i8_products(ctile + l32 * cld + 8 * hf, seq + int64_t(i0) * d + 8 * hf,
                 seq + int64_t(i1) * d + 8 * hf, d, acc, sq);
   }
-  __syncthreads();
+  __syncthreads();   // the candidate tile's region now stages survivors
+  uint32_t cnt_reg[2][4][4];   // per (row tile, j, i): this lane half's staged count
   if (active) {
-    // The exact score (a correctly rounded square root and division) only where an
-    // estimate with the hardware reciprocal square root comes within 64 units in
-    // the last place of the threshold: estimate and score have the same sign and
-    // differ by a few units in the last place (relative error below 2^-21), and
-    // keys of same-signed scores are ordered like their ulp counts.
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const float ss = sq[b] + __shfl_xor(sq[b], 32, WAVE);
+      if (hf == 0) ssr[64 * w + 32 * b + l32] = ss;
       const float rs = ss > 0.f ? __builtin_amdgcn_rsqf(ss) : 0.f;
       const int row = row0 + 32 * b + l32;
+      const bool row_ok = row < L;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const uint4 t4 = *reinterpret_cast<const uint4*>(thr_s + 8 * j + 4 * hf);
-        const uint32_t tv[4] = {t4.x, t4.y, t4.z, t4.w};
+        const float4 e4 = *reinterpret_cast<const float4*>(thr_e + 8 * j + 4 * hf);
+        const float ev[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int c = 8 * j + 4 * hf + i;
-          const uint32_t est = score_key(acc[b][4 * j + i] * rs);
-          if (row < L && est + 64u >= tv[i] && n0 + c < c_end) {
-            const uint32_t key = score_key(i8_score(acc[b][4 * j + i], ss));
-            if (key >= tv[i]) append_survivor(A, lcnt, stage, c, n0 + c, sel_value(key, row));
+          const float dot = acc[b][4 * j + i];
+          const bool maybe = row_ok && dot * rs >= ev[i];
+          const uint64_t bm = __builtin_amdgcn_ballot_w64(maybe);
+          const uint32_t lo = uint32_t(bm), hi = uint32_t(bm >> 32);
+          const uint32_t pos = hf ? __builtin_amdgcn_mbcnt_hi(hi, 0u)
+                                  : __builtin_amdgcn_mbcnt_lo(lo, 0u);
+          const int sg = (c * 4 + w) * 2 + b;
+          if (maybe && pos < uint32_t(FI_SLOTS))
+            stage[sg * FI_SLOTS + pos] = make_uint2(uint32_t(row), __float_as_uint(dot));
+          cnt_reg[b][j][i] = uint32_t(__popc(hf ? hi : lo));
+          if (maybe && pos >= uint32_t(FI_SLOTS)) {   // rare: past the segment, to memory
+            const uint32_t key = score_key(i8_score(dot, ss));
+            if (key >= thr_s[c]) {
+              const int64_t n = n0 + c;
+              const uint32_t gp = atomicAdd(&A.cnt[n], 1u);
+              if (gp < uint32_t(A.cap)) A.surv[n * A.cap + gp] = sel_value(key, row);
+            }
           }
         }
       }
     }
   }
-  flush_survivors(A, lcnt, lbase, stage, FI_CANDS, n0);
+  if (l32 == 0) {   // lanes 0 and 32 publish their half's segment counts
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int sg = ((8 * j + 4 * hf + i) * 4 + w) * 2 + b;
+          scnt[sg] = active ? min(cnt_reg[b][j][i], uint32_t(FI_SLOTS)) : 0u;
+        }
+  }
+  __syncthreads();
+  {   // the exact score of each staged entry (thread = segment); survivors compacted
+    const int sg = tid;
+    const int c = sg / 8;   // segment (c, wave, row tile)
+    const uint32_t t = thr_s[c];
+    const uint32_t m = scnt[sg];
+    uint32_t kept = 0;
+    for (uint32_t q = 0; q < m; ++q) {
+      const uint2 e = stage[sg * FI_SLOTS + q];
+      const float ss = ssr[int(e.x) - ib];
+      const uint32_t key = score_key(i8_score(__uint_as_float(e.y), ss));
+      if (key >= t) stage[sg * FI_SLOTS + (kept++)] = make_uint2(e.x, key);
+    }
+    scnt[sg] = kept;
+  }
+  __syncthreads();
+  if (tid < FI_CANDS) {   // one counter update per candidate
+    uint32_t m = 0;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      soff[tid * 8 + q] = m;
+      m += scnt[tid * 8 + q];
+    }
+    cbase[tid] = m ? atomicAdd(&A.cnt[n0 + tid], m) : 0u;
+  }
+  __syncthreads();
+  {
+    const int sg = tid, c = sg / 8;
+    const uint32_t m = scnt[sg], base = cbase[c] + soff[sg];
+    const int64_t n = n0 + c;
+    for (uint32_t q = 0; q < m; ++q) {
+      const uint2 e = stage[sg * FI_SLOTS + q];
+      if (base + q < uint32_t(A.cap)) A.surv[n * A.cap + base + q] = sel_value(e.y, int(e.x));
+    }
+  }
 }
 
 // ---------------------------------------------------------------- 4. select
@@ -930,8 +969,8 @@ hipError_t launch_select_fused(const tav2_seq& seq, const tav2_cands& c, int k,
   {
     ProfScope prof("nn_filter", st);
     if (i8) {
-      const size_t lds = size_t(filter_region(nct, d)) + 3 * size_t(nct) * 4;
-      const size_t lds_max = size_t(filter_region(nct, 512)) + 3 * size_t(nct) * 4;
+      const size_t lds = size_t(filter_i8_lds(d));
+      const size_t lds_max = size_t(filter_i8_lds(512));
       static std::atomic<bool> done[64] = {};
       if ((e = allow_lds(reinterpret_cast<const void*>(fsel_filter_i8), lds_max, done))) return e;
       fsel_filter_i8<<<dim3(rblocks, ctiles, R), 256, lds, st>>>(A);
