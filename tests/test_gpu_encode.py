@@ -125,6 +125,20 @@ def test_stress_workload_every_8th_candidate(part):
     check_workload(w, ids=ids[(ids >= lo) & (ids < hi)], W=W, inp=inp, gpu=gpu)
 
 
+def test_large_mean_layernorm_inputs():
+    """Every LayerNorm input shifted by about +8 to +16 on all of its features
+    (b_in, b_o and b_2 raised by 8) against a spread of about 0.2: the d_model-256
+    kernel's one-pass statistics (E[x^2] - mean^2 in fp32) stay within the bf16
+    bound.  T = 200: two encoder blocks joined by the K/V cache."""
+    w = synth.scaled(synth.SINGLE, R=1, L=3000, N=16, k=200)
+    W = synth.make_weights(w)
+    W.b_in = (W.b_in + 8.0).astype(np.float32)
+    for L in W.layers:
+        L.b_o = (L.b_o + 8.0).astype(np.float32)
+        L.b_2 = (L.b_2 + 8.0).astype(np.float32)
+    check_workload(w, W=W)
+
+
 def test_short_and_empty_requests_pad_and_zero():
     w = synth.scaled(synth.MIXED, R=3, L=None, L_range=(1, 1), N=4, k=32, rt_len=5, d=256)
     inp = synth.make_inputs(w)
