@@ -144,20 +144,26 @@ __device__ __forceinline__ void copy_floats(float* dst, const float* src, int n)
   for (int e = threadIdx.x; e < n; e += NT) dst[e] = src[e];
 }
 
-// The layer weights and W_in's token half into LDS: the packed image with 8
-// loads in flight per thread, or matrix by matrix from the caller's layout.
+// Waits for the wave's vector memory loads, LDS-DMA included.
+__device__ __forceinline__ void wait_vm_all() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0); expcnt and lgkmcnt unconstrained
+}
+
+// The layer weights and W_in's token half into LDS.  The packed image (wbytes, a
+// multiple of 16) goes by LDS-DMA, asynchronously: 1 KB pieces, piece i issued by
+// wave i mod 4, lane l moving bytes 16 l .. 16 l + 15 of it (lanes past the image
+// re-read its last 16 bytes and drop them past wbytes, at the start of the
+// activation area, which is written before it is read); the caller waits
+// (wait_vm_all in every wave, then a workgroup barrier) before the first LDS read
+// of a weight, so the loads of the first candidate's operands are in flight with
+// it.  Without the image: matrix by matrix from the caller's layout, synchronously.
 __device__ __forceinline__ void load_weights(const Args& A, uint8_t* smem) {
   if (A.packed) {
-    const int units = A.wbytes / 16;
-    const uint4* src = reinterpret_cast<const uint4*>(A.packed);
-    uint4* dst = reinterpret_cast<uint4*>(smem);
-    for (int u0 = threadIdx.x; u0 < units; u0 += 8 * NT) {
-      uint4 v[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = src[min(u0 + j * NT, units - 1)];
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (u0 + j * NT < units) dst[u0 + j * NT] = v[j];
+    const int lane = threadIdx.x % WAVE, w = threadIdx.x / WAVE;
+    const int npiece = (A.wbytes + 1023) / 1024;
+    for (int i = w; i < npiece; i += NT / WAVE) {
+      const int off = min(i * 1024 + 16 * lane, A.wbytes - 16);
+      __builtin_amdgcn_global_load_lds(A.packed + off, smem + i * 1024, 16, 0, 0);
     }
     return;
   }
@@ -473,7 +479,7 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
   bf16_t* vc_wg = A.vcache ? A.vcache + int64_t(blockIdx.x) * A.n_layers * DM * A.tpad : nullptr;
 
   for (int64_t n = blockIdx.x; n < A.total; n += gridDim.x) {
-    __syncthreads();   // weights loaded; the previous candidate is done with the buffers
+    __syncthreads();   // the previous candidate is done with the buffers
     const int Tv = token_valid_len(A.s, n);
     float* out = A.out + n * 2 * DM;
     if (Tv == 0) {
@@ -498,6 +504,7 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
       }
       cvec[tid] = acc;
     }
+    wait_vm_all();     // this wave's share of the weights is in LDS (first candidate)
     __syncthreads();
     // running max of X W_pool^T over the wave's valid tokens: lane holds features 16 f + c16
     float pmax[4] = {-__builtin_inff(), -__builtin_inff(), -__builtin_inff(), -__builtin_inff()};
@@ -696,6 +703,7 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
       out[tid] = vmax(vmax(pool[tid], pool[DM + tid]), vmax(pool[2 * DM + tid], pool[3 * DM + tid])) +
                  A.b_pool[tid];
   }
+  wait_vm_all();   // no LDS-DMA outlives the workgroup (every candidate empty)
 }
 
 // The weights' LDS image: one workgroup per piece (a matrix or a vector).
