@@ -479,7 +479,10 @@ __global__ __launch_bounds__(NT) void encoder_small_kernel(Args A) {
   bf16_t* vc_wg = A.vcache ? A.vcache + int64_t(blockIdx.x) * A.n_layers * DM * A.tpad : nullptr;
 
   for (int64_t n = blockIdx.x; n < A.total; n += gridDim.x) {
-    __syncthreads();   // the previous candidate is done with the buffers
+    // the previous candidate is done with the buffers (no barrier before the
+    // first: a barrier waits for the weights' LDS-DMA, and the first candidate's
+    // metadata and operand loads go out while it is in flight)
+    if (n != blockIdx.x) __syncthreads();
     const int Tv = token_valid_len(A.s, n);
     float* out = A.out + n * 2 * DM;
     if (Tv == 0) {
