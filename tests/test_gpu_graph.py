@@ -14,11 +14,24 @@ from paper_2506_02267_amd import tav2 as T
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("k", [64, 256])   # one encoder block; two blocks (cached keys)
-def test_select_encode_graph_replays_match_eager(k):
-    w = synth.scaled(synth.SINGLE, L=3000, N=70, k=k)
+CASES = {
+    # d_model 256: one encoder block; two blocks (cached keys)
+    "single_k64": dict(base=synth.SINGLE, L=3000, N=70, k=64),
+    "single_k256": dict(base=synth.SINGLE, L=3000, N=70, k=256),
+    # the paper's encoder shape (d_model 64) behind the fused search (rows > 4096),
+    # with a real-time tail: three 64-position blocks
+    "paper": dict(base=synth.PAPER, L=6000, N=40),
+    # fp32 (the LDS-resident fp32 encoder)
+    "tiny_f32": dict(base=synth.TINY, L=900, N=12),
+}
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_select_encode_graph_replays_match_eager(case):
+    kw = dict(CASES[case])
+    w = synth.scaled(kw.pop("base"), **kw)
     inp = synth.make_inputs(w, seed=31)
-    print(f"graph capture L={w.L} N={w.N} k={k}", flush=True)
+    print(f"graph capture {case}: L={w.L} N={w.N} k={w.k} T={w.T}", flush=True)
     seq, rt, cands = upload(inp)
     call = T.SelectEncode(seq, rt, cands, w.k, T.DeviceWeights(synth.make_weights(w)))
     call()                                   # eager (also sets per-device kernel attributes)
