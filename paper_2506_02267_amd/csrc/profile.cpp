@@ -32,8 +32,10 @@ hipEvent_t take_event() {
     g_free.pop_back();
     return e;
   }
+  // timing only: no system-scope fence (and its cache writeback) at each record,
+  // which would otherwise slow the work around the timed launches
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
