@@ -305,11 +305,15 @@ __device__ __forceinline__ void resid_phase(f32x16 (&acc)[2][4], Pre& pre, const
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) xq[j + 1][tt] = bias_ones();
     }
+    // token tile by token tile: each tile's operand is last read two products into
+    // the k-block rather than six, which leaves the register allocator more room
+    {
+      const bf16x8 a0 = stream_frag<Cur>(wq, pre, j, 0), a1 = stream_frag<Cur>(wq, pre, j, 1);
 #pragma unroll
-    for (int ft = 0; ft < 2; ++ft) {
-      const bf16x8 a = stream_frag<Cur>(wq, pre, j, ft);
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt) acc[ft][tt] = mfma32(a, xq[j][tt], acc[ft][tt]);
+      for (int tt = 0; tt < 4; ++tt) {
+        acc[0][tt] = mfma32(a0, xq[j][tt], acc[0][tt]);
+        acc[1][tt] = mfma32(a1, xq[j][tt], acc[1][tt]);
+      }
     }
     side.step(j);
     stream_fetch<Cur, Nxt>(wq, pre, cur, nxt, j, lane);
@@ -990,12 +994,13 @@ __device__ __forceinline__ void ffn1_phase(Pre& pre, const WSeg& cur, const WSeg
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) xq[j + 1][tt] = bias_ones();
     }
+    {   // token tile by token tile (as in resid_phase)
+      const bf16x8 a0 = stream_frag<ShF1>(wq, pre, j, 0), a1 = stream_frag<ShF1>(wq, pre, j, 1);
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const bf16x8 a = stream_frag<ShF1>(wq, pre, j, t);
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt)
-        ha[t][tt] = mfma32(a, xq[j][tt], j == 0 ? f32x16{} : ha[t][tt]);
+      for (int tt = 0; tt < 4; ++tt) {
+        ha[0][tt] = mfma32(a0, xq[j][tt], j == 0 ? f32x16{} : ha[0][tt]);
+        ha[1][tt] = mfma32(a1, xq[j][tt], j == 0 ? f32x16{} : ha[1][tt]);
+      }
     }
     stream_fetch<ShF1, Nxt>(wq, pre, cur, nxt, j, lane);
     sched_fence();
