@@ -546,11 +546,11 @@ __device__ __forceinline__ void attn_init(AttnState<DH>& st, const bf16_t* Qs, i
 }
 
 // One segment of up to 128 keys of K (LDS [key][kld], head dims at col0) and V^T
-// (LDS [dim][vld]) for the wave's two query tiles qa and qb, which see NPA and NPB
-// pairs of 32 keys: S^T for the whole segment first, one row max and one rescale
-// of l and O per segment, then P and O^T += V^T P^T per pair.  The pair counts are
-// template parameters, so both tiles' work is one branch-free block the scheduler
-// can interleave.  S^T tile 2 kp + t holds keys 32 kp + 16 t + 4 gq + i; the P^T
+// (LDS [dim][vld]) for each of the wave's two query tiles qa and qb, which see NPA
+// and NPB pairs of 32 keys: S^T for the whole segment first, one row max and one
+// rescale of l and O per segment, then P and O^T += V^T P^T per pair.  The pair
+// counts are template parameters, so a tile's work is one branch-free block.
+// S^T tile 2 kp + t holds keys 32 kp + 16 t + 4 gq + i; the P^T
 // fragment of pair kp takes them in that order (keys 4gq.., then 16 + 4gq..), and
 // V^T rows store each pair's keys in the same order (vpos), so a lane's V^T
 // fragment is one 16-byte read.  exp2 is the hardware instruction (results below 2^-126
@@ -653,51 +653,44 @@ __device__ __forceinline__ bf16x8 seg_probs(const f32x4v (&s)[8], int kp, float 
   }
   return pb;
 }
-// O^T += V^T P^T for both tiles, pair by pair: each V^T fragment is read once for
-// the two tiles, the next pair's while this pair's probabilities are computed.
-// vf enters holding pair 0 (read after the S products: read before them, its
-// registers make the compiler serialize the K reads).
-template <int DH, int DQA, int DQB, int NPA, int NPB>
-__device__ __forceinline__ void seg_pv2(AttnState<DH>& sa, AttnState<DH>& sb,
-                                        const f32x4v (&s_a)[8], const f32x4v (&s_b)[8], float ma,
-                                        float mb, bf16x8 (&vf)[DH / 16], const bf16_t* Vl,
-                                        int vld, int col0, int lane) {
-  constexpr int NP = NPA > NPB ? NPA : NPB;
-  float psa = 0.f, psb = 0.f;
+// One query tile's segment: S^T, one rescale, then per pair P^T and O^T += V^T P^T,
+// the next pair's V^T fragments read while this pair's probabilities are computed
+// (vf is first read after the S products: read before them, its registers make the
+// compiler serialize the K reads).
+template <int DH, int DQ, int NP, bool FIRST>
+__device__ __forceinline__ void attn_segment1(AttnState<DH>& st, const bf16_t* Kl, int kld,
+                                              const bf16_t* Vl, int vld, int col0, int lane,
+                                              int kvl = 0) {
+  f32x4v sc[8];
+  bf16x8 vf[DH / 16];
+  seg_scores<DH, DQ, NP>(sc, st, Kl, kld, col0, lane, kvl);
+  v_frags<DH>(vf, Vl, vld, col0, 0, lane);
+  const float m = seg_rescale<DH, DQ, NP, FIRST>(st, sc);
+  float ps = 0.f;
 #pragma unroll
   for (int kp = 0; kp < NP; ++kp) {
     bf16x8 vn[DH / 16];
     if (kp + 1 < NP) v_frags<DH>(vn, Vl, vld, col0, kp + 1, lane);
-    if (kp < NPA) {
-      const bf16x8 pb = seg_probs<DH, DQA, NPA>(s_a, kp, ma, psa);
+    const bf16x8 pb = seg_probs<DH, DQ, NP>(sc, kp, m, ps);
 #pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) sa.o[dt] = mfma16(vf[dt], pb, sa.o[dt]);
-    }
-    if (kp < NPB) {
-      const bf16x8 pb = seg_probs<DH, DQB, NPB>(s_b, kp, mb, psb);
-#pragma unroll
-      for (int dt = 0; dt < DH / 16; ++dt) sb.o[dt] = mfma16(vf[dt], pb, sb.o[dt]);
-    }
+    for (int dt = 0; dt < DH / 16; ++dt) st.o[dt] = mfma16(vf[dt], pb, st.o[dt]);
     if (kp + 1 < NP) {
 #pragma unroll
       for (int dt = 0; dt < DH / 16; ++dt) vf[dt] = vn[dt];
     }
   }
-  sa.l += psa;
-  sb.l += psb;
+  st.l += ps;
 }
+// The wave's two query tiles one after the other (both at once keeps twice the
+// score and output registers live, which pushes the residual stream into
+// accumulator registers and back around every segment; in turn each tile reads
+// the segment's V^T fragments itself).
 template <int DH, int DQA, int DQB, int NPA, int NPB, bool FIRST>
 __device__ __forceinline__ void attn_segment2(AttnState<DH>& sa, AttnState<DH>& sb,
                                               const bf16_t* Kl, int kld, const bf16_t* Vl,
                                               int vld, int col0, int lane, int kvl = 0) {
-  f32x4v s_a[8], s_b[8];
-  bf16x8 vf[DH / 16];
-  seg_scores<DH, DQA, NPA>(s_a, sa, Kl, kld, col0, lane, kvl);
-  seg_scores<DH, DQB, NPB>(s_b, sb, Kl, kld, col0, lane, kvl);
-  v_frags<DH>(vf, Vl, vld, col0, 0, lane);
-  const float ma = seg_rescale<DH, DQA, NPA, FIRST>(sa, s_a);
-  const float mb = seg_rescale<DH, DQB, NPB, FIRST>(sb, s_b);
-  seg_pv2<DH, DQA, DQB, NPA, NPB>(sa, sb, s_a, s_b, ma, mb, vf, Vl, vld, col0, lane);
+  attn_segment1<DH, DQA, NPA, FIRST>(sa, Kl, kld, Vl, vld, col0, lane, kvl);
+  attn_segment1<DH, DQB, NPB, FIRST>(sb, Kl, kld, Vl, vld, col0, lane, kvl);
 }
 // The block's own keys for wave W: tiles W and 7 - W see W / 2 + 1 and
 // (7 - W) / 2 + 1 pairs.
