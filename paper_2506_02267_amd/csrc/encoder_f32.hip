@@ -152,9 +152,28 @@ __device__ __forceinline__ void gemm_lds(float (&acc)[RI][CJ], const float* A, i
   }
 }
 
-// acc[i][j] += sum_{k < K} A[r][k] W[c][k]: A in LDS, the weight matrix W
-// ([N][K] with row stride ldw, N <= NB) staged through the LDS chunk Ws, 2^ks k
-// at a time (coalesced along k, stored transposed).  Starts with a barrier
+// One staged chunk of a weight matrix W ([N][K] with row stride ldw, N <= NB) in
+// registers: the thread's 16-byte pieces (4 consecutive k of one column) e = tid +
+// NT q, column e / (kc / 4), k 4 (e % (kc / 4)).  K, ldw and the column offsets are
+// multiples of 4, so a piece is all inside or all past K.
+struct WChunk {
+  float4 v[SPT / 4];
+};
+__device__ __forceinline__ void w_fetch(WChunk& st, const float* __restrict__ W, int ldw, int N,
+                                        int K, int k0, int ks) {
+  const int tid = threadIdx.x, ks4 = ks - 2, spt = ((1 << ks) * NB) / (4 * NT);
+#pragma unroll
+  for (int q = 0; q < SPT / 4; ++q) {
+    const int e = tid + NT * q, c = e >> ks4, kk = (e & ((1 << ks4) - 1)) * 4;
+    st.v[q] = (q < spt && c < N && k0 + kk < K)
+                  ? *reinterpret_cast<const float4*>(W + c * ldw + k0 + kk)
+                  : make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+}
+
+// acc[i][j] += sum_{k < K} A[r][k] W[c][k]: A in LDS, W staged through the LDS
+// chunk Ws, 2^ks k at a time (coalesced along k, stored transposed), each chunk's
+// loads in flight while the one before is multiplied.  Starts with a barrier
 // (earlier readers of Ws and of anything the caller writes before calling are
 // done) and ends without one.
 template <int RI, int CJ>
@@ -162,23 +181,23 @@ __device__ __forceinline__ void gemm_w(float (&acc)[RI][CJ], const float* A, int
                                        int K, const float* __restrict__ W, int ldw, int N,
                                        float* Ws, int ks) {
   const int tid = threadIdx.x;
-  const int kc_full = 1 << ks, spt = (kc_full * NB) / NT;
+  WChunk st;
+  w_fetch(st, W, ldw, N, K, 0, ks);
+  const int kc_full = 1 << ks, spt = (kc_full * NB) / (4 * NT), ks4 = ks - 2;
   for (int k0 = 0; k0 < K; k0 += kc_full) {
     __syncthreads();
-    {
-      float st[SPT];
 #pragma unroll
-      for (int q = 0; q < SPT; ++q) {
-        const int e = tid + NT * q, c = e >> ks, kk = e & (kc_full - 1);
-        st[q] = (q < spt && c < N && k0 + kk < K) ? W[c * ldw + k0 + kk] : 0.f;
-      }
-#pragma unroll
-      for (int q = 0; q < SPT; ++q) {
-        const int e = tid + NT * q, c = e >> ks, kk = e & (kc_full - 1);
-        if (q < spt && c < N) Ws[kk * WS_LD + c] = st[q];
+    for (int q = 0; q < SPT / 4; ++q) {
+      const int e = tid + NT * q, c = e >> ks4, kk = (e & ((1 << ks4) - 1)) * 4;
+      if (q < spt && c < N) {
+        Ws[kk * WS_LD + c] = st.v[q].x;
+        Ws[(kk + 1) * WS_LD + c] = st.v[q].y;
+        Ws[(kk + 2) * WS_LD + c] = st.v[q].z;
+        Ws[(kk + 3) * WS_LD + c] = st.v[q].w;
       }
     }
     __syncthreads();
+    if (k0 + kc_full < K) w_fetch(st, W, ldw, N, K, k0 + kc_full, ks);
     const int kc = K - k0 < kc_full ? K - k0 : kc_full;
     gemm_lds<RI, CJ>(acc, A + k0, lda, rows, kc, Ws, WS_LD);
   }
@@ -423,7 +442,7 @@ __global__ __launch_bounds__(NT) void encode_f32_kernel(Args a) {
         float acc1[RI][2];
         zero<RI, 2>(acc1);
         gemm_w<RI, 2>(acc1, X, a.ldx, Tv, dm, static_cast<const float*>(L.W_1) + int64_t(c0) * dm, dm,
-                  nc, Ws, a.kc_shift);
+                      nc, Ws, a.kc_shift);
 #pragma unroll
         for (int i = 0; i < RI; ++i) {
           const int r = w + NW * i;
@@ -435,7 +454,8 @@ __global__ __launch_bounds__(NT) void encode_f32_kernel(Args a) {
             }
           }
         }
-        gemm_w<RI, 2>(acc2, QV, a.ldh, Tv, nc, static_cast<const float*>(L.W_2) + c0, a.ffn, dm, Ws, a.kc_shift);
+        gemm_w<RI, 2>(acc2, QV, a.ldh, Tv, nc, static_cast<const float*>(L.W_2) + c0, a.ffn, dm, Ws,
+                      a.kc_shift);
       }
       __syncthreads();   // every wave is past its reads of X's rows
       add_norm<RI>(acc2, X, a.ldx, Tv, dm, L.b_2, L.ln2_g, L.ln2_b);
