@@ -328,7 +328,8 @@ tav2_status tav2_select_encode_eq2(const tav2_seq* seq, const tav2_eq2* eq2,
  * Measurement hook for benchmarks and profilers (not needed for serving).
  * tav2_profile_enable(1, site) makes every later kernel launch of the library
  * whose site name equals `site` (NULL: every site) record a HIP event before
- * and after itself on its stream; tav2_profile_enable(0, NULL) stops it.
+ * and after itself on its stream (timing-only events, without a system-scope
+ * fence); tav2_profile_enable(0, NULL) stops it.
  * After the caller has synchronised, tav2_profile_report() writes one line
  * "<site> <launches> <total_ms>" per site into buf (NUL-terminated, truncated
  * to buf_bytes), forgets the recorded launches and returns the untruncated
@@ -336,7 +337,7 @@ tav2_status tav2_select_encode_eq2(const tav2_seq* seq, const tav2_eq2* eq2,
  * nn_fallback (the NN search with on-chip scores, for bf16 and int8 sequences of
  * more than 4096 rows), score_bf16, score_i8, score_f32, topk (the NN search over
  * materialised score rows), gather, pack_weights, cand_proj, encoder_fused (the
- * bf16 encoder), encode_f32.
+ * bf16 encoder of d_model 256), encoder_small (d_model 64), encode_f32.
  */
 int32_t tav2_profile_enable(int32_t on, const char* only_site);
 int64_t tav2_profile_report(char* buf, size_t buf_bytes);
