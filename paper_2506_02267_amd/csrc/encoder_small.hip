@@ -374,9 +374,13 @@ __device__ __forceinline__ void att_pair(Att<DH>& st, const Pair<DH>& f, int lim
 // then the p0 keys of earlier blocks from the cache, one 32-key pair at a time
 // staged in LDS by the whole workgroup (each key is read from the cache once per
 // workgroup, not once per wave); the loads of the next two pairs are in flight
-// while a pair is computed.  Leaves O = softmax(S) V in the Q rows.
+// while a pair is computed.  The stage alternates between Kst / Vst and the
+// block's own K / V^T rows (free once every wave is past the block's own keys,
+// i.e. after the first pair's barrier), so one barrier per pair orders both the
+// stage's writes before its reads and its reads two pairs earlier before its
+// rewrite.  Leaves O = softmax(S) V in the Q rows.
 template <int DH>
-__device__ __forceinline__ void attend(bf16_t* Qs, const bf16_t* Ks, const bf16_t* Vts,
+__device__ __forceinline__ void attend(bf16_t* Qs, bf16_t* Ks, bf16_t* Vts,
                                        const bf16_t* kc, const bf16_t* vc, int tpad, int p0,
                                        int nkv, bool unmasked, bf16_t* Kst, bf16_t* Vst) {
   constexpr int NH = DM / DH;
@@ -420,15 +424,16 @@ __device__ __forceinline__ void attend(bf16_t* Qs, const bf16_t* Ks, const bf16_
   }
   // earlier blocks: every key visible
   auto step = [&](const uint4& kr, const uint4& vr, uint4& kn, uint4& vn, int c) {
-    __syncthreads();   // every wave is done with the previous pair
-    *reinterpret_cast<uint4*>(Kst + kkey * RLD + kcol) = kr;
-    *reinterpret_cast<uint4*>(Vst + vdim * SLD + vcol) = vr;
+    bf16_t* ks = (c & 1) ? Ks : Kst;
+    bf16_t* vs = (c & 1) ? Vts : Vst;
+    *reinterpret_cast<uint4*>(ks + kkey * RLD + kcol) = kr;
+    *reinterpret_cast<uint4*>(vs + vdim * SLD + vcol) = vr;
     __syncthreads();
     fetch(kn, vn, c + 2);
 #pragma unroll
     for (int h = 0; h < NH; ++h) {
       Pair<DH> f;
-      load_pair<DH>(f, Kst, RLD, Vst, SLD, h * DH);
+      load_pair<DH>(f, ks, RLD, vs, SLD, h * DH);
       att_pair<DH>(st[h], f, 32, scale_l2);
     }
   };
